@@ -1,0 +1,264 @@
+/*
+ * jfkv.h -- C ABI of libjfkv.so: attention executed directly over a
+ * group-wise 4-bit quantized, paged KV cache on AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow the KVExec component of "JustFit: Just-in-Time State
+ * Management for Local LLM Serving":
+ *   - a fixed backing pool of 256-token pages, a per-request page table that
+ *     maps token order to pages, page IDs returned to a free list on
+ *     completion (Background, "Compact histories need reusable storage");
+ *   - reference-counted pages shared by requests with a common prefix and
+ *     all-or-nothing page reservation (Sec. 3.3, eq. reservation and the
+ *     refcounted shared prefixes it describes; Algorithm 1 recycles
+ *     zero-reference pages after releasing a request);
+ *   - single-query decode that reads the compressed pages directly, and
+ *     prefill that consumes the same pages as floating operands (Sec. 3.1,
+ *     "Decode and prefill need different kernels"); query heads grouped
+ *     over shared KV heads, each head independent (eq. groupattention);
+ *   - bounded temporary storage: the decode workspace has a size fixed by
+ *     the caller's split cap, independent of context length (Sec. 3.1,
+ *     "Finish one head group ..." motivates bounding workspace; eq.
+ *     layerbytes is what the fused prefill avoids materializing).
+ * Stored format: affine 4-bit codes with one fp16 scale and one fp16 bias
+ * per group of head_dim elements (the affine Q4 format named in the
+ * Introduction, "Four-bit (Q4) weights ..."), eight codes per 32-bit word
+ * (Appendix A, Table codec, per-vector storage).
+ *
+ * ---------------------------------------------------------------------
+ * Pool byte layout (per layer; one set for K and one for V):
+ *   k_codes  uint8 [NP][Hkv][P][d/2]          byte j of a position's row =
+ *                                             code(2j) | code(2j+1) << 4
+ *   v_codes  uint8 [NP][Hkv][P/2][d/4][2][2]  positions paired (2s, 2s+1):
+ *                                             dims 4u..4u+3 of slot t are the
+ *                                             2 bytes at ((t/2)*(d/4)+u)*4 +
+ *                                             (t%2)*2, holding code(4u) |
+ *                                             code(4u+1)<<4 and code(4u+2) |
+ *                                             code(4u+3)<<4
+ *   k_meta, v_meta  fp16 [NP][Hkv][P][d/G][2]  (scale, bias) per group
+ * Bytes per position per layer: 2*Hkv*(d/2 + 4*d/G) (1,152 at Hkv=8,
+ * d=128, G=64).
+ *
+ * Quantizer (bit-exact contract), per group x_0..x_{G-1} of fp16 values:
+ *   mn, mx   = min, max (binary32; -0 orders below +0)
+ *   bias     = fp16 of mn rounded toward -inf
+ *   range    = mx - mn; step = range / 15  (binary32, IEEE round-to-nearest)
+ *   scale    = fp16 of step rounded toward +inf; +0 when range == 0
+ *   code_i   = 0 if scale == 0, else clamp(rint((x_i - bias) / scale), 0, 15)
+ *              with the subtraction and division separate binary32 ops and
+ *              rint rounding half to even
+ *   x^_i     = scale * code_i + bias
+ * Inputs must be finite.
+ *
+ * ---------------------------------------------------------------------
+ * Conventions for every entry point:
+ *   - Every function returns jf_status; no C++ exception crosses the ABI.
+ *   - Arguments are validated before anything is launched; a call that
+ *     fails validation has no side effect.  jf_last_error() then returns a
+ *     message (thread-local; valid until the next jf_* call on the thread).
+ *   - Device pointers are caller-owned (allocated by the caller, e.g. by
+ *     PyTorch); the library never allocates or frees device memory.  Device
+ *     work is enqueued asynchronously on the given stream (NULL = the
+ *     default stream); faults inside kernels surface at the caller's next
+ *     synchronization.  A launch failure returns JF_ERR_DEVICE.
+ *   - Host page-pool objects are owned by the library from _create until
+ *     _destroy and are not thread-safe: callers serialize calls per pool.
+ *   - GQA mapping: query head h reads KV head h / (num_q_heads / Hkv).
+ */
+#ifndef JFKV_H
+#define JFKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  JF_OK = 0,
+  JF_ERR_INVALID = 1,     /* bad argument (NULL, shape, range)               */
+  JF_ERR_NO_PAGES = 2,    /* page reservation could not be satisfied         */
+  JF_ERR_DEVICE = 3,      /* HIP launch or runtime error                     */
+  JF_ERR_UNSUPPORTED = 4, /* valid but not implemented geometry              */
+  JF_ERR_STATE = 5        /* operation not allowed in the object's state     */
+} jf_status;
+
+/* Message for the last failing jf_* call on this thread ("" if none). */
+const char* jf_last_error(void);
+
+/* Library version string. */
+const char* jf_version(void);
+
+/* Pool geometry.  Supported: page_size a multiple of 64 (256 in the paper's
+ * geometry); head_dim 64, 128 or 256; group_size 32, 64 or 128 dividing
+ * head_dim; num_kv_heads >= 1; num_pages >= 1. */
+typedef struct {
+  int32_t page_size;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t group_size;
+  int32_t num_pages;
+} jf_kv_layout;
+
+/* Device pointers to one layer's pools (layout above). */
+typedef struct {
+  void* k_codes;
+  void* k_meta;
+  void* v_codes;
+  void* v_meta;
+} jf_kv_pool_ptrs;
+
+/* Bytes of one codes array and of one meta array for the layout (the same
+ * for K and V).  Errors: JF_ERR_INVALID / JF_ERR_UNSUPPORTED for bad
+ * geometry or NULL outputs. */
+jf_status jf_kv_pool_bytes(const jf_kv_layout* layout, size_t* codes_bytes,
+                           size_t* meta_bytes);
+
+/* ---------------------------------------------------------------------
+ * Host page allocator and per-request page tables (paging: Background,
+ * "Compact histories need reusable storage"; shared prefixes and
+ * reservation: eq. reservation; recycling: Algorithm 1).
+ * ------------------------------------------------------------------- */
+typedef struct jf_page_pool jf_page_pool;
+
+/* Create a pool of num_pages page IDs.  The free list is a stack; with
+ * shuffle_seed != 0 its initial order is a seeded permutation (so
+ * consecutive reservations receive non-contiguous physical pages), with 0
+ * pages are handed out in increasing order.  *out receives the pool. */
+jf_status jf_page_table_pool_create(int32_t num_pages, int32_t page_size,
+                                    uint64_t shuffle_seed, jf_page_pool** out);
+jf_status jf_page_table_pool_destroy(jf_page_pool* pool);
+
+/* New empty request (length 0, no pages); *seq receives its handle. */
+jf_status jf_page_table_create(jf_page_pool* pool, int32_t* seq);
+
+/* New request that shares (copy-free, reference count + 1) the first
+ * prefix_len positions of src.  prefix_len must be a multiple of page_size
+ * and at most src's length, so the new request's next write lands on a page
+ * of its own.  Its length starts at prefix_len. */
+jf_status jf_page_table_fork(jf_page_pool* pool, int32_t src,
+                             int32_t prefix_len, int32_t* seq);
+
+/* Append the n given free pages to seq's page list (explicit placement,
+ * e.g. a reversed or shuffled mapping).  JF_ERR_STATE if any is not free
+ * or listed twice; nothing changes then. */
+jf_status jf_page_table_assign(jf_page_pool* pool, int32_t seq,
+                               const int32_t* page_ids, int32_t n);
+
+/* Ensure seq owns ceil(new_len / page_size) pages, taking missing ones from
+ * the free list; all or nothing (JF_ERR_NO_PAGES leaves seq unchanged).
+ * JF_ERR_STATE if positions length..new_len-1 would fall on a page whose
+ * reference count is above one (shared pages are read-only). */
+jf_status jf_page_table_reserve(jf_page_pool* pool, int32_t seq,
+                                int32_t new_len);
+
+/* Commit seq's length after its rows were appended; len must not exceed
+ * its page capacity. */
+jf_status jf_page_table_set_length(jf_page_pool* pool, int32_t seq,
+                                   int32_t len);
+
+/* Drop seq: each of its pages loses one reference; pages reaching zero go
+ * back on the free list (last released, first reused).  The handle becomes
+ * invalid (JF_ERR_STATE on reuse). */
+jf_status jf_page_table_release(jf_page_pool* pool, int32_t seq);
+
+/* Write the page tables of n requests as a host block table
+ * [n][max_pages] (unused entries -1) and their lengths [n].  JF_ERR_INVALID
+ * if a request has more than max_pages pages. */
+jf_status jf_page_table_export(const jf_page_pool* pool, const int32_t* seqs,
+                               int32_t n, int32_t max_pages,
+                               int32_t* block_table, int32_t* lens);
+
+/* Pages currently free, in use (reference count > 0), and the most pages
+ * ever in use at once. */
+jf_status jf_page_table_stats(const jf_page_pool* pool, int32_t* free_pages,
+                              int32_t* used_pages, int32_t* high_water);
+
+/* Number of pages of seq and its committed length. */
+jf_status jf_page_table_info(const jf_page_pool* pool, int32_t seq,
+                             int32_t* n_pages, int32_t* length);
+
+/* ---------------------------------------------------------------------
+ * Device work.
+ * ------------------------------------------------------------------- */
+
+/* Quantize rows of new K and V and write them into their pages (the
+ * "pending cache writes" a step finishes before its pages may be released,
+ * Algorithm 1).
+ *   k_new, v_new  fp16 [total_tok][Hkv][d] (device), rows of all requests
+ *                 concatenated;
+ *   cu_tok        int32 [B+1] (device) row offsets: request b owns rows
+ *                 cu_tok[b] .. cu_tok[b+1]-1, total_tok == cu_tok[B];
+ *   start_pos     int32 [B] (device) logical position of each request's
+ *                 first new row;
+ *   block_tables  int32 [B][max_pages] (device) physical page of each
+ *                 logical page.
+ * Rows whose logical page is beyond max_pages or whose page ID is outside
+ * [0, num_pages) are skipped (nothing is written for them).  The pages must
+ * have been reserved and not be shared.  Codes, scales and biases are
+ * bit-exact with the quantizer contract above. */
+jf_status jf_kv_quantize_append(const jf_kv_layout* layout,
+                                const jf_kv_pool_ptrs* pool,
+                                const void* k_new, const void* v_new,
+                                const int32_t* cu_tok,
+                                const int32_t* start_pos,
+                                const int32_t* block_tables, int32_t B,
+                                int32_t max_pages, int32_t total_tok,
+                                hipStream_t stream);
+
+/* Workspace bytes jf_decode_attn_q4 needs: B * num_q_heads * max_splits *
+ * (head_dim + 2) * 4.  It does not depend on sequence lengths. */
+jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads,
+                                    int32_t head_dim, int32_t max_splits,
+                                    size_t* bytes);
+
+/* Single-query decode attention over the paged 4-bit cache (split-K with a
+ * log-sum-exp combine).
+ *   q            fp16 [B][num_q_heads][d] (device)
+ *   block_tables int32 [B][max_pages] (device)
+ *   seq_lens     int32 [B] (device): request b attends to its logical
+ *                positions 0..seq_lens[b]-1 (append first, then attend);
+ *                values above max_pages*page_size are clamped; a request
+ *                with length <= 0 gets an all-zero output row
+ *   softmax_scale  logits = softmax_scale * q . k
+ *   max_splits   cap on partials per request and KV head (1..1024); a
+ *                request with n pages uses min(max_splits, n) page-aligned
+ *                splits of equal page counts, the remainder on the first
+ *   workspace    device scratch of at least jf_decode_workspace_bytes()
+ *   out          fp16 [B][num_q_heads][d] (device)
+ * Page IDs outside [0, num_pages) are never dereferenced; the positions
+ * they would hold do not contribute. */
+jf_status jf_decode_attn_q4(const jf_kv_layout* layout,
+                            const jf_kv_pool_ptrs* pool, const void* q,
+                            int32_t B, int32_t num_q_heads,
+                            const int32_t* block_tables, int32_t max_pages,
+                            const int32_t* seq_lens, float softmax_scale,
+                            int32_t max_splits, void* workspace,
+                            size_t workspace_bytes, void* out,
+                            hipStream_t stream);
+
+/* Chunked-prefill attention for one request: query i of the chunk sits at
+ * absolute position prefix_len + i and attends to the dequantized prefix
+ * positions 0..prefix_len-1 (through block_table) and, causally, to the
+ * chunk's own fp16 rows 0..i.  The chunk is not written to the pool here:
+ * call jf_kv_quantize_append afterwards.
+ *   q        fp16 [T][num_q_heads][d] (device)
+ *   k_chunk, v_chunk  fp16 [T][Hkv][d] (device)
+ *   block_table  int32 [max_pages] (device); pages 0..ceil(prefix_len/P)-1
+ *                are read; prefix_len must be <= max_pages * page_size
+ *   out      fp16 [T][num_q_heads][d] (device)
+ * Products run on bf16 matrix cores with fp32 accumulation. */
+jf_status jf_prefill_attn_q4(const jf_kv_layout* layout,
+                             const jf_kv_pool_ptrs* pool, const void* q,
+                             const void* k_chunk, const void* v_chunk,
+                             int32_t T, int32_t num_q_heads,
+                             const int32_t* block_table, int32_t max_pages,
+                             int32_t prefix_len, float softmax_scale,
+                             void* out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* JFKV_H */

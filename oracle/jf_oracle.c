@@ -101,7 +101,7 @@ static float half_to_float(uint16_t h) { return (float)jfo_half_to_double(h); }
 
 /* ------------------------------------------------------------------------
  * Group quantizer.  For one group x_0..x_{G-1} (fp16, finite):
- *   1. mn, mx: exact minimum and maximum in binary32.
+ *   1. mn, mx: exact minimum and maximum in binary32 (-0 below +0).
  *   2. bias  = fp16(mn) rounded toward -inf (exact for fp16 inputs).
  *   3. range = mx - mn; step = range / 15 (binary32, round to nearest);
  *      scale = fp16(step) rounded toward +inf (+0 when range is 0).
@@ -113,11 +113,12 @@ static float half_to_float(uint16_t h) { return (float)jfo_half_to_double(h); }
  * ---------------------------------------------------------------------- */
 void jfo_quantize_group(const uint16_t* x, int32_t G, uint8_t* codes,
                         uint16_t* scale, uint16_t* bias) {
+  /* -0 orders below +0, so the result does not depend on element order */
   float mn = half_to_float(x[0]), mx = mn;
   for (int32_t i = 1; i < G; ++i) {
     float v = half_to_float(x[i]);
-    if (v < mn) mn = v;
-    if (v > mx) mx = v;
+    if (v < mn || (v == mn && signbit(v) && !signbit(mn))) mn = v;
+    if (v > mx || (v == mx && !signbit(v) && signbit(mx))) mx = v;
   }
   uint16_t b16 = jfo_float_to_half(mn, 1);
   volatile float range = mx - mn;

@@ -1,0 +1,436 @@
+// Host side of libjfkv.so: error reporting, argument validation, the page
+// allocator with per-request page tables, and dispatch to the kernels.
+//
+// Paging follows the paper's Background paragraph "Compact histories need
+// reusable storage" (fixed pool of 256-token pages, a page table per
+// request, page IDs returned on completion); shared prefixes hold reference
+// counts and reservation is all-or-nothing (Sec. 3.3, eq. reservation);
+// releasing a request recycles its zero-reference pages (Algorithm 1).
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "jfkv_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+jf_status fail(jf_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+jf_status ok() {
+  g_last_error.clear();
+  return JF_OK;
+}
+
+jf_status device_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(JF_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+jf_status check_layout(const jf_kv_layout* L) {
+  if (!L) return fail(JF_ERR_INVALID, "layout is NULL");
+  if (L->page_size <= 0 || L->num_kv_heads <= 0 || L->head_dim <= 0 ||
+      L->group_size <= 0 || L->num_pages <= 0)
+    return fail(JF_ERR_INVALID, "layout fields must be positive");
+  if (L->head_dim % L->group_size)
+    return fail(JF_ERR_INVALID, "head_dim %d is not a multiple of group_size %d",
+                L->head_dim, L->group_size);
+  if (!jfkv::geometry_supported(*L))
+    return fail(JF_ERR_UNSUPPORTED,
+                "unsupported geometry (page_size %d must be a multiple of 64 and <= 4096, "
+                "head_dim %d in {64,128,256}, group_size %d in {32,64,128})",
+                L->page_size, L->head_dim, L->group_size);
+  return JF_OK;
+}
+
+jf_status check_pool(const jf_kv_pool_ptrs* p) {
+  if (!p || !p->k_codes || !p->k_meta || !p->v_codes || !p->v_meta)
+    return fail(JF_ERR_INVALID, "pool pointers must be non-NULL");
+  return JF_OK;
+}
+
+// splitmix64 (Steele, Lea, Flood 2014): a small seeded generator for the
+// optional shuffled initial order of the free list.
+uint64_t splitmix64(uint64_t& s) {
+  uint64_t z = (s += 0x9e3779b97f4a7c15ull);
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+}  // namespace
+
+namespace jfkv {
+bool geometry_supported(const jf_kv_layout& L) {
+  bool d_ok = L.head_dim == 64 || L.head_dim == 128 || L.head_dim == 256;
+  bool g_ok = (L.group_size == 32 || L.group_size == 64 || L.group_size == 128) &&
+              L.group_size <= L.head_dim;
+  bool p_ok = L.page_size % 64 == 0 && L.page_size <= 4096;
+  return d_ok && g_ok && p_ok;
+}
+}  // namespace jfkv
+
+// ------------------------------------------------------------------ pool
+struct jf_page_pool {
+  struct Seq {
+    std::vector<int32_t> pages;
+    int32_t length = 0;
+    bool live = false;
+  };
+  int32_t num_pages = 0, page_size = 0;
+  std::vector<int32_t> free_stack;  // may hold stale entries; in_free is the truth
+  std::vector<uint8_t> in_free;
+  std::vector<int32_t> refcount;
+  int32_t n_free = 0, used = 0, high_water = 0;
+  std::vector<Seq> seqs;
+
+  int32_t pop_free() {
+    while (!free_stack.empty()) {
+      int32_t p = free_stack.back();
+      free_stack.pop_back();
+      if (in_free[p]) {
+        in_free[p] = 0;
+        --n_free;
+        return p;
+      }
+    }
+    return -1;
+  }
+  void push_free(int32_t p) {
+    in_free[p] = 1;
+    ++n_free;
+    free_stack.push_back(p);
+  }
+  void take_ref(int32_t p) {
+    if (refcount[p]++ == 0) {
+      ++used;
+      if (used > high_water) high_water = used;
+    }
+  }
+  void drop_ref(int32_t p) {
+    if (--refcount[p] == 0) {
+      --used;
+      push_free(p);
+    }
+  }
+  Seq* get(int32_t s) {
+    if (s < 0 || s >= (int32_t)seqs.size() || !seqs[s].live) return nullptr;
+    return &seqs[s];
+  }
+  const Seq* get(int32_t s) const {
+    if (s < 0 || s >= (int32_t)seqs.size() || !seqs[s].live) return nullptr;
+    return &seqs[s];
+  }
+  int32_t new_seq() {
+    seqs.emplace_back();
+    seqs.back().live = true;
+    return (int32_t)seqs.size() - 1;
+  }
+};
+
+extern "C" {
+
+const char* jf_last_error(void) { return g_last_error.c_str(); }
+
+const char* jf_version(void) { return "jfkv 0.1 (gfx950)"; }
+
+jf_status jf_kv_pool_bytes(const jf_kv_layout* layout, size_t* codes_bytes,
+                           size_t* meta_bytes) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if (!codes_bytes || !meta_bytes) return fail(JF_ERR_INVALID, "NULL output");
+  size_t per = (size_t)layout->num_pages * layout->num_kv_heads * layout->page_size;
+  *codes_bytes = per * (size_t)(layout->head_dim / 2);
+  *meta_bytes = per * (size_t)(layout->head_dim / layout->group_size) * 2 * sizeof(uint16_t);
+  return ok();
+}
+
+jf_status jf_page_table_pool_create(int32_t num_pages, int32_t page_size,
+                                    uint64_t shuffle_seed, jf_page_pool** out) {
+  if (!out) return fail(JF_ERR_INVALID, "out is NULL");
+  if (num_pages <= 0 || page_size <= 0)
+    return fail(JF_ERR_INVALID, "num_pages and page_size must be positive");
+  jf_page_pool* p = new (std::nothrow) jf_page_pool;
+  if (!p) return fail(JF_ERR_INVALID, "out of host memory");
+  try {
+    p->num_pages = num_pages;
+    p->page_size = page_size;
+    p->in_free.assign(num_pages, 1);
+    p->refcount.assign(num_pages, 0);
+    std::vector<int32_t> order(num_pages);
+    for (int32_t i = 0; i < num_pages; ++i) order[i] = i;
+    if (shuffle_seed) {
+      uint64_t s = shuffle_seed;
+      for (int32_t i = num_pages - 1; i > 0; --i) {  // Fisher-Yates
+        int32_t j = (int32_t)(splitmix64(s) % (uint64_t)(i + 1));
+        std::swap(order[i], order[j]);
+      }
+    }
+    // the stack pops from the back: hand pages out in `order`
+    p->free_stack.assign(order.rbegin(), order.rend());
+    p->n_free = num_pages;
+  } catch (...) {
+    delete p;
+    return fail(JF_ERR_INVALID, "out of host memory");
+  }
+  *out = p;
+  return ok();
+}
+
+jf_status jf_page_table_pool_destroy(jf_page_pool* pool) {
+  if (!pool) return fail(JF_ERR_INVALID, "pool is NULL");
+  delete pool;
+  return ok();
+}
+
+jf_status jf_page_table_create(jf_page_pool* pool, int32_t* seq) {
+  if (!pool || !seq) return fail(JF_ERR_INVALID, "NULL argument");
+  *seq = pool->new_seq();
+  return ok();
+}
+
+jf_status jf_page_table_fork(jf_page_pool* pool, int32_t src, int32_t prefix_len,
+                             int32_t* seq) {
+  if (!pool || !seq) return fail(JF_ERR_INVALID, "NULL argument");
+  const jf_page_pool::Seq* s = pool->get(src);
+  if (!s) return fail(JF_ERR_STATE, "fork: unknown or released request %d", src);
+  if (prefix_len < 0 || prefix_len % pool->page_size || prefix_len > s->length)
+    return fail(JF_ERR_INVALID,
+                "fork: prefix_len %d must be a multiple of page_size %d and <= length %d",
+                prefix_len, pool->page_size, s->length);
+  int32_t np = prefix_len / pool->page_size;
+  std::vector<int32_t> pages(s->pages.begin(), s->pages.begin() + np);
+  int32_t id = pool->new_seq();
+  for (int32_t pg : pages) pool->take_ref(pg);
+  pool->seqs[id].pages = std::move(pages);
+  pool->seqs[id].length = prefix_len;
+  *seq = id;
+  return ok();
+}
+
+jf_status jf_page_table_assign(jf_page_pool* pool, int32_t seq, const int32_t* page_ids,
+                               int32_t n) {
+  if (!pool || (n > 0 && !page_ids) || n < 0) return fail(JF_ERR_INVALID, "bad argument");
+  jf_page_pool::Seq* s = pool->get(seq);
+  if (!s) return fail(JF_ERR_STATE, "assign: unknown or released request %d", seq);
+  std::vector<uint8_t> seen(pool->num_pages, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t p = page_ids[i];
+    if (p < 0 || p >= pool->num_pages)
+      return fail(JF_ERR_INVALID, "assign: page %d out of range", p);
+    if (!pool->in_free[p] || seen[p])
+      return fail(JF_ERR_STATE, "assign: page %d is not free", p);
+    seen[p] = 1;
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t p = page_ids[i];
+    pool->in_free[p] = 0;  // its stack entry goes stale
+    --pool->n_free;
+    pool->take_ref(p);
+    s->pages.push_back(p);
+  }
+  return ok();
+}
+
+jf_status jf_page_table_reserve(jf_page_pool* pool, int32_t seq, int32_t new_len) {
+  if (!pool) return fail(JF_ERR_INVALID, "pool is NULL");
+  jf_page_pool::Seq* s = pool->get(seq);
+  if (!s) return fail(JF_ERR_STATE, "reserve: unknown or released request %d", seq);
+  if (new_len < 0) return fail(JF_ERR_INVALID, "reserve: negative length");
+  const int32_t P = pool->page_size;
+  int64_t need_pages = ((int64_t)new_len + P - 1) / P;
+  if (new_len > s->length) {
+    // positions length..new_len-1 that land on pages already held must not
+    // be on shared pages
+    int64_t first = s->length / P;
+    int64_t last = std::min<int64_t>(need_pages, (int64_t)s->pages.size());
+    for (int64_t lp = first; lp < last; ++lp)
+      if (pool->refcount[s->pages[lp]] > 1)
+        return fail(JF_ERR_STATE, "reserve: logical page %lld of request %d is shared",
+                    (long long)lp, seq);
+  }
+  int64_t missing = need_pages - (int64_t)s->pages.size();
+  if (missing <= 0) return ok();
+  if (missing > pool->n_free)
+    return fail(JF_ERR_NO_PAGES, "reserve: need %lld pages, %d free", (long long)missing,
+                pool->n_free);
+  for (int64_t i = 0; i < missing; ++i) {
+    int32_t p = pool->pop_free();
+    pool->take_ref(p);
+    s->pages.push_back(p);
+  }
+  return ok();
+}
+
+jf_status jf_page_table_set_length(jf_page_pool* pool, int32_t seq, int32_t len) {
+  if (!pool) return fail(JF_ERR_INVALID, "pool is NULL");
+  jf_page_pool::Seq* s = pool->get(seq);
+  if (!s) return fail(JF_ERR_STATE, "set_length: unknown or released request %d", seq);
+  if (len < 0 || (int64_t)len > (int64_t)s->pages.size() * pool->page_size)
+    return fail(JF_ERR_INVALID, "set_length: %d exceeds the capacity of %zu pages", len,
+                s->pages.size());
+  s->length = len;
+  return ok();
+}
+
+jf_status jf_page_table_release(jf_page_pool* pool, int32_t seq) {
+  if (!pool) return fail(JF_ERR_INVALID, "pool is NULL");
+  jf_page_pool::Seq* s = pool->get(seq);
+  if (!s) return fail(JF_ERR_STATE, "release: unknown or released request %d", seq);
+  for (int32_t p : s->pages) pool->drop_ref(p);
+  s->pages.clear();
+  s->pages.shrink_to_fit();
+  s->length = 0;
+  s->live = false;
+  return ok();
+}
+
+jf_status jf_page_table_export(const jf_page_pool* pool, const int32_t* seqs, int32_t n,
+                               int32_t max_pages, int32_t* block_table, int32_t* lens) {
+  if (!pool || (n > 0 && (!seqs || !block_table || !lens)) || n < 0 || max_pages < 0)
+    return fail(JF_ERR_INVALID, "bad argument");
+  for (int32_t i = 0; i < n; ++i) {
+    const jf_page_pool::Seq* s = pool->get(seqs[i]);
+    if (!s) return fail(JF_ERR_STATE, "export: unknown or released request %d", seqs[i]);
+    if ((int64_t)s->pages.size() > max_pages)
+      return fail(JF_ERR_INVALID, "export: request %d has %zu pages > max_pages %d", seqs[i],
+                  s->pages.size(), max_pages);
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    const jf_page_pool::Seq* s = pool->get(seqs[i]);
+    int32_t* row = block_table + (size_t)i * max_pages;
+    size_t k = 0;
+    for (; k < s->pages.size(); ++k) row[k] = s->pages[k];
+    for (; k < (size_t)max_pages; ++k) row[k] = -1;
+    lens[i] = s->length;
+  }
+  return ok();
+}
+
+jf_status jf_page_table_stats(const jf_page_pool* pool, int32_t* free_pages,
+                              int32_t* used_pages, int32_t* high_water) {
+  if (!pool || !free_pages || !used_pages || !high_water)
+    return fail(JF_ERR_INVALID, "NULL argument");
+  *free_pages = pool->n_free;
+  *used_pages = pool->used;
+  *high_water = pool->high_water;
+  return ok();
+}
+
+jf_status jf_page_table_info(const jf_page_pool* pool, int32_t seq, int32_t* n_pages,
+                             int32_t* length) {
+  if (!pool || !n_pages || !length) return fail(JF_ERR_INVALID, "NULL argument");
+  const jf_page_pool::Seq* s = pool->get(seq);
+  if (!s) return fail(JF_ERR_STATE, "info: unknown or released request %d", seq);
+  *n_pages = (int32_t)s->pages.size();
+  *length = s->length;
+  return ok();
+}
+
+// ------------------------------------------------------------------ device
+jf_status jf_kv_quantize_append(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                                const void* k_new, const void* v_new, const int32_t* cu_tok,
+                                const int32_t* start_pos, const int32_t* block_tables,
+                                int32_t B, int32_t max_pages, int32_t total_tok,
+                                hipStream_t stream) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if ((st = check_pool(pool))) return st;
+  if (B <= 0 || max_pages <= 0 || total_tok < 0)
+    return fail(JF_ERR_INVALID, "B and max_pages must be positive, total_tok >= 0");
+  if (total_tok == 0) return ok();
+  if (!k_new || !v_new || !cu_tok || !start_pos || !block_tables)
+    return fail(JF_ERR_INVALID, "NULL device pointer");
+  return device_status(jfkv::launch_quantize_append(*layout, *pool, k_new, v_new, cu_tok,
+                                                    start_pos, block_tables, B, max_pages,
+                                                    total_tok, stream),
+                       "quantize_append launch");
+}
+
+jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads, int32_t head_dim,
+                                    int32_t max_splits, size_t* bytes) {
+  if (!bytes || B <= 0 || num_q_heads <= 0 || head_dim <= 0 || max_splits <= 0 ||
+      max_splits > 1024)
+    return fail(JF_ERR_INVALID, "bad argument (max_splits must be 1..1024)");
+  *bytes = (size_t)B * num_q_heads * max_splits * (head_dim + 2) * sizeof(float);
+  return ok();
+}
+
+jf_status jf_decode_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                            const void* q, int32_t B, int32_t num_q_heads,
+                            const int32_t* block_tables, int32_t max_pages,
+                            const int32_t* seq_lens, float softmax_scale, int32_t max_splits,
+                            void* workspace, size_t workspace_bytes, void* out,
+                            hipStream_t stream) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if ((st = check_pool(pool))) return st;
+  if (!q || !block_tables || !seq_lens || !workspace || !out)
+    return fail(JF_ERR_INVALID, "NULL device pointer");
+  if (B <= 0 || num_q_heads <= 0 || max_pages <= 0)
+    return fail(JF_ERR_INVALID, "B, num_q_heads and max_pages must be positive");
+  if (num_q_heads % layout->num_kv_heads)
+    return fail(JF_ERR_INVALID, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                num_q_heads, layout->num_kv_heads);
+  if ((int64_t)max_pages * layout->page_size > INT32_MAX)
+    return fail(JF_ERR_INVALID, "max_pages * page_size overflows int32");
+  size_t need = 0;
+  if ((st = jf_decode_workspace_bytes(B, num_q_heads, layout->head_dim, max_splits, &need)))
+    return st;
+  if (workspace_bytes < need)
+    return fail(JF_ERR_INVALID, "workspace %zu bytes < required %zu", workspace_bytes, need);
+  if (!(softmax_scale == softmax_scale) || softmax_scale == INFINITY ||
+      softmax_scale == -INFINITY)
+    return fail(JF_ERR_INVALID, "softmax_scale must be finite");
+  return device_status(jfkv::launch_decode(*layout, *pool, q, B, num_q_heads, block_tables,
+                                           max_pages, seq_lens, softmax_scale, max_splits,
+                                           workspace, out, stream),
+                       "decode launch");
+}
+
+jf_status jf_prefill_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                             const void* q, const void* k_chunk, const void* v_chunk,
+                             int32_t T, int32_t num_q_heads, const int32_t* block_table,
+                             int32_t max_pages, int32_t prefix_len, float softmax_scale,
+                             void* out, hipStream_t stream) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if ((st = check_pool(pool))) return st;
+  if (T < 0 || prefix_len < 0 || num_q_heads <= 0 || max_pages < 0)
+    return fail(JF_ERR_INVALID, "negative size");
+  if (num_q_heads % layout->num_kv_heads)
+    return fail(JF_ERR_INVALID, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                num_q_heads, layout->num_kv_heads);
+  if ((int64_t)prefix_len > (int64_t)max_pages * layout->page_size)
+    return fail(JF_ERR_INVALID, "prefix_len %d exceeds max_pages %d * page_size %d",
+                prefix_len, max_pages, layout->page_size);
+  if ((int64_t)prefix_len + T > INT32_MAX)
+    return fail(JF_ERR_INVALID, "prefix_len + T overflows int32");
+  if (!(softmax_scale == softmax_scale) || softmax_scale == INFINITY ||
+      softmax_scale == -INFINITY)
+    return fail(JF_ERR_INVALID, "softmax_scale must be finite");
+  if (T == 0) return ok();
+  if (!q || !k_chunk || !v_chunk || !out || (prefix_len > 0 && !block_table))
+    return fail(JF_ERR_INVALID, "NULL device pointer");
+  return device_status(jfkv::launch_prefill(*layout, *pool, q, k_chunk, v_chunk, T,
+                                            num_q_heads, block_table, max_pages, prefix_len,
+                                            softmax_scale, out, stream),
+                       "prefill launch");
+}
+
+}  // extern "C"

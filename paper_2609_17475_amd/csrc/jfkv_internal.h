@@ -1,0 +1,39 @@
+// Internal declarations shared by the host dispatcher and the kernel files
+// of libjfkv.so.  Not part of the public ABI (include/jfkv.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "jfkv.h"
+
+namespace jfkv {
+
+// Geometry accepted by every device entry point (validated on the host).
+bool geometry_supported(const jf_kv_layout& L);
+
+// Kernel launchers.  They assume validated arguments and return the HIP
+// launch status.
+hipError_t launch_quantize_append(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
+                                  const void* k_new, const void* v_new,
+                                  const int32_t* cu_tok, const int32_t* start_pos,
+                                  const int32_t* block_tables, int32_t B,
+                                  int32_t max_pages, int32_t total_tok,
+                                  hipStream_t stream);
+
+hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
+                         const void* q, int32_t B, int32_t num_q_heads,
+                         const int32_t* block_tables, int32_t max_pages,
+                         const int32_t* seq_lens, float softmax_scale,
+                         int32_t max_splits, void* workspace, void* out,
+                         hipStream_t stream);
+
+hipError_t launch_prefill(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
+                          const void* q, const void* k_chunk, const void* v_chunk,
+                          int32_t T, int32_t num_q_heads,
+                          const int32_t* block_table, int32_t max_pages,
+                          int32_t prefix_len, float softmax_scale, void* out,
+                          hipStream_t stream);
+
+}  // namespace jfkv

@@ -1,0 +1,293 @@
+"""ctypes binding of libjfkv.so (include/jfkv.h).
+
+Argument marshalling only: every step of quantize-append, decode and prefill
+runs in the library's HIP kernels.  Device buffers are torch tensors on the
+GPU; the stream is torch's current stream unless one is given.  Errors raise
+``JfError`` with the library's message.  If the shared library is missing the
+import of this module fails loudly: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libjfkv.so")
+
+JF_OK, JF_ERR_INVALID, JF_ERR_NO_PAGES, JF_ERR_DEVICE, JF_ERR_UNSUPPORTED, JF_ERR_STATE = range(6)
+STATUS_NAMES = {0: "JF_OK", 1: "JF_ERR_INVALID", 2: "JF_ERR_NO_PAGES", 3: "JF_ERR_DEVICE",
+                4: "JF_ERR_UNSUPPORTED", 5: "JF_ERR_STATE"}
+
+# every symbol include/jfkv.h declares
+EXPORTS = [
+    "jf_last_error", "jf_version", "jf_kv_pool_bytes",
+    "jf_page_table_pool_create", "jf_page_table_pool_destroy", "jf_page_table_create",
+    "jf_page_table_fork", "jf_page_table_assign", "jf_page_table_reserve",
+    "jf_page_table_set_length", "jf_page_table_release", "jf_page_table_export",
+    "jf_page_table_stats", "jf_page_table_info",
+    "jf_kv_quantize_append", "jf_decode_workspace_bytes", "jf_decode_attn_q4",
+    "jf_prefill_attn_q4",
+]
+
+
+class JfError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("%s: %s" % (STATUS_NAMES.get(status, str(status)), message))
+        self.status = status
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [("page_size", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32)]
+
+
+class PoolPtrs(ctypes.Structure):
+    _fields_ = [("k_codes", ctypes.c_void_p), ("k_meta", ctypes.c_void_p),
+                ("v_codes", ctypes.c_void_p), ("v_meta", ctypes.c_void_p)]
+
+
+def _load():
+    # Load torch first: its wheel ships its own HIP runtime (same SONAME as
+    # /opt/rocm's), and the library must bind to that one, which owns the
+    # streams and allocations it receives.  Loading libjfkv.so first would
+    # map a second runtime version into the process.
+    import torch  # noqa: F401
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libjfkv.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t
+    pi32 = ctypes.POINTER(ctypes.c_int32)
+    st = ctypes.c_int
+    sig = {
+        "jf_last_error": (ctypes.c_char_p, []),
+        "jf_version": (ctypes.c_char_p, []),
+        "jf_kv_pool_bytes": (st, [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
+        "jf_page_table_pool_create": (st, [i32, i32, u64, ctypes.POINTER(P)]),
+        "jf_page_table_pool_destroy": (st, [P]),
+        "jf_page_table_create": (st, [P, pi32]),
+        "jf_page_table_fork": (st, [P, i32, i32, pi32]),
+        "jf_page_table_assign": (st, [P, i32, P, i32]),
+        "jf_page_table_reserve": (st, [P, i32, i32]),
+        "jf_page_table_set_length": (st, [P, i32, i32]),
+        "jf_page_table_release": (st, [P, i32]),
+        "jf_page_table_export": (st, [P, P, i32, i32, P, P]),
+        "jf_page_table_stats": (st, [P, pi32, pi32, pi32]),
+        "jf_page_table_info": (st, [P, i32, pi32, pi32]),
+        "jf_kv_quantize_append": (st, [P, P, P, P, P, P, P, i32, i32, i32, P]),
+        "jf_decode_workspace_bytes": (st, [i32, i32, i32, i32, ctypes.POINTER(sz)]),
+        "jf_decode_attn_q4": (st, [P, P, P, i32, i32, P, i32, P, ctypes.c_float, i32, P, sz, P,
+                                   P]),
+        "jf_prefill_attn_q4": (st, [P, P, P, P, P, i32, i32, P, i32, i32, ctypes.c_float, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    return L
+
+
+lib = _load()
+
+
+def _check(status: int):
+    if status != JF_OK:
+        raise JfError(status, lib.jf_last_error().decode())
+
+
+def version() -> str:
+    return lib.jf_version().decode()
+
+
+def layout(page_size: int, num_kv_heads: int, head_dim: int, group_size: int,
+           num_pages: int) -> Layout:
+    return Layout(page_size, num_kv_heads, head_dim, group_size, num_pages)
+
+
+def kv_pool_bytes(lay: Layout):
+    cb, mb = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib.jf_kv_pool_bytes(ctypes.byref(lay), ctypes.byref(cb), ctypes.byref(mb)))
+    return cb.value, mb.value
+
+
+# ------------------------------------------------------------ page tables
+class PagePool:
+    """Host page allocator with per-request page tables (owned by the library)."""
+
+    def __init__(self, num_pages: int, page_size: int, shuffle_seed: int = 0):
+        h = ctypes.c_void_p()
+        _check(lib.jf_page_table_pool_create(num_pages, page_size, shuffle_seed, ctypes.byref(h)))
+        self._h = h
+        self.num_pages = num_pages
+        self.page_size = page_size
+
+    def close(self):
+        if self._h:
+            _check(lib.jf_page_table_pool_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def create(self) -> int:
+        s = ctypes.c_int32()
+        _check(lib.jf_page_table_create(self._h, ctypes.byref(s)))
+        return s.value
+
+    def fork(self, src: int, prefix_len: int) -> int:
+        s = ctypes.c_int32()
+        _check(lib.jf_page_table_fork(self._h, src, prefix_len, ctypes.byref(s)))
+        return s.value
+
+    def assign(self, seq: int, page_ids: Sequence[int]):
+        arr = (ctypes.c_int32 * len(page_ids))(*[int(p) for p in page_ids])
+        _check(lib.jf_page_table_assign(self._h, seq, arr, len(page_ids)))
+
+    def reserve(self, seq: int, new_len: int):
+        _check(lib.jf_page_table_reserve(self._h, seq, new_len))
+
+    def set_length(self, seq: int, length: int):
+        _check(lib.jf_page_table_set_length(self._h, seq, length))
+
+    def release(self, seq: int):
+        _check(lib.jf_page_table_release(self._h, seq))
+
+    def export(self, seqs: Sequence[int], max_pages: int):
+        """-> (block_table list[list[int]] padded with -1, lens list[int])."""
+        n = len(seqs)
+        s = (ctypes.c_int32 * max(n, 1))(*seqs)
+        bt = (ctypes.c_int32 * max(n * max_pages, 1))()
+        ln = (ctypes.c_int32 * max(n, 1))()
+        _check(lib.jf_page_table_export(self._h, s, n, max_pages, bt, ln))
+        table = [list(bt[i * max_pages:(i + 1) * max_pages]) for i in range(n)]
+        return table, list(ln[:n])
+
+    def stats(self):
+        f, u, h = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check(lib.jf_page_table_stats(self._h, ctypes.byref(f), ctypes.byref(u), ctypes.byref(h)))
+        return {"free": f.value, "used": u.value, "high_water": h.value}
+
+    def info(self, seq: int):
+        n, ln = ctypes.c_int32(), ctypes.c_int32()
+        _check(lib.jf_page_table_info(self._h, seq, ctypes.byref(n), ctypes.byref(ln)))
+        return n.value, ln.value
+
+
+# ------------------------------------------------------------ device work
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+class KVPool:
+    """One layer's K and V pools in device memory (uint8 codes, fp16 meta)."""
+
+    def __init__(self, lay: Layout, device="cuda", fill: Optional[int] = None):
+        import torch
+        self.layout = lay
+        cb, mb = kv_pool_bytes(lay)
+
+        def buf(n):
+            t = torch.empty(n, dtype=torch.uint8, device=device)
+            if fill is not None:
+                t.fill_(fill)
+            return t
+
+        self.k_codes = buf(cb)
+        self.v_codes = buf(cb)
+        self.k_meta = buf(mb).view(torch.float16)
+        self.v_meta = buf(mb).view(torch.float16)
+
+    def ptrs(self) -> PoolPtrs:
+        return PoolPtrs(self.k_codes.data_ptr(), self.k_meta.data_ptr(),
+                        self.v_codes.data_ptr(), self.v_meta.data_ptr())
+
+
+def _dev_check(t, name, dtype=None):
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
+
+
+def jf_kv_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_tables,
+                          stream=None):
+    import torch
+    for t, n, dt in ((k_new, "k_new", torch.float16), (v_new, "v_new", torch.float16),
+                     (cu_tok, "cu_tok", torch.int32), (start_pos, "start_pos", torch.int32),
+                     (block_tables, "block_tables", torch.int32)):
+        _dev_check(t, n, dt)
+    lay = pool.layout
+    total = k_new.shape[0]
+    if tuple(k_new.shape) != (total, lay.num_kv_heads, lay.head_dim) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [total_tok][Hkv][d]")
+    B = start_pos.shape[0]
+    if cu_tok.shape[0] != B + 1 or block_tables.dim() != 2 or block_tables.shape[0] != B:
+        raise ValueError("cu_tok [B+1], start_pos [B], block_tables [B][max_pages]")
+    ptrs = pool.ptrs()
+    _check(lib.jf_kv_quantize_append(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new),
+                                     _ptr(v_new), _ptr(cu_tok), _ptr(start_pos),
+                                     _ptr(block_tables), B, block_tables.shape[1], total,
+                                     _stream(stream)))
+
+
+def jf_decode_workspace_bytes(B: int, num_q_heads: int, head_dim: int, max_splits: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.jf_decode_workspace_bytes(B, num_q_heads, head_dim, max_splits, ctypes.byref(n)))
+    return n.value
+
+
+def jf_decode_attn_q4(pool: KVPool, q, block_tables, seq_lens, softmax_scale: float,
+                      max_splits: int, workspace, out, stream=None):
+    import torch
+    _dev_check(q, "q", torch.float16)
+    _dev_check(block_tables, "block_tables", torch.int32)
+    _dev_check(seq_lens, "seq_lens", torch.int32)
+    _dev_check(workspace, "workspace")
+    _dev_check(out, "out", torch.float16)
+    lay = pool.layout
+    B, Hq, d = q.shape
+    if d != lay.head_dim or out.shape != q.shape:
+        raise ValueError("q/out must be [B][Hq][head_dim]")
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("block_tables [B][max_pages], seq_lens [B]")
+    ptrs = pool.ptrs()
+    _check(lib.jf_decode_attn_q4(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), B, Hq,
+                                 _ptr(block_tables), block_tables.shape[1], _ptr(seq_lens),
+                                 float(softmax_scale), int(max_splits), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _ptr(out),
+                                 _stream(stream)))
+
+
+def jf_prefill_attn_q4(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len: int,
+                       softmax_scale: float, out, stream=None):
+    import torch
+    _dev_check(q, "q", torch.float16)
+    _dev_check(k_chunk, "k_chunk", torch.float16)
+    _dev_check(v_chunk, "v_chunk", torch.float16)
+    _dev_check(block_table, "block_table", torch.int32)
+    _dev_check(out, "out", torch.float16)
+    lay = pool.layout
+    T, Hq, d = q.shape
+    if d != lay.head_dim or out.shape != q.shape:
+        raise ValueError("q/out must be [T][Hq][head_dim]")
+    if tuple(k_chunk.shape) != (T, lay.num_kv_heads, d) or v_chunk.shape != k_chunk.shape:
+        raise ValueError("k_chunk/v_chunk must be [T][Hkv][head_dim]")
+    ptrs = pool.ptrs()
+    _check(lib.jf_prefill_attn_q4(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), _ptr(k_chunk),
+                                  _ptr(v_chunk), T, Hq, _ptr(block_table), block_table.shape[-1],
+                                  int(prefix_len), float(softmax_scale), _ptr(out),
+                                  _stream(stream)))

@@ -1,0 +1,87 @@
+"""The C ABI of libjfkv.so: every symbol include/jfkv.h declares is exported,
+and argument validation rejects bad calls before anything touches a GPU
+(CPU only: these calls fail validation, so no device work is enqueued)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+jfkv = pytest.importorskip("paper_2609_17475_amd.jfkv")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "jfkv.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(jf_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 18
+    lib = ctypes.CDLL(jfkv.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(jfkv.EXPORTS) == names
+
+
+def test_pool_bytes_closed_form_and_geometry_checks():
+    lay = jfkv.layout(256, 8, 128, 64, 1024)
+    cb, mb = jfkv.kv_pool_bytes(lay)
+    assert 2 * (cb + mb) == 1024 * 256 * 1152
+    for bad, st in [((256, 8, 128, 48, 4), jfkv.JF_ERR_INVALID),
+                    ((256, 8, 96, 32, 4), jfkv.JF_ERR_UNSUPPORTED),
+                    ((100, 8, 128, 64, 4), jfkv.JF_ERR_UNSUPPORTED),
+                    ((256, 0, 128, 64, 4), jfkv.JF_ERR_INVALID)]:
+        with pytest.raises(jfkv.JfError) as e:
+            jfkv.kv_pool_bytes(jfkv.layout(*bad))
+        assert e.value.status == st
+
+
+def test_workspace_bound_is_independent_of_length():
+    assert jfkv.jf_decode_workspace_bytes(1, 32, 128, 64) == 64 * 32 * 130 * 4
+    assert jfkv.jf_decode_workspace_bytes(2, 32, 128, 64) == 2 * 64 * 32 * 130 * 4
+    with pytest.raises(jfkv.JfError):
+        jfkv.jf_decode_workspace_bytes(1, 32, 128, 0)
+    with pytest.raises(jfkv.JfError):
+        jfkv.jf_decode_workspace_bytes(1, 32, 128, 2048)
+
+
+def _raw_decode(lay, ptrs, q=1, B=1, Hq=32, bt=1, max_pages=4, lens=1, scale=1.0, splits=8,
+                ws=1, ws_bytes=10 ** 9, out=1):
+    return jfkv.lib.jf_decode_attn_q4(ctypes.byref(lay), ctypes.byref(ptrs), q, B, Hq, bt,
+                                      max_pages, lens, scale, splits, ws, ws_bytes, out, None)
+
+
+def test_decode_validation_rejects_without_launch():
+    lay = jfkv.layout(256, 8, 128, 64, 16)
+    ptrs = jfkv.PoolPtrs(1, 1, 1, 1)
+    assert _raw_decode(lay, ptrs, Hq=30) == jfkv.JF_ERR_INVALID  # Hq % Hkv
+    assert b"multiple" in jfkv.lib.jf_last_error()
+    assert _raw_decode(lay, ptrs, ws_bytes=100) == jfkv.JF_ERR_INVALID
+    assert _raw_decode(lay, ptrs, q=None) == jfkv.JF_ERR_INVALID
+    assert _raw_decode(lay, jfkv.PoolPtrs(1, None, 1, 1)) == jfkv.JF_ERR_INVALID
+    assert _raw_decode(lay, ptrs, splits=0) == jfkv.JF_ERR_INVALID
+    assert _raw_decode(lay, ptrs, scale=float("nan")) == jfkv.JF_ERR_INVALID
+    assert _raw_decode(jfkv.layout(256, 8, 96, 32, 16), ptrs) == jfkv.JF_ERR_UNSUPPORTED
+
+
+def test_prefill_and_append_validation():
+    lay = jfkv.layout(256, 8, 128, 64, 16)
+    ptrs = jfkv.PoolPtrs(1, 1, 1, 1)
+    L = jfkv.lib
+    # prefix beyond the table capacity
+    st = L.jf_prefill_attn_q4(ctypes.byref(lay), ctypes.byref(ptrs), 1, 1, 1, 16, 32, 1, 2, 513,
+                              1.0, 1, None)
+    assert st == jfkv.JF_ERR_INVALID
+    # T = 0 is a no-op that succeeds without touching the device
+    st = L.jf_prefill_attn_q4(ctypes.byref(lay), ctypes.byref(ptrs), 1, 1, 1, 0, 32, 1, 2, 0,
+                              1.0, 1, None)
+    assert st == jfkv.JF_OK
+    st = L.jf_kv_quantize_append(ctypes.byref(lay), ctypes.byref(ptrs), 1, 1, 1, 1, 1, 0, 4, 1,
+                                 None)
+    assert st == jfkv.JF_ERR_INVALID  # B = 0
+    st = L.jf_kv_quantize_append(ctypes.byref(lay), ctypes.byref(ptrs), 1, 1, 1, 1, 1, 1, 4, 0,
+                                 None)
+    assert st == jfkv.JF_OK  # nothing to append

@@ -164,3 +164,22 @@ def test_ties_round_half_even():
     expect = [int(np.rint(k + 0.5)) for k in range(15)]  # numpy rint: half-even
     assert list(codes[2:17]) == expect
     assert expect[:4] == [0, 2, 2, 4]
+
+
+def test_signed_zero_order_is_element_order_independent():
+    """-0 orders below +0 for the minimum and above-zero ties go to +0 for the
+    maximum, whatever the element order."""
+    x = np.zeros(64, np.float16)
+    x[5] = np.float16(-0.0)
+    for perm_seed in range(5):
+        xp = np.random.default_rng(perm_seed).permutation(x)
+        codes, s, b = oracle.quantize_group(xp)
+        assert np.signbit(b) and float(s) == 0.0 and not np.signbit(s)
+    y = np.zeros(64, np.float16)
+    y[:] = np.float16(-0.0)
+    y[9] = np.float16(0.0)
+    y[10] = np.float16(2.0)
+    for perm_seed in range(5):
+        yp = np.random.default_rng(perm_seed).permutation(y)
+        codes, s, b = oracle.quantize_group(yp)
+        assert np.signbit(b)
