@@ -1,0 +1,213 @@
+#!/usr/bin/env python
+"""Decode attention over a 4-bit paged KV cache at a 262,144-position window.
+
+One step = one decode step of one layer for one request: host page
+reservation, quantize-append of the step's new K/V row into its page (position
+262,143), then split-K decode attention of 32 query heads (8 KV heads, d=128,
+GQA 4:1) over all 262,144 positions through a 1,024-entry shuffled page table,
+with the log-sum-exp combine.  Inputs (cache, page table, the steps' new rows
+and queries) are resident in HBM before timing.  Consecutive steps use
+different layers' pools (--layers, default 8 x 302 MB), so a step never finds
+the previous step's cache lines in the 256 MB last-level cache, as in a model
+whose layers each own a pool.
+
+Prints one JSON line: KV positions/s/layer (value), HBM GB/s of the decode
+kernels against the 8 TB/s peak (roofline), and the CPU oracle timed on a
+bounded sample (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn KV positions/s/layer + achieved HBM GB/s (% of peak) at 256K ctx"
+HBM_PEAK_GBS = 8000.0
+BYTES_PER_POSITION = 1152  # 2 * Hkv * (d/2 + 4*d/G) at Hkv=8, d=128, G=64
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(k16, v16, q16, table, n_sample: int):
+    """The CPU oracle on a bounded sample of the same workload: a decode step
+    (append one row, attend) over the first n_sample positions of the window,
+    all 32 query heads.  Building the sample's cache is untimed setup."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_17475_amd import workloads
+    P, hkv, d, G = 256, 8, 128, 64
+    NP = int(table.max()) + 1
+    lay = oracle.layout(P, hkv, d, G, NP)
+    pool = oracle.Pool(lay)
+    n_cached = n_sample - 1
+    oracle.quantize_append(pool, k16[:n_cached], v16[:n_cached], [0, n_cached], [0], table[None])
+    t0 = time.perf_counter()
+    oracle.quantize_append(pool, k16[n_cached:n_sample], v16[n_cached:n_sample], [0, 1],
+                           [n_cached], table[None])
+    oracle.decode(pool, q16[None], table[None], [n_sample], 1.0)
+    dt = time.perf_counter() - t0
+    threads = min(oracle.max_threads(), hkv)  # the decode loop has one task per KV head
+    return {"value": n_sample / dt, "unit": "KV positions/s/layer", "cores": threads,
+            "kind": "oracle", "seconds": dt,
+            "sample": "one decode step (quantize-append 1 row + fp64 attention of 32 q heads) "
+                      "over the first %d positions of the 262,144-position window; "
+                      "scaled as positions/s" % n_sample}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--layers", type=int, default=8, help="pools rotated across steps")
+    ap.add_argument("--max-splits", type=int, default=64)
+    ap.add_argument("--cpu-sample", type=int, default=65536,
+                    help="positions in the CPU oracle sample (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_17475_amd import jfkv, workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = workloads.WORKLOADS["decode_256k"]
+    P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
+    L = wl.seq_lens[0]
+    n_cached = L - 1
+    n_steps_total = args.warmup + args.steps
+    NP = wl.pool_pages
+    lay = jfkv.layout(P, hkv, d, G, NP)
+
+    # ---- page table: one request holding the full window (shuffled pages)
+    pp = jfkv.PagePool(NP, P, shuffle_seed=wl.seed)
+    seq = pp.create()
+    pp.reserve(seq, L)
+    pp.set_length(seq, n_cached)
+    table_rows, _ = pp.export([seq], L // P)
+    table = np.array(table_rows, np.int32)
+    t_table = torch.from_numpy(table).to(dev)
+
+    # ---- inputs (seeded, drawn on the device)
+    t0 = time.perf_counter()
+    k, v = workloads.gen_kv_device(wl.seed, n_cached + n_steps_total, hkv, d, wl.n_outlier, dev)
+    q = workloads.gen_q_device(wl.seed + 1, n_steps_total, hq, d, dev)
+    log("inputs drawn in %.1fs" % (time.perf_counter() - t0))
+
+    # ---- layer 0 cache built by the library's quantize-append, copied to the others
+    pools = [jfkv.KVPool(lay, device=dev) for _ in range(args.layers)]
+    t0 = time.perf_counter()
+    jfkv.jf_kv_quantize_append(pools[0], k[:n_cached], v[:n_cached],
+                               torch.tensor([0, n_cached], dtype=torch.int32, device=dev),
+                               torch.tensor([0], dtype=torch.int32, device=dev), t_table)
+    torch.cuda.synchronize()
+    log("bulk quantize of %d rows: %.1f ms (incl. launch)" % (n_cached, 1e3 * (time.perf_counter() - t0)))
+    for p in pools[1:]:
+        for n in ("k_codes", "v_codes", "k_meta", "v_meta"):
+            getattr(p, n).copy_(getattr(pools[0], n))
+    torch.cuda.synchronize()
+
+    # ---- per-step bound calls: append row n_cached + s at position n_cached, attend L
+    cu = torch.tensor([0, 1], dtype=torch.int32, device=dev)
+    start = torch.tensor([n_cached], dtype=torch.int32, device=dev)
+    lens = torch.tensor([L], dtype=torch.int32, device=dev)
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(1, hq, d, args.max_splits), dtype=torch.uint8,
+                     device=dev)
+    out = torch.empty((n_steps_total, 1, hq, d), dtype=torch.float16, device=dev)
+    stream = torch.cuda.current_stream()
+    appends, decodes = [], []
+    for s in range(n_steps_total):
+        pool = pools[s % args.layers]
+        row = slice(n_cached + s, n_cached + s + 1)
+        appends.append(jfkv.bind_quantize_append(pool, k[row], v[row], cu, start, t_table, stream))
+        decodes.append(jfkv.bind_decode(pool, q[s:s + 1].view(1, hq, d), t_table, lens, 1.0,
+                                        args.max_splits, ws, out[s], stream))
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(n_steps_total)]
+
+    def step(s):
+        pp.reserve(seq, L)  # host page reservation (already satisfied at the window)
+        ev[s][0].record(stream)
+        appends[s]()
+        ev[s][1].record(stream)
+        decodes[s]()
+        ev[s][2].record(stream)
+
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.warmup, n_steps_total):
+        step(s)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    timed = range(args.warmup, n_steps_total)
+    t_app = [ev[s][0].elapsed_time(ev[s][1]) for s in timed]
+    t_dec = [ev[s][1].elapsed_time(ev[s][2]) for s in timed]
+    ms_per_step = 1e3 * wall / args.steps
+    dec_ms = float(np.mean(t_dec))
+    dec_bytes = L * BYTES_PER_POSITION
+    achieved = dec_bytes / (dec_ms * 1e-3) / 1e9
+    log("append %.2f us  decode %.2f us (min %.2f)  wall/step %.2f us" % (
+        1e3 * np.mean(t_app), 1e3 * dec_ms, 1e3 * np.min(t_dec), 1e3 * ms_per_step))
+
+    # sanity: the timed steps produced finite outputs
+    assert torch.isfinite(out.float()).all().item(), "non-finite decode output"
+
+    result = {
+        "metric": METRIC,
+        "value": L / (ms_per_step * 1e-3),
+        "unit": "KV positions/s/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u4 codes x f16 -> f32",
+        "data": "synthetic",
+        "config": {"workload": "decode_256k", "positions": L, "batch": 1, "num_q_heads": hq,
+                   "num_kv_heads": hkv, "head_dim": d, "page_size": P, "group_size": G,
+                   "pages": L // P, "max_splits": args.max_splits,
+                   "layers_rotated": args.layers},
+        "hbm_GBs": achieved,
+        "hbm_pct_of_peak": 100.0 * achieved / HBM_PEAK_GBS,
+        "us_per_step": {"append": 1e3 * float(np.mean(t_app)), "decode": 1e3 * dec_ms,
+                        "wall": 1e3 * ms_per_step},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "decode (split + combine)",
+                     "algorithmic_bytes": dec_bytes},
+    }
+    if args.cpu_sample > 0:
+        try:
+            n_s = min(args.cpu_sample, L)
+            rows = n_s
+            kh = k[:rows].cpu().numpy()
+            vh = v[:rows].cpu().numpy()
+            qh = q[args.warmup].cpu().numpy()
+            result["cpu_baseline"] = cpu_baseline(kh, vh, qh, table[0], n_s)
+        except Exception as e:  # the baseline is a report, not the product
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -13,7 +13,7 @@ import os
 from typing import Optional, Sequence
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libjfkv.so")
+LIB_PATH = os.environ.get("JFKV_LIB") or os.path.join(HERE, "libjfkv.so")  # JFKV_LIB: another build
 
 JF_OK, JF_ERR_INVALID, JF_ERR_NO_PAGES, JF_ERR_DEVICE, JF_ERR_UNSUPPORTED, JF_ERR_STATE = range(6)
 STATUS_NAMES = {0: "JF_OK", 1: "JF_ERR_INVALID", 2: "JF_ERR_NO_PAGES", 3: "JF_ERR_DEVICE",
@@ -291,3 +291,51 @@ def jf_prefill_attn_q4(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_le
                                   _ptr(v_chunk), T, Hq, _ptr(block_table), block_table.shape[-1],
                                   int(prefix_len), float(softmax_scale), _ptr(out),
                                   _stream(stream)))
+
+
+# ------------------------------------------------------------ pre-bound calls
+class BoundCall:
+    """A library call with its ctypes arguments marshalled once (for timing
+    loops and graph capture, where per-call Python work would dominate)."""
+
+    def __init__(self, fn, args, keep):
+        self._fn = fn
+        self._args = args
+        self._keep = keep  # owners of the pointers (tensors, structs)
+
+    def __call__(self):
+        _check(self._fn(*self._args))
+
+
+def bind_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_tables,
+                         stream=None) -> BoundCall:
+    lay, ptrs = pool.layout, pool.ptrs()
+    B = start_pos.shape[0]
+    args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new), _ptr(v_new), _ptr(cu_tok),
+            _ptr(start_pos), _ptr(block_tables), B, block_tables.shape[1], k_new.shape[0],
+            _stream(stream))
+    return BoundCall(lib.jf_kv_quantize_append, args,
+                     (lay, ptrs, pool, k_new, v_new, cu_tok, start_pos, block_tables))
+
+
+def bind_decode(pool: KVPool, q, block_tables, seq_lens, softmax_scale, max_splits, workspace,
+                out, stream=None) -> BoundCall:
+    lay, ptrs = pool.layout, pool.ptrs()
+    B, Hq, _ = q.shape
+    args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), B, Hq, _ptr(block_tables),
+            block_tables.shape[1], _ptr(seq_lens), float(softmax_scale), int(max_splits),
+            _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(out),
+            _stream(stream))
+    return BoundCall(lib.jf_decode_attn_q4, args,
+                     (lay, ptrs, pool, q, block_tables, seq_lens, workspace, out))
+
+
+def bind_prefill(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len, softmax_scale, out,
+                 stream=None) -> BoundCall:
+    lay, ptrs = pool.layout, pool.ptrs()
+    T, Hq, _ = q.shape
+    args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), _ptr(k_chunk), _ptr(v_chunk), T, Hq,
+            _ptr(block_table), block_table.shape[-1], int(prefix_len), float(softmax_scale),
+            _ptr(out), _stream(stream))
+    return BoundCall(lib.jf_prefill_attn_q4, args,
+                     (lay, ptrs, pool, q, k_chunk, v_chunk, block_table, out))

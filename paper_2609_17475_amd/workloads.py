@@ -78,6 +78,12 @@ def outlier_count(head_dim: int, fraction: float = 0.02) -> int:
     return int(round(fraction * head_dim))
 
 
+def to_f16(x: np.ndarray) -> np.ndarray:
+    """Round float32 to fp16 (IEEE round-to-nearest-even), vectorized."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.float16).numpy()
+
+
 def _kv(rng, n_rows, hkv, d, n_out):
     k = rng.standard_normal((n_rows, hkv, d), dtype=np.float32)
     v = rng.standard_normal((n_rows, hkv, d), dtype=np.float32)
@@ -86,7 +92,7 @@ def _kv(rng, n_rows, hkv, d, n_out):
             ch = rng.choice(d, size=n_out, replace=False) if n_out else []
             for c in ch:
                 x[:, h, c] *= 8.0
-    return k.astype(np.float16), v.astype(np.float16)
+    return to_f16(k), to_f16(v)
 
 
 def gen_kv(seed: int, n_rows: int, hkv: int, d: int, n_out: int):
@@ -100,8 +106,8 @@ def gen_all(seed: int, n_rows: int, hkv: int, d: int, n_out: int, n_q_rows: int,
     """Full draw in recipe order: K, V, q fp16 [n_q_rows][hq][d], page permutation."""
     rng = np.random.default_rng(seed)
     k, v = _kv(rng, n_rows, hkv, d, n_out)
-    q = (rng.standard_normal((n_q_rows, hq, d), dtype=np.float32)
-         * np.float32(1.0 / math.sqrt(d))).astype(np.float16)
+    q = to_f16(rng.standard_normal((n_q_rows, hq, d), dtype=np.float32)
+               * np.float32(1.0 / math.sqrt(d)))
     perm = rng.permutation(n_pages).astype(np.int32)
     return k, v, q, perm
 
@@ -134,3 +140,31 @@ def needle_queries(k16: np.ndarray, hq: int, seed: int, gap: float = 12.0,
 def page_order(seed: int, n_pages_pool: int) -> np.ndarray:
     """A seeded permutation of a pool's page IDs."""
     return np.random.default_rng(seed).permutation(n_pages_pool).astype(np.int32)
+
+
+def gen_kv_device(seed: int, n_rows: int, hkv: int, d: int, n_out: int, device="cuda"):
+    """Device-side draw for the large workloads (same recipe, torch's seeded
+    generator on `device` instead of numpy PCG64): K, V fp16 [n_rows][hkv][d].
+    Outlier channels: for K then V, for each KV head, the first n_out entries of
+    a seeded permutation of the channels, scaled by 8."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    out = []
+    for _ in range(2):
+        x = torch.randn((n_rows, hkv, d), generator=g, device=device, dtype=torch.float32)
+        out.append(x)
+    for x in out:
+        for h in range(hkv):
+            ch = torch.randperm(d, generator=g, device=device)[:n_out]
+            x[:, h, ch] *= 8.0
+    return out[0].to(torch.float16), out[1].to(torch.float16)
+
+
+def gen_q_device(seed: int, n_rows: int, hq: int, d: int, device="cuda"):
+    """Queries fp16 [n_rows][hq][d] ~ N(0,1)/sqrt(d), torch's seeded generator."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    x = torch.randn((n_rows, hq, d), generator=g, device=device, dtype=torch.float32)
+    return (x * (1.0 / math.sqrt(d))).to(torch.float16)

@@ -117,7 +117,7 @@ def decode_gpu(case: Case, q: np.ndarray, max_splits=64, scale=1.0, lens=None, t
     dev = "cuda"
     tables = case.tables if tables is None else tables
     lens = case.lens if lens is None else lens
-    ws = torch.empty(jfkv.jf_decode_workspace_bytes(B, q.shape[1], q.shape[2], max_splits),
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(B, q.shape[1], q.shape[2], max_splits),
                      dtype=torch.uint8, device=dev)
     out = torch.empty(q.shape, dtype=torch.float16, device=dev)
     jfkv.jf_decode_attn_q4(case.gpu, torch.from_numpy(q).to(dev),

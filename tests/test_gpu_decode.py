@@ -138,3 +138,19 @@ def test_empty_and_clamped_lengths():
     # a length beyond the table capacity is clamped to max_pages * page_size
     got2 = decode_gpu(case, q[:1], lens=[10 ** 6], tables=case.tables[:1])
     check_tol(got2, decode_oracle(case, q[:1], lens=[128], tables=case.tables[:1]), what="clamp")
+
+
+def test_invalid_page_entries_are_skipped():
+    """A page-table entry outside [0, num_pages) is never read and its
+    positions do not contribute; attention is order-free over positions, so the
+    reference is the same request with that page's positions removed."""
+    log("decode invalid page entries")
+    case = build(P=64, hkv=2, d=128, G=64, hq=8, lens=(64 * 12,), seed=71)
+    q = _q(15, 1, 8, 128)
+    bad = case.tables.copy()
+    bad[0, 0] = -1                       # first page: no valid position seen before it
+    bad[0, 5] = case.lay.num_pages + 3   # out of range
+    got = decode_gpu(case, q, tables=bad)
+    keep = [p for i, p in enumerate(case.tables[0]) if i not in (0, 5)]
+    ref = decode_oracle(case, q, lens=[64 * 10], tables=np.array([keep], np.int32))
+    check_tol(got, ref, what="invalid pages")

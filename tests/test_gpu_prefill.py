@@ -45,7 +45,8 @@ def test_prefill_matches_oracle(P, hkv, hq, d, G, p0, T):
     q = (rng.standard_normal((T, hq, d)) / np.sqrt(d)).astype(np.float16)
     got = prefill_gpu(case, q, kc, vc, p0)
     ref = oracle.prefill(case.host, q, kc, vc, case.tables[0], p0, 1.0)
-    check_tol(got, ref, atol=2e-3, rel_elem=2.0 ** -8, rel_l2=4e-3, what="prefill")
+    log("  max err %.3e rel L2 %.3e" % check_tol(got, ref, atol=2e-3, rel_elem=2.0 ** -8,
+                                                 rel_l2=4e-3, what="prefill"))
 
 
 def test_prefill_then_append_chunk_bit_exact():
