@@ -54,10 +54,8 @@ constexpr float kTau = 2.0f;   // lazy-rescale margin, log2 units
 constexpr float kMinit = -1e30f;
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kStages = 3;     // LDS ring depth per wave
 constexpr int kCodeBytes = 4096;  // K + V codes of one row (any supported d)
-constexpr int kMetaBytes = 1024;  // K + V meta of one row (up to d/32 groups)
-constexpr int kStageBytes = kCodeBytes + kMetaBytes;
+constexpr int kRingBudget = 73728;  // LDS bytes per block for the rings (2 blocks per CU)
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
 __device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uint32_t, v); }
@@ -156,6 +154,22 @@ __device__ __forceinline__ void lds_read_k(uint32_t k0_addr, uint32_t k1_addr, u
       : "v"(k0_addr), "v"(k1_addr), "v"(km_addr), "v"(vm_addr)
       : "memory");
 }
+__device__ __forceinline__ void lds_read_kv(uint32_t k0_addr, uint32_t k1_addr, uint32_t km_addr,
+                                            uint32_t vm_addr, uint32_t v_addr, uint4& k0,
+                                            uint4& k1, uint2& km, uint2& vm, uint4& v0,
+                                            uint4& v1) {
+  asm volatile(
+      "ds_read_b128 %0, %6\n\t"
+      "ds_read_b128 %1, %7\n\t"
+      "ds_read_b64 %2, %8\n\t"
+      "ds_read_b64 %3, %9\n\t"
+      "ds_read_b128 %4, %10\n\t"
+      "ds_read_b128 %5, %10 offset:16\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(k0), "=&v"(k1), "=&v"(km), "=&v"(vm), "=&v"(v0), "=&v"(v1)
+      : "v"(k0_addr), "v"(k1_addr), "v"(km_addr), "v"(vm_addr), "v"(v_addr)
+      : "memory");
+}
 __device__ __forceinline__ void lds_read_v(uint32_t v_addr, uint4& v0, uint4& v1) {
   asm volatile(
       "ds_read_b128 %0, %2\n\t"
@@ -187,10 +201,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   constexpr int META_WORDS = ROWPOS * NG;          // per row, K or V
   constexpr int META_DMAS = (META_WORDS + 63) / 64;
   constexpr int DMAS_PER_ROW = 4 + 2 * META_DMAS;  // K 2, V 2, meta
+  constexpr int kMetaBytes = 2 * 256 * META_DMAS;  // K then V meta, 256 B per DMA
+  constexpr int kStageBytes = kCodeBytes + kMetaBytes;
+  constexpr int kStages = kRingBudget / (kWaves * kStageBytes) >= 4 ? 4 : 3;
+  static_assert(kStages <= 4, "wait cascade covers up to 3 rows ahead");
   // lane j of a unit owns head j's softmax state when there is one head per lane
   constexpr bool kLaneHeads = (LPP == HPB) && (LPP == 2 || LPP == 4);
   static_assert(ROWPOS * D == kCodeBytes, "row codes");
-  static_assert(2 * META_WORDS * 4 <= kMetaBytes, "row meta");
+  static_assert(kStages * kWaves * kStageBytes <= kRingBudget, "ring size");
 
   __shared__ __attribute__((aligned(16))) uint8_t smem[kWaves][kStages][kStageBytes];
 
@@ -314,11 +332,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
   const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
   for (int r = 0; r < my_rows; ++r) {
-    if (r + kStages - 1 < my_rows) {
-      issue_row(r + kStages - 1);
-      wait_vm<DMAS_PER_ROW * (kStages - 1)>();
-    } else if (r + kStages - 2 < my_rows) {
-      wait_vm<DMAS_PER_ROW * (kStages - 2)>();
+    // rows issued after row r: min(kStages - 1, my_rows - 1 - r); wait until
+    // only those are in flight
+    if (r + kStages - 1 < my_rows) issue_row(r + kStages - 1);
+    const int ahead = min(kStages - 1, my_rows - 1 - r);
+    if (ahead >= 3) {
+      wait_vm<DMAS_PER_ROW * 3>();
+    } else if (ahead == 2) {
+      wait_vm<DMAS_PER_ROW * 2>();
+    } else if (ahead == 1) {
+      wait_vm<DMAS_PER_ROW>();
     } else {
       wait_vm<0>();
     }
@@ -340,9 +363,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const uint32_t st = ring_lds + (r % kStages) * kStageBytes;
     uint4 kw0, kw1, vw0, vw1;
     uint2 km, vm;
+#ifdef JF_SPLIT_LDS_READS
     lds_read_k(st + (2 * unit) * (D / 2) + 16 * j, st + (2 * unit + 1) * (D / 2) + 16 * j,
                st + kCodeBytes + (g * ROWPOS + 2 * unit) * 4,
                st + kCodeBytes + kMetaBytes / 2 + (g * ROWPOS + 2 * unit) * 4, kw0, kw1, km, vm);
+#else
+    lds_read_kv(st + (2 * unit) * (D / 2) + 16 * j, st + (2 * unit + 1) * (D / 2) + 16 * j,
+                st + kCodeBytes + (g * ROWPOS + 2 * unit) * 4,
+                st + kCodeBytes + kMetaBytes / 2 + (g * ROWPOS + 2 * unit) * 4,
+                st + 2048 + unit * D + 32 * j, kw0, kw1, km, vm, vw0, vw1);
+#endif
 
     // ---- QK partial dot products over the lane's 32 dims
     float d0[HPB], d1[HPB];
@@ -468,7 +498,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         W[h] = pp * sv;
       }
     }
+#ifdef JF_SPLIT_LDS_READS
     lds_read_v(st + 2048 + unit * D + 32 * j, vw0, vw1);
+#endif
     const uint32_t va[8] = {vw0.x, vw0.y, vw0.z, vw0.w, vw1.x, vw1.y, vw1.z, vw1.w};
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
@@ -551,13 +583,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 // while an in-kernel ticket would need device-scope fences, which write back
 // an XCD's L2 on this GPU).  256 threads: 256/D threads per dim, each summing
 // a strided subset of the splits with independent loads.
+constexpr int kCombineThreads = 512;
+
 template <int D>
-__global__ __launch_bounds__(kThreads) void decode_combine_kernel(
+__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(
     const float* __restrict__ ws, const int32_t* __restrict__ seq_lens, __half* __restrict__ out,
     int Hq, int P, int max_pages, int max_splits) {
-  constexpr int PARTS = kThreads / D;
+  constexpr int NT = kCombineThreads, NW = NT / 64;
+  constexpr int PARTS = NT / D;
   __shared__ float s_w[1024];
-  __shared__ float s_red[kWaves];
+  __shared__ float s_red[NW];
   __shared__ float s_part[PARTS][D];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -570,12 +605,12 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(
   const int n_pages = (L + P - 1) / P;
   const int S = min(max_splits, n_pages);
   const float* recs = ws + ((size_t)b * Hq + h) * max_splits * (D + 2);
-  // one round of loads for every split's (m, l); S <= 1024 = 4 per thread
-  float mv[4], lv[4];
+  // one round of loads for every split's (m, l); S <= 1024
+  float mv[2], lv[2];
   float M = -INFINITY;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int s = tid + k * kThreads;
+  for (int k = 0; k < 2; ++k) {
+    const int s = tid + k * NT;
     mv[k] = (s < S) ? recs[(size_t)s * (D + 2) + D] : -INFINITY;
     lv[k] = (s < S) ? recs[(size_t)s * (D + 2) + D + 1] : 0.0f;
     M = fmaxf(M, mv[k]);
@@ -583,12 +618,14 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(
   M = wave_max(M);
   if (lane == 0) s_red[wave] = M;
   __syncthreads();
-  M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
+  M = s_red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) M = fmaxf(M, s_red[w]);
   float den = 0.0f;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int s = tid + k * kThreads;
-    const float w = (mv[k] == -INFINITY) ? 0.0f : lv[k] * __builtin_amdgcn_exp2f(mv[k] - M);
+  for (int k = 0; k < 2; ++k) {
+    const int s = tid + k * NT;
+    const float w = (s < S && mv[k] != -INFINITY) ? lv[k] * __builtin_amdgcn_exp2f(mv[k] - M) : 0.0f;
     if (s < S) s_w[s] = w;
     den += w;
   }
@@ -596,20 +633,25 @@ __global__ __launch_bounds__(kThreads) void decode_combine_kernel(
   __syncthreads();  // s_red reads done before it is reused
   if (lane == 0) s_red[wave] = den;
   __syncthreads();
-  den = s_red[0] + s_red[1] + s_red[2] + s_red[3];
-  // weighted sum over splits: thread (part, dim) takes splits part, part+PARTS, ...
-  const int i = tid % D, part = tid / D;
-  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  int s = part;
-  for (; s + 7 * PARTS < S; s += 8 * PARTS) {
+  den = 0.0f;
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-      acc[k] = fmaf(s_w[s + k * PARTS], recs[(size_t)(s + k * PARTS) * (D + 2) + i], acc[k]);
+  for (int w = 0; w < NW; ++w) den += s_red[w];
+  // weighted sum: thread (part, dim) takes splits part, part+PARTS, ...; 16
+  // independent loads per round
+  const int i = tid % D, part = tid / D;
+  float acc[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) acc[k] = 0.0f;
+  for (int s0 = part; s0 < S; s0 += 16 * PARTS) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int s = s0 + k * PARTS;
+      if (s < S) acc[k] = fmaf(s_w[s], recs[(size_t)s * (D + 2) + i], acc[k]);
+    }
   }
-  for (; s < S; s += PARTS) acc[0] = fmaf(s_w[s], recs[(size_t)s * (D + 2) + i], acc[0]);
   float num = 0.0f;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) num += acc[k];
+  for (int k = 0; k < 16; ++k) num += acc[k];
   s_part[part][i] = num;
   __syncthreads();
   if (tid < D) {
@@ -637,7 +679,7 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
                      L.num_pages, max_pages, max_splits, n_hchunks, scale * kLog2e);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(Hq, B), dim3(kThreads), 0, stream,
+  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(Hq, B), dim3(kCombineThreads), 0, stream,
                      static_cast<const float*>(ws), lens, static_cast<__half*>(out), Hq,
                      L.page_size, max_pages, max_splits);
   return hipGetLastError();
