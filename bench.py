@@ -20,6 +20,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -35,31 +36,79 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(k16, v16, q16, table, n_sample: int):
-    """The CPU oracle on a bounded sample of the same workload: a decode step
-    (append one row, attend) over the first n_sample positions of the window,
-    all 32 query heads.  Building the sample's cache is untimed setup."""
-    import numpy as np
-
+def cpu_baseline(k16, v16, q16, table, n_sample: int, min_seconds: float):
+    """The CPU oracle on a bounded sample of the same workload: one decode step
+    (append one row, attend) over the first n_sample positions of the window
+    (by default all of it), all 32 query heads.  Building the sample's cache
+    is untimed setup."""
     import oracle
-    from paper_2609_17475_amd import workloads
     P, hkv, d, G = 256, 8, 128, 64
     NP = int(table.max()) + 1
     lay = oracle.layout(P, hkv, d, G, NP)
     pool = oracle.Pool(lay)
     n_cached = n_sample - 1
     oracle.quantize_append(pool, k16[:n_cached], v16[:n_cached], [0, n_cached], [0], table[None])
+    steps = 0
     t0 = time.perf_counter()
-    oracle.quantize_append(pool, k16[n_cached:n_sample], v16[n_cached:n_sample], [0, 1],
-                           [n_cached], table[None])
-    oracle.decode(pool, q16[None], table[None], [n_sample], 1.0)
-    dt = time.perf_counter() - t0
+    while True:  # repeat the step (same row, same position) until min_seconds have passed
+        oracle.quantize_append(pool, k16[n_cached:n_sample], v16[n_cached:n_sample], [0, 1],
+                               [n_cached], table[None])
+        oracle.decode(pool, q16[None], table[None], [n_sample], 1.0)
+        steps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
     threads = min(oracle.max_threads(), hkv)  # the decode loop has one task per KV head
-    return {"value": n_sample / dt, "unit": "KV positions/s/layer", "cores": threads,
-            "kind": "oracle", "seconds": dt,
-            "sample": "one decode step (quantize-append 1 row + fp64 attention of 32 q heads) "
-                      "over the first %d positions of the 262,144-position window; "
-                      "scaled as positions/s" % n_sample}
+    return {"value": n_sample * steps / dt, "unit": "KV positions/s/layer", "cores": threads,
+            "kind": "oracle", "seconds": dt, "steps": steps, "host_cpus": len(os.sched_getaffinity(0)),
+            "cpu_model": _cpu_model(),
+            "sample": "decode steps (quantize-append 1 row + fp64 attention of 32 q heads) "
+                      "over the first %d positions of the 262,144-position window, repeated "
+                      "for at least %.0f s, as positions/s" % (n_sample, min_seconds)}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_kernel_decode_256k_traffic.md")
+DECODE_SOURCE = os.path.join(ROOT, "paper_2609_17475_amd", "csrc", "decode.hip")
+
+
+def measured_traffic():
+    """HBM bytes per decode call from the committed counter profile, or None
+    when the decode source has changed since the counters were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    sha = hashlib.sha256(open(DECODE_SOURCE, "rb").read()).hexdigest()
+    m_sha = re.search(r"decode_source_sha256:\s*([0-9a-f]{64})", text)
+    m_b = re.search(r"traffic_bytes_per_call:\s*([0-9]+)", text)
+    if not m_sha or not m_b or m_sha.group(1) != sha:
+        return None
+    return int(m_b.group(1))
+
+
+def copy_calibration(n_bytes: int, reps: int):
+    """A plain device copy of known size, run under the FETCH_SIZE/WRITE_SIZE
+    counters to scale them to bytes."""
+    import torch
+    dev = torch.device("cuda:0")
+    src = torch.ones(n_bytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n_bytes, "copy_bytes_written": n_bytes, "reps": reps}),
+          flush=True)
 
 
 def main():
@@ -69,13 +118,20 @@ def main():
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--layers", type=int, default=8, help="pools rotated across steps")
     ap.add_argument("--max-splits", type=int, default=64)
-    ap.add_argument("--cpu-sample", type=int, default=65536,
+    ap.add_argument("--cpu-sample", type=int, default=262144,
                     help="positions in the CPU oracle sample (0 = skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="repeat the CPU oracle step for at least this long")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES bytes (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, max(1, args.steps))
+        return
 
     import numpy as np
     import torch
@@ -191,7 +247,7 @@ def main():
         "us_per_step": {"append": 1e3 * float(np.mean(t_app)), "decode": 1e3 * dec_ms,
                         "wall": 1e3 * ms_per_step},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
                      "kernel": "decode (split + combine)",
                      "algorithmic_bytes": dec_bytes},
     }
@@ -202,7 +258,7 @@ def main():
             kh = k[:rows].cpu().numpy()
             vh = v[:rows].cpu().numpy()
             qh = q[args.warmup].cpu().numpy()
-            result["cpu_baseline"] = cpu_baseline(kh, vh, qh, table[0], n_s)
+            result["cpu_baseline"] = cpu_baseline(kh, vh, qh, table[0], n_s, args.cpu_seconds)
         except Exception as e:  # the baseline is a report, not the product
             log("cpu baseline failed: %r" % (e,))
             result["cpu_baseline"] = None

@@ -20,8 +20,8 @@
  *     "Finish one head group ..." motivates bounding workspace; eq.
  *     layerbytes is what the fused prefill avoids materializing).
  * Stored format: affine 4-bit codes with one fp16 scale and one fp16 bias
- * per group of head_dim elements (the affine Q4 format named in the
- * Introduction, "Four-bit (Q4) weights ..."), eight codes per 32-bit word
+ * per group of head_dim elements (the affine 4-bit format the Introduction
+ * describes for weights: a scale and an offset per group), eight codes per 32-bit word
  * (Appendix A, Table codec, per-vector storage).
  *
  * ---------------------------------------------------------------------

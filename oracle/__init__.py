@@ -8,8 +8,8 @@ implements the same written definitions independently.
 Paper: "JustFit: Just-in-Time State Management for Local LLM Serving", KVExec.
   * paged pool + page table: Background, "Compact histories need reusable
     storage" (eq. kvbytes);
-  * affine 4-bit codes with per-group scale and offset: Introduction, "Four-bit
-    (Q4) weights ..."; eight codes per 32-bit word: Appendix A, Table codec;
+  * affine 4-bit codes with per-group scale and offset: the Introduction's
+    paragraph on four-bit weights; eight codes per 32-bit word: Appendix A, Table codec;
   * exact softmax attention over dequantized pages, heads independent:
     Sec. 3.1 (eq. groupattention).
 

@@ -13,8 +13,8 @@
  *     per-request page table (Background, "Compact histories need reusable
  *     storage"; eq. kvbytes gives the per-position payload);
  *   - group-wise affine 4-bit codes with one fp16 scale and one fp16 bias per
- *     group (the affine Q4 format named in the Introduction, "Four-bit (Q4)
- *     weights ...": stored values plus scales and offsets), packed eight codes
+ *     group (the affine 4-bit format the Introduction describes for
+ *     weights: stored values plus scales and offsets), packed eight codes
  *     per 32-bit word (Appendix A, Table codec, per-vector storage);
  *   - exact softmax attention over the dequantized pages for single-query
  *     decode and for chunked prefill (Sec. 3.1 KVExec, "Decode and prefill

@@ -1,8 +1,8 @@
 // Quantize-and-append of new K/V rows into 4-bit pages (gfx950).
 //
 // Encoding: group-wise affine 4-bit codes with an fp16 scale and bias per
-// group of head_dim elements (the affine Q4 format of the paper's
-// Introduction, "Four-bit (Q4) weights"), written into 256-token pages
+// group of head_dim elements (the affine 4-bit format the paper's
+// Introduction describes for weights), written into 256-token pages
 // through the request's page table (Background, "Compact histories need
 // reusable storage").  The contract is bit-exact; every binary32 step is a
 // separately rounded IEEE operation in the order given in include/jfkv.h.

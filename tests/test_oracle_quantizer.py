@@ -1,7 +1,7 @@
 """Pins for the oracle's fp16 conversions and group quantizer (CPU only).
 
 The quantizer is an encoding (affine 4-bit with per-group scale and offset,
-the Q4 format named in the paper's Introduction, "Four-bit (Q4) weights");
+the affine 4-bit format the paper's Introduction describes for weights);
 these tests pin it to facts that do not come from the oracle itself:
 numpy's binary16 conversion (an independent library routine), the definition
 of directed rounding, and the error bound of affine quantization with the
