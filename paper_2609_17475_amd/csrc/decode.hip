@@ -40,6 +40,8 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "jfkv_internal.h"
 
 namespace {
@@ -52,10 +54,16 @@ constexpr float kTau = 2.0f;   // lazy-rescale margin, log2 units
 // Initial running maximum: finite, so that a row with every position masked
 // (-inf logits) before any valid one gives p = 2^(-inf - kMinit) = 0, not NaN.
 constexpr float kMinit = -1e30f;
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;     // 8 waves: two splits of 4 waves, one block per CU
 constexpr int kWaves = kThreads / 64;
+constexpr int kSplitWaves = 4;    // waves per split
 constexpr int kCodeBytes = 4096;  // K + V codes of one row (any supported d)
-constexpr int kRingBudget = 73728;  // LDS bytes per block for the rings (2 blocks per CU)
+constexpr int kRingBudget = 163840;  // LDS bytes per block for the rings (all of a CU's LDS)
+// Block barrier every kBarrierRows rows: the two waves that share a SIMD
+// belong to one block, so the barrier keeps them at the same row (the
+// hardware issues oldest-first, which otherwise lets one wave finish long
+// before the other and leaves the SIMD with a single wave at the end).
+constexpr int kBarrierRows = 2;
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
 __device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uint32_t, v); }
@@ -111,6 +119,23 @@ __device__ __forceinline__ float bcast_head(float v, int h) {
   return __builtin_bit_cast(float, bcast_head_u<LPP>(__builtin_bit_cast(uint32_t, v), h));
 }
 
+// Lane index from a volatile instruction: code that uses it cannot be hoisted
+// out of a loop, so rarely taken paths keep no lane-derived registers live.
+__device__ __forceinline__ int lane_id_volatile() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+__device__ __forceinline__ float shfl_xor_at(float v, int lane, int off) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_ds_bpermute((lane ^ off) << 2, __builtin_bit_cast(int, v)));
+}
+// Maximum over lanes lane % from .. == const: offsets from, 2 from, ..., 32.
+__device__ __forceinline__ float xor_max_from(float v, int from) {
+  const int ln = lane_id_volatile();
+  for (int off = from; off < 64; off <<= 1) v = fmaxf(v, shfl_xor_at(v, ln, off));
+  return v;
+}
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) v = fmaxf(v, __shfl_xor(v, off));
@@ -170,6 +195,26 @@ __device__ __forceinline__ void lds_read_kv(uint32_t k0_addr, uint32_t k1_addr, 
       : "v"(k0_addr), "v"(k1_addr), "v"(km_addr), "v"(vm_addr), "v"(v_addr)
       : "memory");
 }
+// All reads of one staged row at compile-time offsets from three per-lane
+// bases (K codes, meta words, V codes), waited for once.
+template <int K0, int K1, int KM, int VM, int V0>
+__device__ __forceinline__ void lds_read_row(uint32_t k_addr, uint32_t m_addr, uint32_t v_addr,
+                                             uint4& k0, uint4& k1, uint2& km, uint2& vm, uint4& v0,
+                                             uint4& v1) {
+  static_assert(K0 >= 0 && V0 + 16 < 65536 && KM < 65536 && VM < 65536, "ds offsets");
+  asm volatile(
+      "ds_read_b128 %0, %6 offset:%9\n\t"
+      "ds_read_b128 %1, %6 offset:%10\n\t"
+      "ds_read_b64 %2, %7 offset:%11\n\t"
+      "ds_read_b64 %3, %7 offset:%12\n\t"
+      "ds_read_b128 %4, %8 offset:%13\n\t"
+      "ds_read_b128 %5, %8 offset:%14\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(k0), "=&v"(k1), "=&v"(km), "=&v"(vm), "=&v"(v0), "=&v"(v1)
+      : "v"(k_addr), "v"(m_addr), "v"(v_addr), "i"(K0), "i"(K1), "i"(KM), "i"(VM), "i"(V0),
+        "i"(V0 + 16)
+      : "memory");
+}
 __device__ __forceinline__ void lds_read_v(uint32_t v_addr, uint4& v0, uint4& v1) {
   asm volatile(
       "ds_read_b128 %0, %2\n\t"
@@ -178,6 +223,21 @@ __device__ __forceinline__ void lds_read_v(uint32_t v_addr, uint4& v0, uint4& v1
       : "=&v"(v0), "=&v"(v1)
       : "v"(v_addr)
       : "memory");
+}
+
+// Sum over the units of a 16-lane row (lanes of equal j = lane % LPP):
+// rotations by LPP, 2 LPP, ... within the row.
+template <int N>
+__device__ __forceinline__ float row_ror_add(float v) {
+  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                                   0x120 + N, 0xF, 0xF, false));
+}
+template <int LPP>
+__device__ __forceinline__ float row_units_sum(float v) {
+  if constexpr (LPP <= 2) v = row_ror_add<2>(v);
+  if constexpr (LPP <= 4) v = row_ror_add<4>(v);
+  if constexpr (LPP <= 8) v = row_ror_add<8>(v);
+  return v;
 }
 
 // Page-aligned split s of n_pages pages into S parts (remainder first).
@@ -212,7 +272,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 
   __shared__ __attribute__((aligned(16))) uint8_t smem[kWaves][kStages][kStageBytes];
 
-  const int split = blockIdx.x;
   const int kv = blockIdx.y / n_hchunks;
   const int hc = blockIdx.y % n_hchunks;
   const int b = blockIdx.z;
@@ -221,21 +280,130 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int nh = min(HPB, gq - hc * HPB);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int wave_blk = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int half = wave_blk / kSplitWaves;
+  const int wave = wave_blk % kSplitWaves;  // wave within its split
+  const int split = 2 * blockIdx.x + half;
 
   const int L = min(seq_lens[b], max_pages * P);
   if (L <= 0) return;  // the combine writes the all-zero output row
   const int n_pages = (L + P - 1) / P;
   const int S = min(max_splits, n_pages);
-  if (split >= S) return;
-  int pb, pe;
-  split_range(n_pages, S, split, pb, pe);
+  if (2 * (int)blockIdx.x >= S) return;  // both splits of the block are empty
+  const bool split_on = split < S;  // else this half only joins the barriers
+  int pb = 0, pe = 0;
+  if (split_on) split_range(n_pages, S, split, pb, pe);
   const int t_end = min(pe * P, L);
   const int rows_per_page = P / ROWPOS;
+  // rows of the block's busiest wave (the first split has the most pages)
+  int pb_first, pe_first;
+  split_range(n_pages, S, 2 * blockIdx.x, pb_first, pe_first);
+  const int block_rows =
+      ((pe_first - pb_first + kSplitWaves - 1) / kSplitWaves) * rows_per_page;
 
   const int unit = lane / LPP;
   const int j = lane % LPP;
   const int g = (32 * j) / G;  // the lane's scale group
+
+  // query words of the lane's 32 dims for each head (loaded now, unpacked
+  // after the first rows' loads are in flight)
+  uint4 qraw[HPB][4];
+#pragma unroll
+  for (int h = 0; h < HPB; ++h) {
+    const int head = h0 + min(h, nh - 1);
+    const uint4* src = reinterpret_cast<const uint4*>(q + ((size_t)b * Hq + head) * D + 32 * j);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) qraw[h][m] = src[m];
+  }
+
+  // ---- this wave's rows: pages pb + wave, pb + wave + 4, ...; every row of each
+  const int my_pages = (pe - pb - wave + kSplitWaves - 1) / kSplitWaves;
+  const int my_rows = (pe - pb > wave) ? my_pages * rows_per_page : 0;
+  const size_t head_codes = (size_t)P * (D / 2);
+  const size_t page_codes = (size_t)Hkv * head_codes;
+  uint8_t* ring = smem[wave_blk][0];
+  const uint32_t ring_lds = (uint32_t)(uintptr_t)ring;
+
+  // This wave's page IDs, 64 per vector register (lane k holds its k-th page),
+  // read with v_readlane when the issue cursor enters a page.
+  auto load_group = [&](int grp) {
+    const int k = 64 * grp + lane;
+    return (k < my_pages) ? block_tables[(size_t)b * max_pages + pb + wave + k * kSplitWaves] : -1;
+  };
+  int pg_grp = load_group(0);
+
+  // Per-lane parts of the load addresses (the row parts are scalar).
+  const uint32_t code_off = 16 * lane;
+  uint32_t meta_off[META_DMAS];  // transposed: word w = (group w / ROWPOS, pos w % ROWPOS)
+#pragma unroll
+  for (int i = 0; i < META_DMAS; ++i) {
+    const int w = 64 * i + lane;
+    const int wi = (w < META_WORDS) ? w : 0;
+    meta_off[i] = 4u * (uint32_t)((wi % ROWPOS) * NG + wi / ROWPOS);
+  }
+
+  // Issue cursor: the next row to load (page index ipk of the wave, row irr
+  // of the page) and the scalar addresses of that row.
+  int ipk = 0, irr = 0;
+  const uint8_t* ik = k_codes;
+  const uint8_t* iv = v_codes;
+  size_t im = 0;  // byte offset of the row's (scale, bias) words in k_meta / v_meta
+  bool iok = false;
+  auto enter_page = [&]() {
+    if ((ipk & 63) == 0 && ipk > 0) pg_grp = load_group(ipk >> 6);  // > 64 pages per wave
+    int page = __builtin_amdgcn_readlane(pg_grp, ipk & 63);
+    iok = (unsigned)page < (unsigned)NP;
+    if (!iok) page = 0;  // never read past the pool; the positions are masked
+    ik = k_codes + page * page_codes + kv * head_codes;
+    iv = v_codes + page * page_codes + kv * head_codes;
+    im = (((size_t)page * Hkv + kv) * P) * NG * 4;
+  };
+  bool stage_ok[kStages];
+  // Loads of the next row into stage ST; past the wave's last row, loads of
+  // one 16-byte run by every lane (same count, negligible traffic) keep the
+  // number of loads in flight per row constant.
+  auto issue = [&](auto st_c, bool real) {
+    constexpr int ST = decltype(st_c)::value;
+    uint8_t* st = ring + ST * kStageBytes;
+    if (real) {
+      dma16(ik + code_off, st);
+      dma16(ik + 1024 + code_off, st + 1024);
+      dma16(iv + code_off, st + 2048);
+      dma16(iv + 1024 + code_off, st + 3072);
+      const uint8_t* km8 = reinterpret_cast<const uint8_t*>(k_meta) + im;
+      const uint8_t* vm8 = reinterpret_cast<const uint8_t*>(v_meta) + im;
+#pragma unroll
+      for (int i = 0; i < META_DMAS; ++i) {
+        dma4(km8 + meta_off[i], st + kCodeBytes + 256 * i);
+        dma4(vm8 + meta_off[i], st + kCodeBytes + kMetaBytes / 2 + 256 * i);
+      }
+      stage_ok[ST] = iok;
+      // advance the cursor
+      ik += ROWPOS * (D / 2);
+      iv += ROWPOS * (D / 2);
+      im += ROWPOS * NG * 4;
+      if (++irr == rows_per_page) {
+        irr = 0;
+        ++ipk;
+        if (ipk < my_pages) enter_page();
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dma16(k_codes, st + 1024 * i);
+#pragma unroll
+      for (int i = 0; i < 2 * META_DMAS; ++i) dma4(k_meta, st + kCodeBytes + 256 * i);
+      stage_ok[ST] = false;
+    }
+  };
+  if (my_rows > 0) enter_page();
+  // All stages are in flight while a row is computed: a row's stage is read
+  // into registers first and then refilled with the row kStages ahead.
+  if (my_rows > 0) {
+    issue(std::integral_constant<int, 0>{}, 0 < my_rows);
+    issue(std::integral_constant<int, 1>{}, 1 < my_rows);
+    issue(std::integral_constant<int, 2>{}, 2 < my_rows);
+    if constexpr (kStages == 4) issue(std::integral_constant<int, 3>{}, 3 < my_rows);
+  }
 
   // ---- query pairs in unpack order: word m (dims 8m..8m+7 of the lane's 32),
   // pair k = (dim 8m+k, dim 8m+k+4); odd k pre-divided by 16
@@ -243,12 +411,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   float qsum[HPB];
 #pragma unroll
   for (int h = 0; h < HPB; ++h) {
-    const int head = h0 + min(h, nh - 1);
-    const uint4* src = reinterpret_cast<const uint4*>(q + ((size_t)b * Hq + head) * D + 32 * j);
     float s = 0.0f;
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
-      const uint4 u = src[m];
+      const uint4 u = qraw[h][m];
       const uint32_t wq[4] = {u.x, u.y, u.z, u.w};
       _Float16 e[8];
 #pragma unroll
@@ -280,99 +446,36 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     for (int i = 0; i < 32; ++i) acc[h][i] = 0.0f;
   }
 
-  // ---- this wave's rows: pages pb + wave, pb + wave + 4, ...; every row of each
-  const int my_pages = (pe - pb - wave + kWaves - 1) / kWaves;
-  const int my_rows = (pe - pb > wave) ? my_pages * rows_per_page : 0;
-  const size_t head_codes = (size_t)P * (D / 2);
-  const size_t page_codes = (size_t)Hkv * head_codes;
-  uint8_t* ring = smem[wave][0];
-  const uint32_t ring_lds = (uint32_t)(uintptr_t)ring;
 
-  // This wave's page IDs, 64 per vector register (lane k holds its k-th page of
-  // the group), read per row with v_readlane: no memory access on the row path.
-  auto load_group = [&](int grp) {
-    const int k = 64 * grp + lane;
-    return (k < my_pages) ? block_tables[(size_t)b * max_pages + pb + wave + k * kWaves] : -1;
-  };
-  int pg_cur = load_group(0), pg_nxt = load_group(1);
-  int grp_cur = 0;
-  auto page_of = [&](int pk) {  // pk: the wave's page index, within groups cur or cur+1
-    const int g2 = pk >> 6;
-    const int v = (g2 == grp_cur) ? __builtin_amdgcn_readlane(pg_cur, pk & 63)
-                                  : __builtin_amdgcn_readlane(pg_nxt, pk & 63);
-    return v;
-  };
-
-  // Issue the loads of row r (of this wave) into stage r % kStages.
-  auto issue_row = [&](int r) {
-    const int s0 = (r % rows_per_page) * ROWPOS;
-    int page = page_of(r / rows_per_page);
-    if ((unsigned)page >= (unsigned)NP) page = 0;  // never read past the pool; masked below
-    uint8_t* st = ring + (r % kStages) * kStageBytes;
-    const uint8_t* kc = k_codes + page * page_codes + kv * head_codes + (size_t)s0 * (D / 2);
-    const uint8_t* vc = v_codes + page * page_codes + kv * head_codes + (size_t)(s0 / 2) * D;
-    dma16(kc + 16 * lane, st);
-    dma16(kc + 1024 + 16 * lane, st + 1024);
-    dma16(vc + 16 * lane, st + 2048);
-    dma16(vc + 1024 + 16 * lane, st + 3072);
-    const size_t mbase = (((size_t)page * Hkv + kv) * P + s0) * NG;
-#pragma unroll
-    for (int i = 0; i < META_DMAS; ++i) {
-      const int w = 64 * i + lane;  // transposed: word w = (group w / ROWPOS, pos w % ROWPOS)
-      const int wi = (w < META_WORDS) ? w : 0;
-      const size_t src = mbase + (size_t)(wi % ROWPOS) * NG + wi / ROWPOS;
-      if (w < META_WORDS) {
-        dma4(k_meta + src, st + kCodeBytes + 256 * i);
-        dma4(v_meta + src, st + kCodeBytes + kMetaBytes / 2 + 256 * i);
-      }
-    }
-  };
-
-  for (int r = 0; r < kStages - 1 && r < my_rows; ++r) issue_row(r);
-
+  // Compute cursor: page index cpk of the wave, row crr of the page.
+  int crr = 0;
+  int t_row = (pb + wave) * P;  // first position of the row
+  const int t_lane = 2 * unit;  // the lane's position pair within a row
+  const uint32_t lds_k = ring_lds + (2 * unit) * (D / 2) + 16 * j;
+  const uint32_t lds_m = ring_lds + kCodeBytes + (g * ROWPOS + 2 * unit) * 4;
+  const uint32_t lds_v = ring_lds + 2048 + unit * D + 32 * j;
   const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
-  for (int r = 0; r < my_rows; ++r) {
-    // rows issued after row r: min(kStages - 1, my_rows - 1 - r); wait until
-    // only those are in flight
-    if (r + kStages - 1 < my_rows) issue_row(r + kStages - 1);
-    const int ahead = min(kStages - 1, my_rows - 1 - r);
-    if (ahead >= 3) {
-      wait_vm<DMAS_PER_ROW * 3>();
-    } else if (ahead == 2) {
-      wait_vm<DMAS_PER_ROW * 2>();
-    } else if (ahead == 1) {
-      wait_vm<DMAS_PER_ROW>();
-    } else {
-      wait_vm<0>();
-    }
-    const int pk = r / rows_per_page;
-    const int pi = pb + wave + pk * kWaves;
-    const int page = page_of(pk);
-    const int t_row = pi * P + (r % rows_per_page) * ROWPOS;
-    if ((r % rows_per_page) == rows_per_page - 1 && ((pk + 1) & 63) == 0) {
-      // leaving page group grp_cur: shift the groups (the ring already holds
-      // rows of the next group, whose IDs come from pg_nxt)
-      grp_cur += 1;
-      pg_cur = pg_nxt;
-      pg_nxt = load_group(grp_cur + 1);
-    }
-    const int t0 = t_row + 2 * unit;
-    const bool pg_ok = (unsigned)page < (unsigned)NP;
-    const bool ok0 = pg_ok && t0 < t_end, ok1 = pg_ok && t0 + 1 < t_end;
 
-    const uint32_t st = ring_lds + (r % kStages) * kStageBytes;
+  int issued_rows = kStages;  // rows whose loads were issued (incl. past the end)
+  auto irr_left_impl = [&]() { return issued_rows++ < my_rows; };
+  auto row = [&](auto st_c) {
+    constexpr int ST = decltype(st_c)::value;
+    // wait until only the kStages - 1 rows after this one are in flight
+    wait_vm<DMAS_PER_ROW * (kStages - 1)>();
+    const bool pg_ok = stage_ok[ST];
+    const bool full = pg_ok && t_row + ROWPOS <= t_end;  // wave-uniform
+    bool ok0 = true, ok1 = true;
+    if (!full) {
+      ok0 = pg_ok && t_row + t_lane < t_end;
+      ok1 = pg_ok && t_row + t_lane + 1 < t_end;
+    }
     uint4 kw0, kw1, vw0, vw1;
     uint2 km, vm;
-#ifdef JF_SPLIT_LDS_READS
-    lds_read_k(st + (2 * unit) * (D / 2) + 16 * j, st + (2 * unit + 1) * (D / 2) + 16 * j,
-               st + kCodeBytes + (g * ROWPOS + 2 * unit) * 4,
-               st + kCodeBytes + kMetaBytes / 2 + (g * ROWPOS + 2 * unit) * 4, kw0, kw1, km, vm);
-#else
-    lds_read_kv(st + (2 * unit) * (D / 2) + 16 * j, st + (2 * unit + 1) * (D / 2) + 16 * j,
-                st + kCodeBytes + (g * ROWPOS + 2 * unit) * 4,
-                st + kCodeBytes + kMetaBytes / 2 + (g * ROWPOS + 2 * unit) * 4,
-                st + 2048 + unit * D + 32 * j, kw0, kw1, km, vm, vw0, vw1);
-#endif
+    lds_read_row<ST * kStageBytes, ST * kStageBytes + D / 2, ST * kStageBytes,
+                 ST * kStageBytes + kMetaBytes / 2, ST * kStageBytes>(lds_k, lds_m, lds_v, kw0,
+                                                                      kw1, km, vm, vw0, vw1);
+    // the stage is in registers now (the read waits for its data): refill it
+    issue(std::integral_constant<int, ST>{}, irr_left_impl());
 
     // ---- QK partial dot products over the lane's 32 dims
     float d0[HPB], d1[HPB];
@@ -399,14 +502,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
     const float sk0 = lo_f(km.x) * kfold, bk0 = hi_f(km.x);
     const float sk1 = lo_f(km.y) * kfold, bk1 = hi_f(km.y);
-    const bool full = pg_ok && t_row + ROWPOS <= t_end;  // wave-uniform
     float v0[HPB], v1[HPB];
 #pragma unroll
     for (int h = 0; h < HPB; ++h) {
       v0[h] = fmaf(sk0, d0[h], bk0 * qsum[h]);
       v1[h] = fmaf(sk1, d1[h], bk1 * qsum[h]);
     }
-    const uint32_t vm0 = ok0 ? vm.x : 0u, vm1 = ok1 ? vm.y : 0u;
+    uint32_t vm0 = vm.x, vm1 = vm.y;
+    if (!full) {
+      vm0 = ok0 ? vm0 : 0u;
+      vm1 = ok1 ? vm1 : 0u;
+    }
     const h2 sv = as_h2(__builtin_amdgcn_perm(vm1, vm0, 0x05040100u));  // (s_t0, s_t1)
     const uint32_t bv = __builtin_amdgcn_perm(vm1, vm0, 0x07060302u);    // (b_t0, b_t1)
     h2 W[HPB];
@@ -435,9 +541,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         sm1 = ok1 ? sm1 : -INFINITY;
       }
       if (__builtin_amdgcn_ballot_w64(fmaxf(sm0, sm1) > thr_mine) != 0) {
-        float mx = fmaxf(sm0, sm1);
-#pragma unroll
-        for (int off = LPP; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        const float mx = xor_max_from(fmaxf(sm0, sm1), LPP);
         float alpha = 1.0f;
         if (mx > m_mine) {  // uniform across the lanes of head j
           alpha = __builtin_amdgcn_exp2f(m_mine - mx);
@@ -477,7 +581,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       if (__builtin_amdgcn_ballot_w64(need) != 0) {
 #pragma unroll
         for (int h = 0; h < HPB; ++h) {
-          const float mx = wave_max(fmaxf(s0[h], s1[h]));
+          const float mx = xor_max_from(fmaxf(s0[h], s1[h]), 1);
           if (mx > m_run[h]) {  // wave-uniform
             const float alpha = __builtin_amdgcn_exp2f(m_run[h] - mx);
             m_run[h] = mx;
@@ -498,9 +602,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         W[h] = pp * sv;
       }
     }
-#ifdef JF_SPLIT_LDS_READS
-    lds_read_v(st + 2048 + unit * D + 32 * j, vw0, vw1);
-#endif
     const uint32_t va[8] = {vw0.x, vw0.y, vw0.z, vw0.w, vw1.x, vw1.y, vw1.z, vw1.w};
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
@@ -513,76 +614,129 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         for (int k = 0; k < 4; ++k)
           acc[h][4 * m + k] = __builtin_amdgcn_fdot2(W[h], as_h2(c[k]), acc[h][4 * m + k], false);
     }
+    // advance the compute cursor
+    t_row += ROWPOS;
+    if (++crr == rows_per_page) {
+      crr = 0;
+      t_row += (kSplitWaves - 1) * P;  // next page of this wave: 4 pages on
+    }
+  };
+
+  for (int r0 = 0; r0 < block_rows; r0 += kStages) {
+#define JF_ROW(ST_)                                                                  \
+    {                                                                                \
+      const int r = r0 + ST_;                                                        \
+      if (r < block_rows) {                                                          \
+        if (r > 0 && r % kBarrierRows == 0) __builtin_amdgcn_s_barrier();            \
+        if (r < my_rows) row(std::integral_constant<int, ST_>{});                    \
+      }                                                                              \
+    }
+    JF_ROW(0)
+    JF_ROW(1)
+    JF_ROW(2)
+    if constexpr (kStages == 4) JF_ROW(3)
+#undef JF_ROW
   }
   wait_vm<0>();
   if constexpr (kLaneHeads) {
 #pragma unroll
-    for (int h = 0; h < HPB; ++h) {
-      m_run[h] = bcast_head<LPP>(m_mine, h);
-      l_acc[h] = bcast_head<LPP>(l_mine, h);
-    }
+    for (int h = 0; h < HPB; ++h) m_run[h] = bcast_head<LPP>(m_mine, h);
   }
-  __syncthreads();  // all waves done with their rings: reuse LDS for the merge
 
-  // ---- merge the units of each wave and the waves of the block
-  float* red = reinterpret_cast<float*>(&smem[0][0][0]);  // [kWaves][UNITS][D]
-  float* red_l = red + kWaves * UNITS * D;                // [kWaves][UNITS]
-  float* red_m = red_l + kWaves * UNITS;                  // [kWaves][HPB]
-  static_assert(sizeof(float) * (kWaves * UNITS * (D + 1) + kWaves * HPB) <=
-                    sizeof(smem), "merge buffer");
-  if (lane == 0) {
-#pragma unroll
-    for (int h = 0; h < HPB; ++h) red_m[wave * HPB + h] = m_run[h];
-  }
-  __syncthreads();
-  const int n_rec = Hq * max_splits;
+  // ---- merge.  Each wave sums its units (lanes of equal j) within 16-lane
+  // rows and writes one partial per row into its own ring, which is idle now;
+  // after one barrier the split's threads add the four waves' partials,
+  // rescaled to the split's maximum.
+  constexpr int kRows = 4;  // 16-lane rows per wave
+  constexpr int kWaveFloats = kStages * kStageBytes / 4;
+  float* part = reinterpret_cast<float*>(ring);   // [kRows][HPB][D] code-unit sums
+  float* part_b = part + kRows * HPB * D;          // [kRows][HPB][LPP] bias sums
+  float* part_l = part_b + kRows * HPB * LPP;      // [kRows][HPB]
+  float* part_m = part_l + kRows * HPB;            // [HPB]
+  static_assert(kRows * HPB * (D + LPP + 1) + HPB <= kWaveFloats, "merge partials fit a ring");
+  // lane-derived indices recomputed here (volatile), so that none of them
+  // stays live through the row loop
+  const int lane_e = lane_id_volatile();
+  const int row16 = lane_e >> 4;
+  const int je = lane_e & 15;
+  const bool writer = je < LPP;  // then je is the lane's j
+  // reduce and store four sums at a time (the scheduling barrier keeps the
+  // rotations from all being issued ahead of the stores, which would need a
+  // second register file's worth of temporaries)
 #pragma unroll
   for (int h = 0; h < HPB; ++h) {
-    float M = -INFINITY;
+    float* dst = part + (row16 * HPB + h) * D + 32 * je;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, red_m[w * HPB + h]);
-    const float f = (m_run[h] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run[h] - M);
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      // undo the 2^-24 (even dims) or 2^-20 (odd dims of each 4) code factor
-      const float cf = (i & 1) ? 1048576.0f : 16777216.0f;
-      red[(wave * UNITS + unit) * D + 32 * j + i] = fmaf(acc[h][i], cf, b_acc[h]) * f;
+    for (int i = 0; i < 32; i += 4) {
+      const float r0 = row_units_sum<LPP>(acc[h][i]), r1 = row_units_sum<LPP>(acc[h][i + 1]);
+      const float r2 = row_units_sum<LPP>(acc[h][i + 2]), r3 = row_units_sum<LPP>(acc[h][i + 3]);
+      if (writer) *reinterpret_cast<float4*>(dst + i) = make_float4(r0, r1, r2, r3);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (j == 0) red_l[wave * UNITS + unit] = l_acc[h] * f;
-    __syncthreads();
-    if (h < nh) {
-      for (int i = tid; i < D; i += kThreads) {
-        float o4[8] = {0, 0, 0, 0, 0, 0, 0, 0}, l4[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    const float bsum = row_units_sum<LPP>(b_acc[h]);
+    if (writer) part_b[(row16 * HPB + h) * LPP + je] = bsum;
+  }
+  if constexpr (kLaneHeads) {
+    const float lsum = row_units_sum<LPP>(l_mine);
+    if (writer) part_l[row16 * HPB + je] = lsum;
+  } else {
 #pragma unroll
-        for (int u = 0; u < kWaves * UNITS; ++u) {  // independent partial sums
-          o4[u & 7] += red[u * D + i];
-          l4[u & 7] += red_l[u];
-        }
-        float o = 0.0f, l = 0.0f;
+    for (int h = 0; h < HPB; ++h) {
+      const float lsum = row_units_sum<LPP>(l_acc[h]);
+      if (writer && je == 0) part_l[row16 * HPB + h] = lsum;
+    }
+  }
+  if (lane_e == 0) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          o += o4[k];
-          l += l4[k];
+    for (int h = 0; h < HPB; ++h) part_m[h] = m_run[h];
+  }
+  __syncthreads();
+
+  if (split_on) {
+    const float* base = reinterpret_cast<const float*>(smem[half * kSplitWaves][0]);
+    for (int o = wave * 64 + lane_e; o < nh * D; o += 64 * kSplitWaves) {
+      const int h = o / D, dd = o % D, jj = dd / 32;
+      // undo the 2^-24 (even dims) or 2^-20 (odd dims of each 4) code factor
+      const float cf = (dd & 1) ? 1048576.0f : 16777216.0f;
+      float mw[kSplitWaves];
+      float M = kMinit;
+#pragma unroll
+      for (int w = 0; w < kSplitWaves; ++w) {
+        mw[w] = base[w * kWaveFloats + kRows * HPB * (D + LPP + 1) + h];
+        M = fmaxf(M, mw[w]);
+      }
+      float num = 0.0f, den = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kSplitWaves; ++w) {
+        const float* pw = base + w * kWaveFloats;
+        float a = 0.0f, bs = 0.0f, ls = 0.0f;
+#pragma unroll
+        for (int rr = 0; rr < kRows; ++rr) {
+          a += pw[(rr * HPB + h) * D + dd];
+          bs += pw[kRows * HPB * D + (rr * HPB + h) * LPP + jj];
+          ls += pw[kRows * HPB * (D + LPP) + rr * HPB + h];
         }
-        float* rec = ws + (((size_t)b * Hq + (h0 + h)) * max_splits + split) * (D + 2);
-        rec[i] = (l > 0.0f) ? o / l : 0.0f;
-        if (i == 0) {
-          rec[D] = M;
-          rec[D + 1] = l;
-        }
+        const float f = __builtin_amdgcn_exp2f(mw[w] - M);
+        num = fmaf(f, fmaf(a, cf, bs), num);
+        den = fmaf(f, ls, den);
+      }
+      float* rec = ws + (((size_t)b * Hq + (h0 + h)) * max_splits + split) * (D + 2);
+      rec[dd] = (den > 0.0f) ? num / den : 0.0f;
+      if (dd == 0) {
+        rec[D] = M;
+        rec[D + 1] = den;
       }
     }
-    __syncthreads();
   }
-  (void)n_rec;
 
 }
 
 // Log-sum-exp combine of a (request, query head)'s split partials (a
 // separate kernel: the kernel boundary makes every split's partial visible,
 // while an in-kernel ticket would need device-scope fences, which write back
-// an XCD's L2 on this GPU).  256 threads: 256/D threads per dim, each summing
-// a strided subset of the splits with independent loads.
+// an XCD's L2 on this GPU).  One round of loads covers up to kCombineThreads /
+// (D / 16) splits: each thread fetches 16 dims of one split's o and that
+// split's (m, l); more splits take further rounds with a running maximum.
 constexpr int kCombineThreads = 512;
 
 template <int D>
@@ -590,10 +744,13 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(
     const float* __restrict__ ws, const int32_t* __restrict__ seq_lens, __half* __restrict__ out,
     int Hq, int P, int max_pages, int max_splits) {
   constexpr int NT = kCombineThreads, NW = NT / 64;
-  constexpr int PARTS = NT / D;
-  __shared__ float s_w[1024];
+  constexpr int TPS = D / 16;      // threads per split
+  constexpr int CH = NT / TPS;     // splits per round
+  constexpr int QP = NT / D;       // threads per dim in the split sum
+  static_assert(CH % QP == 0, "");
+  __shared__ __attribute__((aligned(16))) float s_val[CH][D + 4];
   __shared__ float s_red[NW];
-  __shared__ float s_part[PARTS][D];
+  __shared__ float s_part[QP][D];
   const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int L = min(seq_lens[b], max_pages * P);
@@ -605,61 +762,68 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(
   const int n_pages = (L + P - 1) / P;
   const int S = min(max_splits, n_pages);
   const float* recs = ws + ((size_t)b * Hq + h) * max_splits * (D + 2);
-  // one round of loads for every split's (m, l); S <= 1024
-  float mv[2], lv[2];
-  float M = -INFINITY;
+  const int sl = tid / TPS, part = tid % TPS;  // split within the round, 16-dim part
+  float run_m = -INFINITY, run_den = 0.0f, run_acc = 0.0f;  // run_acc: dim tid (tid < D)
+  for (int s0 = 0; s0 < S; s0 += CH) {
+    const int s = s0 + sl;
+    float o[16];
+    float m = -INFINITY, l = 0.0f;
+    if (s < S) {
+      const float* rec = recs + (size_t)s * (D + 2);
+      const float4* src = reinterpret_cast<const float4*>(rec + 16 * part);
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int s = tid + k * NT;
-    mv[k] = (s < S) ? recs[(size_t)s * (D + 2) + D] : -INFINITY;
-    lv[k] = (s < S) ? recs[(size_t)s * (D + 2) + D + 1] : 0.0f;
-    M = fmaxf(M, mv[k]);
-  }
-  M = wave_max(M);
-  if (lane == 0) s_red[wave] = M;
-  __syncthreads();
-  M = s_red[0];
+      for (int k = 0; k < 4; ++k) {
+        const float4 v = src[k];
+        o[4 * k] = v.x;
+        o[4 * k + 1] = v.y;
+        o[4 * k + 2] = v.z;
+        o[4 * k + 3] = v.w;
+      }
+      m = rec[D];
+      l = rec[D + 1];
+    } else {
 #pragma unroll
-  for (int w = 1; w < NW; ++w) M = fmaxf(M, s_red[w]);
-  float den = 0.0f;
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int s = tid + k * NT;
-    const float w = (s < S && mv[k] != -INFINITY) ? lv[k] * __builtin_amdgcn_exp2f(mv[k] - M) : 0.0f;
-    if (s < S) s_w[s] = w;
-    den += w;
-  }
-  den = wave_sum(den);
-  __syncthreads();  // s_red reads done before it is reused
-  if (lane == 0) s_red[wave] = den;
-  __syncthreads();
-  den = 0.0f;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) den += s_red[w];
-  // weighted sum: thread (part, dim) takes splits part, part+PARTS, ...; 16
-  // independent loads per round
-  const int i = tid % D, part = tid / D;
-  float acc[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) acc[k] = 0.0f;
-  for (int s0 = part; s0 < S; s0 += 16 * PARTS) {
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const int s = s0 + k * PARTS;
-      if (s < S) acc[k] = fmaf(s_w[s], recs[(size_t)s * (D + 2) + i], acc[k]);
+      for (int k = 0; k < 16; ++k) o[k] = 0.0f;
     }
-  }
-  float num = 0.0f;
+    // maximum of the round
+    float mx = wave_max((l > 0.0f) ? m : -INFINITY);
+    if (lane == 0) s_red[wave] = mx;
+    __syncthreads();
+    mx = s_red[0];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) num += acc[k];
-  s_part[part][i] = num;
-  __syncthreads();
-  if (tid < D) {
-    float o = 0.0f;
+    for (int w = 1; w < NW; ++w) mx = fmaxf(mx, s_red[w]);
+    const float M = fmaxf(run_m, mx);
+    const float w_s = (l > 0.0f) ? l * __builtin_amdgcn_exp2f(m - M) : 0.0f;
 #pragma unroll
-    for (int k = 0; k < PARTS; ++k) o += s_part[k][tid];
-    dst[tid] = __float2half_rn((den > 0.0f && M != -INFINITY) ? o / den : 0.0f);
+    for (int k = 0; k < 16; k += 4)
+      *reinterpret_cast<float4*>(&s_val[sl][16 * part + k]) =
+          make_float4(w_s * o[k], w_s * o[k + 1], w_s * o[k + 2], w_s * o[k + 3]);
+    float den = wave_sum(part == 0 ? w_s : 0.0f);
+    __syncthreads();  // s_val complete; s_red reads done
+    if (lane == 0) s_red[wave] = den;
+    {
+      const int d = tid % D, q = tid / D;
+      float acc = 0.0f;
+#pragma unroll 8
+      for (int k = q; k < CH; k += QP) acc += s_val[k][d];
+      s_part[q][d] = acc;
+    }
+    __syncthreads();
+    den = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) den += s_red[w];
+    const float f = (run_m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(run_m - M);
+    run_den = run_den * f + den;
+    if (tid < D) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int q = 0; q < QP; ++q) acc += s_part[q][tid];
+      run_acc = run_acc * f + acc;
+    }
+    run_m = M;
+    __syncthreads();  // before the next round overwrites the shared buffers
   }
+  if (tid < D) dst[tid] = __float2half_rn(run_den > 0.0f ? run_acc / run_den : 0.0f);
 }
 
 template <int D, int G, int HPB>
@@ -669,7 +833,7 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
                     hipStream_t stream) {
   const int gq = Hq / L.num_kv_heads;
   const int n_hchunks = (gq + HPB - 1) / HPB;
-  dim3 grid(max_splits, L.num_kv_heads * n_hchunks, B);
+  dim3 grid((max_splits + 1) / 2, L.num_kv_heads * n_hchunks, B);
   hipLaunchKernelGGL((decode_kernel<D, G, HPB>), grid, dim3(kThreads), 0, stream,
                      static_cast<const uint8_t*>(pool.k_codes),
                      static_cast<const uint32_t*>(pool.k_meta),
