@@ -54,16 +54,11 @@ constexpr float kTau = 2.0f;   // lazy-rescale margin, log2 units
 // Initial running maximum: finite, so that a row with every position masked
 // (-inf logits) before any valid one gives p = 2^(-inf - kMinit) = 0, not NaN.
 constexpr float kMinit = -1e30f;
-constexpr int kThreads = 512;     // 8 waves: two splits of 4 waves, one block per CU
+constexpr int kThreads = 256;     // 4 waves: one split; two blocks per CU
 constexpr int kWaves = kThreads / 64;
-constexpr int kSplitWaves = 4;    // waves per split
+constexpr int kSplitWaves = kWaves;  // waves per split
 constexpr int kCodeBytes = 4096;  // K + V codes of one row (any supported d)
-constexpr int kRingBudget = 163840;  // LDS bytes per block for the rings (all of a CU's LDS)
-// Block barrier every kBarrierRows rows: the two waves that share a SIMD
-// belong to one block, so the barrier keeps them at the same row (the
-// hardware issues oldest-first, which otherwise lets one wave finish long
-// before the other and leaves the SIMD with a single wave at the end).
-constexpr int kBarrierRows = 2;
+constexpr int kRingBudget = 81920;  // LDS bytes per block for the rings (half of a CU's LDS)
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
 __device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uint32_t, v); }
@@ -75,6 +70,22 @@ __device__ __forceinline__ float dot2h(h2 a, uint32_t b, float c) {
 }
 __device__ __forceinline__ float lo_f(uint32_t u) { return (float)as_h2(u).x; }
 __device__ __forceinline__ float hi_f(uint32_t u) { return (float)as_h2(u).y; }
+
+// First product of a dot-product chain: v_dot2 with a zero accumulator (the
+// compiler would otherwise zero a register and accumulate into it).
+__device__ __forceinline__ float dot2_first(uint32_t a, h2 b) {
+  float d;
+  asm("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+// s * n + b * q with s and b the low and high fp16 halves of one (scale,
+// bias) word, converted exactly inside v_fma_mix.
+__device__ __forceinline__ float fold_meta(uint32_t sb, float n, float q) {
+  float t, r;
+  asm("v_fma_mix_f32 %0, %1, %2, 0 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(t) : "v"(sb), "v"(q));
+  asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel_hi:[1,0,0]" : "=v"(r) : "v"(sb), "v"(n), "v"(t));
+  return r;
+}
 
 // Cross-lane sums within aligned groups of 2, 4 or 8 lanes (DPP).
 __device__ __forceinline__ float dpp_f(float v, int ctrl) {
@@ -197,22 +208,23 @@ __device__ __forceinline__ void lds_read_kv(uint32_t k0_addr, uint32_t k1_addr, 
 }
 // All reads of one staged row at compile-time offsets from three per-lane
 // bases (K codes, meta words, V codes), waited for once.
-template <int K0, int K1, int KM, int VM, int V0>
-__device__ __forceinline__ void lds_read_row(uint32_t k_addr, uint32_t m_addr, uint32_t v_addr,
-                                             uint4& k0, uint4& k1, uint2& km, uint2& vm, uint4& v0,
+template <int OFF, int VM>
+__device__ __forceinline__ void lds_read_row(uint32_t k0_addr, uint32_t k1_addr, uint32_t m_addr,
+                                             uint32_t v0_addr, uint32_t v1_addr, uint4& k0,
+                                             uint4& k1, uint2& km, uint2& vm, uint4& v0,
                                              uint4& v1) {
-  static_assert(K0 >= 0 && V0 + 16 < 65536 && KM < 65536 && VM < 65536, "ds offsets");
+  static_assert(OFF >= 0 && OFF + VM < 65536, "ds offsets");
   asm volatile(
-      "ds_read_b128 %0, %6 offset:%9\n\t"
-      "ds_read_b128 %1, %6 offset:%10\n\t"
-      "ds_read_b64 %2, %7 offset:%11\n\t"
-      "ds_read_b64 %3, %7 offset:%12\n\t"
-      "ds_read_b128 %4, %8 offset:%13\n\t"
-      "ds_read_b128 %5, %8 offset:%14\n\t"
+      "ds_read_b128 %0, %6 offset:%11\n\t"
+      "ds_read_b128 %1, %7 offset:%11\n\t"
+      "ds_read_b64 %2, %8 offset:%11\n\t"
+      "ds_read_b64 %3, %8 offset:%12\n\t"
+      "ds_read_b128 %4, %9 offset:%11\n\t"
+      "ds_read_b128 %5, %10 offset:%11\n\t"
       "s_waitcnt lgkmcnt(0)"
       : "=&v"(k0), "=&v"(k1), "=&v"(km), "=&v"(vm), "=&v"(v0), "=&v"(v1)
-      : "v"(k_addr), "v"(m_addr), "v"(v_addr), "i"(K0), "i"(K1), "i"(KM), "i"(VM), "i"(V0),
-        "i"(V0 + 16)
+      : "v"(k0_addr), "v"(k1_addr), "v"(m_addr), "v"(v0_addr), "v"(v1_addr), "i"(OFF),
+        "i"(OFF + VM)
       : "memory");
 }
 __device__ __forceinline__ void lds_read_v(uint32_t v_addr, uint4& v0, uint4& v1) {
@@ -230,7 +242,7 @@ __device__ __forceinline__ void lds_read_v(uint32_t v_addr, uint4& v0, uint4& v1
 template <int N>
 __device__ __forceinline__ float row_ror_add(float v) {
   return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
-                                                                   0x120 + N, 0xF, 0xF, false));
+                                                                   0x120 + N, 0xF, 0xF, true));
 }
 template <int LPP>
 __device__ __forceinline__ float row_units_sum(float v) {
@@ -280,48 +292,29 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int nh = min(HPB, gq - hc * HPB);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave_blk = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
-  const int half = wave_blk / kSplitWaves;
-  const int wave = wave_blk % kSplitWaves;  // wave within its split
-  const int split = 2 * blockIdx.x + half;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int split = blockIdx.x;
 
   const int L = min(seq_lens[b], max_pages * P);
   if (L <= 0) return;  // the combine writes the all-zero output row
   const int n_pages = (L + P - 1) / P;
   const int S = min(max_splits, n_pages);
-  if (2 * (int)blockIdx.x >= S) return;  // both splits of the block are empty
-  const bool split_on = split < S;  // else this half only joins the barriers
-  int pb = 0, pe = 0;
-  if (split_on) split_range(n_pages, S, split, pb, pe);
+  if (split >= S) return;
+  int pb, pe;
+  split_range(n_pages, S, split, pb, pe);
   const int t_end = min(pe * P, L);
   const int rows_per_page = P / ROWPOS;
-  // rows of the block's busiest wave (the first split has the most pages)
-  int pb_first, pe_first;
-  split_range(n_pages, S, 2 * blockIdx.x, pb_first, pe_first);
-  const int block_rows =
-      ((pe_first - pb_first + kSplitWaves - 1) / kSplitWaves) * rows_per_page;
 
   const int unit = lane / LPP;
   const int j = lane % LPP;
   const int g = (32 * j) / G;  // the lane's scale group
-
-  // query words of the lane's 32 dims for each head (loaded now, unpacked
-  // after the first rows' loads are in flight)
-  uint4 qraw[HPB][4];
-#pragma unroll
-  for (int h = 0; h < HPB; ++h) {
-    const int head = h0 + min(h, nh - 1);
-    const uint4* src = reinterpret_cast<const uint4*>(q + ((size_t)b * Hq + head) * D + 32 * j);
-#pragma unroll
-    for (int m = 0; m < 4; ++m) qraw[h][m] = src[m];
-  }
 
   // ---- this wave's rows: pages pb + wave, pb + wave + 4, ...; every row of each
   const int my_pages = (pe - pb - wave + kSplitWaves - 1) / kSplitWaves;
   const int my_rows = (pe - pb > wave) ? my_pages * rows_per_page : 0;
   const size_t head_codes = (size_t)P * (D / 2);
   const size_t page_codes = (size_t)Hkv * head_codes;
-  uint8_t* ring = smem[wave_blk][0];
+  uint8_t* ring = smem[wave][0];
   const uint32_t ring_lds = (uint32_t)(uintptr_t)ring;
 
   // This wave's page IDs, 64 per vector register (lane k holds its k-th page),
@@ -332,14 +325,36 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   };
   int pg_grp = load_group(0);
 
+  // query words of the lane's 32 dims for each head (loaded with the page
+  // IDs, unpacked once the first rows' loads are in flight)
+  // Slot k of lane j holds head j ^ k when lane j owns head j's softmax
+  // (then the reduce-scatter of the unit needs no selects), else head k.
+  uint4 qraw[HPB][4];
+#pragma unroll
+  for (int h = 0; h < HPB; ++h) {
+    const int head = h0 + min(kLaneHeads ? (j ^ h) : h, nh - 1);
+    const uint4* src = reinterpret_cast<const uint4*>(q + ((size_t)b * Hq + head) * D + 32 * j);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) qraw[h][m] = src[m];
+  }
+
   // Per-lane parts of the load addresses (the row parts are scalar).
-  const uint32_t code_off = 16 * lane;
-  uint32_t meta_off[META_DMAS];  // transposed: word w = (group w / ROWPOS, pos w % ROWPOS)
+  // LDS placement (d = 128): a DMA lane stores 16 bytes at 16 * lane, so the
+  // chunk a lane fetches decides the LDS layout.  K: odd units (position
+  // pairs) swap their two positions; V: odd units swap the two 16-byte halves
+  // of each lane's 32 bytes; meta: odd groups XOR the position with ROWPOS/2.
+  // Each read instruction then spreads its 16-lane passes over all 32 banks.
+  constexpr bool kSwizzle = (D == 128);
+  const uint32_t k_off = 16u * (kSwizzle ? (lane ^ ((lane >> 1) & 4)) : lane);
+  const uint32_t v_off = 16u * (kSwizzle ? (lane ^ ((lane >> 3) & 1)) : lane);
+  uint32_t meta_off[META_DMAS];  // LDS word w = (group w / ROWPOS, slot w % ROWPOS)
 #pragma unroll
   for (int i = 0; i < META_DMAS; ++i) {
     const int w = 64 * i + lane;
     const int wi = (w < META_WORDS) ? w : 0;
-    meta_off[i] = 4u * (uint32_t)((wi % ROWPOS) * NG + wi / ROWPOS);
+    const int grp = wi / ROWPOS;
+    const int pos = (wi % ROWPOS) ^ ((grp & 1) * (ROWPOS / 2));
+    meta_off[i] = 4u * (uint32_t)(pos * NG + grp);
   }
 
   // Issue cursor: the next row to load (page index ipk of the wave, row irr
@@ -350,7 +365,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   size_t im = 0;  // byte offset of the row's (scale, bias) words in k_meta / v_meta
   bool iok = false;
   auto enter_page = [&]() {
-    if ((ipk & 63) == 0 && ipk > 0) pg_grp = load_group(ipk >> 6);  // > 64 pages per wave
+    if ((ipk & 63) == 0 && ipk > 0) {  // more than 64 pages per wave: next 64 IDs
+      pg_grp = load_group(ipk >> 6);
+      wait_vm<0>();  // here, so that the common path carries no pending load
+    }
     int page = __builtin_amdgcn_readlane(pg_grp, ipk & 63);
     iok = (unsigned)page < (unsigned)NP;
     if (!iok) page = 0;  // never read past the pool; the positions are masked
@@ -366,10 +384,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     constexpr int ST = decltype(st_c)::value;
     uint8_t* st = ring + ST * kStageBytes;
     if (real) {
-      dma16(ik + code_off, st);
-      dma16(ik + 1024 + code_off, st + 1024);
-      dma16(iv + code_off, st + 2048);
-      dma16(iv + 1024 + code_off, st + 3072);
+      dma16(ik + k_off, st);
+      dma16(ik + 1024 + k_off, st + 1024);
+      dma16(iv + v_off, st + 2048);
+      dma16(iv + 1024 + v_off, st + 3072);
       const uint8_t* km8 = reinterpret_cast<const uint8_t*>(k_meta) + im;
       const uint8_t* vm8 = reinterpret_cast<const uint8_t*>(v_meta) + im;
 #pragma unroll
@@ -395,6 +413,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       stage_ok[ST] = false;
     }
   };
+  wait_vm<0>();  // page IDs and query words (issued together) have arrived
   if (my_rows > 0) enter_page();
   // All stages are in flight while a row is computed: a row's stage is read
   // into registers first and then refilled with the row kStages ahead.
@@ -429,10 +448,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         s += (float)e[k] + (float)e[k + 4];
       }
     }
-    qsum[h] = s * scale_log2;
+    qsum[h] = kLaneHeads ? s * (1.0f / 16777216.0f) : s * scale_log2;
   }
-  // logit (log2 units) = kscale * raw_dot + bias * qsum
+  // logit (log2 units) = kfold * (scale * raw_dot + bias * qsum * 2^-24) in the
+  // lane-heads path; kfold * scale * raw_dot + bias * qsum otherwise
   const float kfold = 16777216.0f * scale_log2;  // 2^24
+  // Lane-heads path: query sums over the dims that share a scale group with
+  // the lane, for the slots whose scale/bias fold happens after the group's
+  // lanes are summed (G = 64: slots 0 and 2 after one step; G = 128: slot 0
+  // after two steps).
+  if constexpr (kLaneHeads && LPP == 4 && G >= 64) {
+    qsum[0] += dpp_f(qsum[1], 0xB1);
+    qsum[2] += dpp_f(qsum[3], 0xB1);
+    if constexpr (G >= 128) qsum[0] += dpp_f(qsum[2], 0x4E);
+  }
+  if constexpr (kLaneHeads && LPP == 2 && G >= 64) qsum[0] += dpp_f(qsum[1], 0xB1);
 
   float m_mine = kMinit, thr_mine = kMinit, l_mine = 0.0f;  // head j (kLaneHeads)
   float m_run[HPB], l_acc[HPB], b_acc[HPB];
@@ -451,9 +481,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   int crr = 0;
   int t_row = (pb + wave) * P;  // first position of the row
   const int t_lane = 2 * unit;  // the lane's position pair within a row
-  const uint32_t lds_k = ring_lds + (2 * unit) * (D / 2) + 16 * j;
-  const uint32_t lds_m = ring_lds + kCodeBytes + (g * ROWPOS + 2 * unit) * 4;
-  const uint32_t lds_v = ring_lds + 2048 + unit * D + 32 * j;
+  const int odd_unit = kSwizzle ? (unit & 1) : 0;
+  const uint32_t lds_k0 = ring_lds + (2 * unit) * (D / 2) + 16 * j + 64 * odd_unit;
+  const uint32_t lds_k1 = ring_lds + (2 * unit + 1) * (D / 2) + 16 * j - 64 * odd_unit;
+  const uint32_t lds_m =
+      ring_lds + kCodeBytes + (g * ROWPOS + ((2 * unit) ^ ((g & 1) * (ROWPOS / 2)))) * 4;
+  const uint32_t lds_v0 = ring_lds + 2048 + unit * D + 32 * j + 16 * odd_unit;
+  const uint32_t lds_v1 = ring_lds + 2048 + unit * D + 32 * j + 16 - 16 * odd_unit;
   const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
 
   int issued_rows = kStages;  // rows whose loads were issued (incl. past the end)
@@ -471,16 +505,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
     uint4 kw0, kw1, vw0, vw1;
     uint2 km, vm;
-    lds_read_row<ST * kStageBytes, ST * kStageBytes + D / 2, ST * kStageBytes,
-                 ST * kStageBytes + kMetaBytes / 2, ST * kStageBytes>(lds_k, lds_m, lds_v, kw0,
-                                                                      kw1, km, vm, vw0, vw1);
+    lds_read_row<ST * kStageBytes, kMetaBytes / 2>(lds_k0, lds_k1, lds_m, lds_v0, lds_v1, kw0, kw1,
+                                                   km, vm, vw0, vw1);
     // the stage is in registers now (the read waits for its data): refill it
     issue(std::integral_constant<int, ST>{}, irr_left_impl());
 
     // ---- QK partial dot products over the lane's 32 dims
     float d0[HPB], d1[HPB];
-#pragma unroll
-    for (int h = 0; h < HPB; ++h) d0[h] = d1[h] = 0.0f;
     {
       const uint32_t ka[4] = {kw0.x, kw0.y, kw0.z, kw0.w};
       const uint32_t kb[4] = {kw1.x, kw1.y, kw1.z, kw1.w};
@@ -495,18 +526,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         for (int h = 0; h < HPB; ++h)
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            d0[h] = dot2(ca[k], qp[h][m][k], d0[h]);
-            d1[h] = dot2(cb[k], qp[h][m][k], d1[h]);
+            if (m == 0 && k == 0) {
+              d0[h] = dot2_first(ca[k], qp[h][m][k]);
+              d1[h] = dot2_first(cb[k], qp[h][m][k]);
+            } else {
+              d0[h] = dot2(ca[k], qp[h][m][k], d0[h]);
+              d1[h] = dot2(cb[k], qp[h][m][k], d1[h]);
+            }
           }
       }
     }
-    const float sk0 = lo_f(km.x) * kfold, bk0 = hi_f(km.x);
-    const float sk1 = lo_f(km.y) * kfold, bk1 = hi_f(km.y);
     float v0[HPB], v1[HPB];
+    if constexpr (!kLaneHeads) {
+      const float sk0 = lo_f(km.x) * kfold, bk0 = hi_f(km.x);
+      const float sk1 = lo_f(km.y) * kfold, bk1 = hi_f(km.y);
 #pragma unroll
-    for (int h = 0; h < HPB; ++h) {
-      v0[h] = fmaf(sk0, d0[h], bk0 * qsum[h]);
-      v1[h] = fmaf(sk1, d1[h], bk1 * qsum[h]);
+      for (int h = 0; h < HPB; ++h) {
+        v0[h] = fmaf(sk0, d0[h], bk0 * qsum[h]);
+        v1[h] = fmaf(sk1, d1[h], bk1 * qsum[h]);
+      }
     }
     uint32_t vm0 = vm.x, vm1 = vm.y;
     if (!full) {
@@ -517,25 +555,52 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const uint32_t bv = __builtin_amdgcn_perm(vm1, vm0, 0x07060302u);    // (b_t0, b_t1)
     h2 W[HPB];
     if constexpr (kLaneHeads) {
-      // reduce-scatter over the unit: lane j keeps the full logits of head j
+      // reduce-scatter over the unit (lane j keeps head j = slot 0), folding
+      // each group's scale and bias in once the lanes of that group are summed
       float sm0, sm1;
       if constexpr (LPP == 4) {
-        const bool odd = j & 1, hi = j & 2;
-        float k00 = odd ? v0[1] : v0[0], k01 = odd ? v0[3] : v0[2];
-        float k10 = odd ? v1[1] : v1[0], k11 = odd ? v1[3] : v1[2];
-        const float s00 = odd ? v0[0] : v0[1], s01 = odd ? v0[2] : v0[3];
-        const float s10 = odd ? v1[0] : v1[1], s11 = odd ? v1[2] : v1[3];
-        k00 += dpp_f(s00, 0xB1);
-        k01 += dpp_f(s01, 0xB1);
-        k10 += dpp_f(s10, 0xB1);
-        k11 += dpp_f(s11, 0xB1);
-        sm0 = (hi ? k01 : k00) + dpp_f(hi ? k00 : k01, 0x4E);
-        sm1 = (hi ? k11 : k10) + dpp_f(hi ? k10 : k11, 0x4E);
+        float e0[4], e1[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          e0[k] = d0[k];
+          e1[k] = d1[k];
+          if constexpr (G == 32) {
+            e0[k] = fold_meta(km.x, e0[k], qsum[k]);
+            e1[k] = fold_meta(km.y, e1[k], qsum[k]);
+          }
+        }
+        float n00 = e0[0] + dpp_f(e0[1], 0xB1), n02 = e0[2] + dpp_f(e0[3], 0xB1);
+        float n10 = e1[0] + dpp_f(e1[1], 0xB1), n12 = e1[2] + dpp_f(e1[3], 0xB1);
+        if constexpr (G == 64) {
+          n00 = fold_meta(km.x, n00, qsum[0]);
+          n02 = fold_meta(km.x, n02, qsum[2]);
+          n10 = fold_meta(km.y, n10, qsum[0]);
+          n12 = fold_meta(km.y, n12, qsum[2]);
+        }
+        sm0 = n00 + dpp_f(n02, 0x4E);
+        sm1 = n10 + dpp_f(n12, 0x4E);
+        if constexpr (G >= 128) {
+          sm0 = fold_meta(km.x, sm0, qsum[0]);
+          sm1 = fold_meta(km.y, sm1, qsum[0]);
+        }
       } else {  // LPP == 2
-        const bool odd = j & 1;
-        sm0 = (odd ? v0[1] : v0[0]) + dpp_f(odd ? v0[0] : v0[1], 0xB1);
-        sm1 = (odd ? v1[1] : v1[0]) + dpp_f(odd ? v1[0] : v1[1], 0xB1);
+        float e0[2] = {d0[0], d0[1]}, e1[2] = {d1[0], d1[1]};
+        if constexpr (G == 32) {
+#pragma unroll
+          for (int k = 0; k < 2; ++k) {
+            e0[k] = fold_meta(km.x, e0[k], qsum[k]);
+            e1[k] = fold_meta(km.y, e1[k], qsum[k]);
+          }
+        }
+        sm0 = e0[0] + dpp_f(e0[1], 0xB1);
+        sm1 = e1[0] + dpp_f(e1[1], 0xB1);
+        if constexpr (G >= 64) {
+          sm0 = fold_meta(km.x, sm0, qsum[0]);
+          sm1 = fold_meta(km.y, sm1, qsum[0]);
+        }
       }
+      sm0 *= kfold;
+      sm1 *= kfold;
       if (!full) {
         sm0 = ok0 ? sm0 : -INFINITY;
         sm1 = ok1 ? sm1 : -INFINITY;
@@ -622,20 +687,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
   };
 
-  for (int r0 = 0; r0 < block_rows; r0 += kStages) {
-#define JF_ROW(ST_)                                                                  \
-    {                                                                                \
-      const int r = r0 + ST_;                                                        \
-      if (r < block_rows) {                                                          \
-        if (r > 0 && r % kBarrierRows == 0) __builtin_amdgcn_s_barrier();            \
-        if (r < my_rows) row(std::integral_constant<int, ST_>{});                    \
-      }                                                                              \
+  for (int r0 = 0; r0 < my_rows; r0 += kStages) {
+    row(std::integral_constant<int, 0>{});
+    if (r0 + 1 < my_rows) row(std::integral_constant<int, 1>{});
+    if (r0 + 2 < my_rows) row(std::integral_constant<int, 2>{});
+    if constexpr (kStages == 4) {
+      if (r0 + 3 < my_rows) row(std::integral_constant<int, 3>{});
     }
-    JF_ROW(0)
-    JF_ROW(1)
-    JF_ROW(2)
-    if constexpr (kStages == 4) JF_ROW(3)
-#undef JF_ROW
   }
   wait_vm<0>();
   if constexpr (kLaneHeads) {
@@ -692,8 +750,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   }
   __syncthreads();
 
-  if (split_on) {
-    const float* base = reinterpret_cast<const float*>(smem[half * kSplitWaves][0]);
+  {
+    const float* base = reinterpret_cast<const float*>(smem[0][0]);
     for (int o = wave * 64 + lane_e; o < nh * D; o += 64 * kSplitWaves) {
       const int h = o / D, dd = o % D, jj = dd / 32;
       // undo the 2^-24 (even dims) or 2^-20 (odd dims of each 4) code factor
@@ -833,7 +891,7 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
                     hipStream_t stream) {
   const int gq = Hq / L.num_kv_heads;
   const int n_hchunks = (gq + HPB - 1) / HPB;
-  dim3 grid((max_splits + 1) / 2, L.num_kv_heads * n_hchunks, B);
+  dim3 grid(max_splits, L.num_kv_heads * n_hchunks, B);
   hipLaunchKernelGGL((decode_kernel<D, G, HPB>), grid, dim3(kThreads), 0, stream,
                      static_cast<const uint8_t*>(pool.k_codes),
                      static_cast<const uint32_t*>(pool.k_meta),
