@@ -208,15 +208,19 @@ jf_status jf_kv_quantize_append(const jf_kv_layout* layout,
                                 int32_t max_pages, int32_t total_tok,
                                 hipStream_t stream);
 
-/* Workspace bytes jf_decode_attn_q4 needs: B * num_q_heads * max_splits *
- * (head_dim + 2) * 4 bytes of fp32 partials (o, m, l per split).  It does not
- * depend on sequence lengths. */
+/* Workspace bytes jf_decode_attn_q4 needs: a fixed 262,144-byte region of
+ * completion counters (room for B * num_q_heads <= 65,536; larger products
+ * return JF_ERR_UNSUPPORTED), then B * num_q_heads * max_splits *
+ * (head_dim + 4) * 4 bytes of fp32 partials (o/l, m, l per split, padded to
+ * 16-byte records).  It does
+ * not depend on sequence lengths. */
 jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads,
                                     int32_t head_dim, int32_t max_splits,
                                     size_t* bytes);
 
-/* Single-query decode attention over the paged 4-bit cache (split-K, then a
- * log-sum-exp combine of the partials; two kernels on `stream`).
+/* Single-query decode attention over the paged 4-bit cache: split-K
+ * partials, then a log-sum-exp combine done by the last split of each
+ * (request, KV head) to finish; one kernel on `stream`.
  *   q            fp16 [B][num_q_heads][d] (device)
  *   block_tables int32 [B][max_pages] (device)
  *   seq_lens     int32 [B] (device): request b attends to its logical
@@ -227,8 +231,12 @@ jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads,
  *   max_splits   cap on partials per request and KV head (1..1024); a
  *                request with n pages uses min(max_splits, n) page-aligned
  *                splits of equal page counts, the remainder on the first
- *   workspace    device scratch of at least jf_decode_workspace_bytes(), no
- *                initialization needed; concurrent calls must not share one
+ *   workspace    device scratch of at least jf_decode_workspace_bytes().
+ *                Its first 262,144 bytes (completion counters) must be zero
+ *                before the first call, e.g. by allocating it zero-filled;
+ *                every call that completes leaves them zero, so the same
+ *                workspace serves any later call of any shape that fits.
+ *                Calls that may overlap in time must not share one.
  *   out          fp16 [B][num_q_heads][d] (device)
  * Page IDs outside [0, num_pages) are never dereferenced; the positions
  * they would hold do not contribute. */

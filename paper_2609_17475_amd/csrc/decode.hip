@@ -259,13 +259,95 @@ __device__ __forceinline__ void split_range(int n_pages, int S, int s, int& pb, 
   pe = pb + base + (s < rem ? 1 : 0);
 }
 
+// Coherent (sc1: device-scope) buffer loads of split records; the resource
+// covers one head's records, so every access is bounds-checked by the
+// hardware as well.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+constexpr int kCpolSc1 = 16;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t records_rsrc(const float* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+// Log-sum-exp combine of the split records of heads h0 .. h0+nh-1 (nh <= 4)
+// of request b: M = max m_s, w_s = l_s 2^(m_s - M), o = sum w_s o_s / sum w_s.
+// Wave w combines head w: lane (c, k) holds dims 4c..4c+3 and the splits
+// s = k, k + KP, ... (KP = 64 / (D/4)), fetched KCH at a time with coherent
+// loads and folded into a running maximum; the KP parts meet by shuffles.
+// Records: [max_splits][D + 4] fp32 per head (o/l in 0..D-1, m at D, l at
+// D+1).
+template <int D>
+__device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int h0, int nh,
+                               int max_splits, int S) {
+  constexpr int CPL = D / 4;      // float4 chunks of a record's o
+  constexpr int KP = 64 / CPL;    // lanes per chunk (split parts)
+  constexpr int KCH = 8;          // splits per lane per round
+  static_assert(KP >= 1 && 64 % CPL == 0, "");
+  const int lane = threadIdx.x & 63, h = threadIdx.x >> 6;
+  if (h >= nh) return;
+  const int c = lane % CPL, k = lane / CPL;
+  const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (D + 4);
+  const __amdgpu_buffer_rsrc_t rs = records_rsrc(recs, (uint32_t)S * (D + 4) * 4);
+  float m_run = -INFINITY, den = 0.0f;
+  float num[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int s0 = k; s0 < S; s0 += KP * KCH) {
+    f32x4 o[KCH];
+    f32x2 ml[KCH];
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const int s = min(s0 + KP * i, S - 1);  // past the end: a valid record, weight 0
+      o[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (s * (D + 4) + 4 * c) * 4, 0, kCpolSc1);
+      ml[i] = __builtin_amdgcn_raw_buffer_load_b64(rs, (s * (D + 4) + D) * 4, 0, kCpolSc1);
+    }
+    float mx = m_run;
+#pragma unroll
+    for (int i = 0; i < KCH; ++i)
+      if (s0 + KP * i < S && ml[i].y > 0.0f) mx = fmaxf(mx, ml[i].x);
+    const float f = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - mx);
+    den *= f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) num[e] *= f;
+#pragma unroll
+    for (int i = 0; i < KCH; ++i) {
+      const bool on = s0 + KP * i < S && ml[i].y > 0.0f;
+      const float w = on ? ml[i].y * __builtin_amdgcn_exp2f(ml[i].x - mx) : 0.0f;
+      den += w;
+      num[0] = fmaf(w, o[i].x, num[0]);
+      num[1] = fmaf(w, o[i].y, num[1]);
+      num[2] = fmaf(w, o[i].z, num[2]);
+      num[3] = fmaf(w, o[i].w, num[3]);
+    }
+    m_run = mx;
+  }
+  // merge the KP parts of each chunk (lanes c, c + CPL, ...)
+#pragma unroll
+  for (int off = CPL; off < 64; off <<= 1) {
+    const float mo = __shfl_xor(m_run, off);
+    const float M = fmaxf(m_run, mo);
+    const float fa = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - M);
+    const float fb = (mo == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mo - M);
+    den = den * fa + __shfl_xor(den, off) * fb;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) num[e] = num[e] * fa + __shfl_xor(num[e], off) * fb;
+    m_run = M;
+  }
+  if (k == 0) {
+    const float r = den > 0.0f ? 1.0f / den : 0.0f;
+    __half2* dst = reinterpret_cast<__half2*>(out + ((size_t)b * Hq + h0 + h) * D + 4 * c);
+    dst[0] = __floats2half2_rn(num[0] * r, num[1] * r);
+    dst[1] = __floats2half2_rn(num[2] * r, num[3] * r);
+  }
+}
+
 template <int D, int G, int HPB>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void decode_kernel(
     const uint8_t* __restrict__ k_codes, const uint32_t* __restrict__ k_meta,
     const uint8_t* __restrict__ v_codes, const uint32_t* __restrict__ v_meta,
     const __half* __restrict__ q, const int32_t* __restrict__ block_tables,
-    const int32_t* __restrict__ seq_lens, float* __restrict__ ws, int Hq, int Hkv, int P, int NP,
-    int max_pages, int max_splits, int n_hchunks, float scale_log2) {
+    const int32_t* __restrict__ seq_lens, float* __restrict__ ws, uint32_t* __restrict__ tickets,
+    __half* __restrict__ out, int Hq, int Hkv, int P, int NP, int max_pages, int max_splits,
+    int n_hchunks, float scale_log2) {
   constexpr int LPP = D / 32;            // lanes per position pair (unit)
   constexpr int UNITS = 64 / LPP;        // units per wave
   constexpr int ROWPOS = 2 * UNITS;      // positions per row
@@ -296,7 +378,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int split = blockIdx.x;
 
   const int L = min(seq_lens[b], max_pages * P);
-  if (L <= 0) return;  // the combine writes the all-zero output row
+  if (L <= 0) {  // an empty request: all-zero output rows, written by split 0
+    if (split == 0)
+      for (int i = tid; i < nh * D; i += kThreads)
+        out[((size_t)b * Hq + h0) * D + i] = __float2half(0.0f);
+    return;
+  }
   const int n_pages = (L + P - 1) / P;
   const int S = min(max_splits, n_pages);
   if (split >= S) return;
@@ -309,21 +396,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const int j = lane % LPP;
   const int g = (32 * j) / G;  // the lane's scale group
 
-  // ---- this wave's rows: pages pb + wave, pb + wave + 4, ...; every row of each
-  const int my_pages = (pe - pb - wave + kSplitWaves - 1) / kSplitWaves;
-  const int my_rows = (pe - pb > wave) ? my_pages * rows_per_page : 0;
+  // ---- this wave's rows: the split's rows in page order, g = wave, wave + 4,
+  // ... (the four waves read neighbouring rows of one page at a time)
+  const int n_split_pages = pe - pb;
+  const int split_rows = n_split_pages * rows_per_page;
+  const int my_rows = (split_rows > wave) ? (split_rows - wave + kSplitWaves - 1) / kSplitWaves : 0;
   const size_t head_codes = (size_t)P * (D / 2);
   const size_t page_codes = (size_t)Hkv * head_codes;
   uint8_t* ring = smem[wave][0];
   const uint32_t ring_lds = (uint32_t)(uintptr_t)ring;
 
-  // This wave's page IDs, 64 per vector register (lane k holds its k-th page),
-  // read with v_readlane when the issue cursor enters a page.
+  // The split's page IDs, 64 per vector register (lane k holds page pb + k of
+  // the group), read with v_readlane when the issue cursor enters a page.
   auto load_group = [&](int grp) {
     const int k = 64 * grp + lane;
-    return (k < my_pages) ? block_tables[(size_t)b * max_pages + pb + wave + k * kSplitWaves] : -1;
+    return (k < n_split_pages) ? block_tables[(size_t)b * max_pages + pb + k] : -1;
   };
   int pg_grp = load_group(0);
+  int cur_grp = 0;
 
   // query words of the lane's 32 dims for each head (loaded with the page
   // IDs, unpacked once the first rows' loads are in flight)
@@ -357,24 +447,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     meta_off[i] = 4u * (uint32_t)(pos * NG + grp);
   }
 
-  // Issue cursor: the next row to load (page index ipk of the wave, row irr
-  // of the page) and the scalar addresses of that row.
-  int ipk = 0, irr = 0;
+  // Issue cursor: the next row to load (page ipk of the split, row irr of the
+  // page) and the scalar addresses of that row.
+  int ipk = wave / rows_per_page, irr = wave % rows_per_page;
   const uint8_t* ik = k_codes;
   const uint8_t* iv = v_codes;
   size_t im = 0;  // byte offset of the row's (scale, bias) words in k_meta / v_meta
   bool iok = false;
   auto enter_page = [&]() {
-    if ((ipk & 63) == 0 && ipk > 0) {  // more than 64 pages per wave: next 64 IDs
-      pg_grp = load_group(ipk >> 6);
+    if ((ipk >> 6) != cur_grp) {  // more than 64 pages per split: next 64 IDs
+      cur_grp = ipk >> 6;
+      pg_grp = load_group(cur_grp);
       wait_vm<0>();  // here, so that the common path carries no pending load
     }
     int page = __builtin_amdgcn_readlane(pg_grp, ipk & 63);
     iok = (unsigned)page < (unsigned)NP;
     if (!iok) page = 0;  // never read past the pool; the positions are masked
-    ik = k_codes + page * page_codes + kv * head_codes;
-    iv = v_codes + page * page_codes + kv * head_codes;
-    im = (((size_t)page * Hkv + kv) * P) * NG * 4;
+    ik = k_codes + page * page_codes + kv * head_codes + (size_t)irr * ROWPOS * (D / 2);
+    iv = v_codes + page * page_codes + kv * head_codes + (size_t)irr * ROWPOS * (D / 2);
+    im = ((((size_t)page * Hkv + kv) * P) + (size_t)irr * ROWPOS) * NG * 4;
   };
   bool stage_ok[kStages];
   // Loads of the next row into stage ST; past the wave's last row, loads of
@@ -396,14 +487,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         dma4(vm8 + meta_off[i], st + kCodeBytes + kMetaBytes / 2 + 256 * i);
       }
       stage_ok[ST] = iok;
-      // advance the cursor
-      ik += ROWPOS * (D / 2);
-      iv += ROWPOS * (D / 2);
-      im += ROWPOS * NG * 4;
-      if (++irr == rows_per_page) {
-        irr = 0;
-        ++ipk;
-        if (ipk < my_pages) enter_page();
+      // advance the cursor by kSplitWaves rows
+      irr += kSplitWaves;
+      if (irr < rows_per_page) {
+        ik += kSplitWaves * ROWPOS * (D / 2);
+        iv += kSplitWaves * ROWPOS * (D / 2);
+        im += kSplitWaves * ROWPOS * NG * 4;
+      } else {
+        do {
+          irr -= rows_per_page;
+          ++ipk;
+        } while (irr >= rows_per_page);
+        if (ipk < n_split_pages) enter_page();
       }
     } else {
 #pragma unroll
@@ -477,9 +572,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   }
 
 
-  // Compute cursor: page index cpk of the wave, row crr of the page.
-  int crr = 0;
-  int t_row = (pb + wave) * P;  // first position of the row
+  // Compute cursor: the first (logical) position of the row; the split's
+  // pages are consecutive logical pages, so row g starts at pb * P + g * ROWPOS.
+  int t_row = pb * P + wave * ROWPOS;
   const int t_lane = 2 * unit;  // the lane's position pair within a row
   const int odd_unit = kSwizzle ? (unit & 1) : 0;
   const uint32_t lds_k0 = ring_lds + (2 * unit) * (D / 2) + 16 * j + 64 * odd_unit;
@@ -679,12 +774,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         for (int k = 0; k < 4; ++k)
           acc[h][4 * m + k] = __builtin_amdgcn_fdot2(W[h], as_h2(c[k]), acc[h][4 * m + k], false);
     }
-    // advance the compute cursor
-    t_row += ROWPOS;
-    if (++crr == rows_per_page) {
-      crr = 0;
-      t_row += (kSplitWaves - 1) * P;  // next page of this wave: 4 pages on
-    }
+    // advance the compute cursor by kSplitWaves rows (positions stay
+    // consecutive across pages of the split)
+    t_row += kSplitWaves * ROWPOS;
   };
 
   for (int r0 = 0; r0 < my_rows; r0 += kStages) {
@@ -778,110 +870,31 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         num = fmaf(f, fmaf(a, cf, bs), num);
         den = fmaf(f, ls, den);
       }
-      float* rec = ws + (((size_t)b * Hq + (h0 + h)) * max_splits + split) * (D + 2);
-      rec[dd] = (den > 0.0f) ? num / den : 0.0f;
+      // agent-scope stores write through to the device-coherent level, so the
+      // block that combines (on any XCD) reads them without a cache flush
+      float* rec = ws + (((size_t)b * Hq + (h0 + h)) * max_splits + split) * (D + 4);
+      __hip_atomic_store(&rec[dd], (den > 0.0f) ? num / den : 0.0f, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
       if (dd == 0) {
-        rec[D] = M;
-        rec[D + 1] = den;
+        __hip_atomic_store(&rec[D], M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&rec[D + 1], den, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
   }
 
-}
+  // ---- the last split of this (request, KV head, head chunk) to finish
+  // combines all of them (log-sum-exp), so no second kernel is needed
+  wait_vm<0>();     // this thread's records are stored
+  __syncthreads();  // ... and every thread's; the merge buffers are free
+  __shared__ uint32_t s_ticket;
+  uint32_t* ticket = tickets + ((size_t)b * Hkv + kv) * n_hchunks + hc;
+  if (tid == 0)
+    s_ticket = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (s_ticket != (uint32_t)(S - 1)) return;
+  if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  combine_splits<D>(ws, out, b, Hq, h0, nh, max_splits, S);
 
-// Log-sum-exp combine of a (request, query head)'s split partials (a
-// separate kernel: the kernel boundary makes every split's partial visible,
-// while an in-kernel ticket would need device-scope fences, which write back
-// an XCD's L2 on this GPU).  One round of loads covers up to kCombineThreads /
-// (D / 16) splits: each thread fetches 16 dims of one split's o and that
-// split's (m, l); more splits take further rounds with a running maximum.
-constexpr int kCombineThreads = 512;
-
-template <int D>
-__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(
-    const float* __restrict__ ws, const int32_t* __restrict__ seq_lens, __half* __restrict__ out,
-    int Hq, int P, int max_pages, int max_splits) {
-  constexpr int NT = kCombineThreads, NW = NT / 64;
-  constexpr int TPS = D / 16;      // threads per split
-  constexpr int CH = NT / TPS;     // splits per round
-  constexpr int QP = NT / D;       // threads per dim in the split sum
-  static_assert(CH % QP == 0, "");
-  __shared__ __attribute__((aligned(16))) float s_val[CH][D + 4];
-  __shared__ float s_red[NW];
-  __shared__ float s_part[QP][D];
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int L = min(seq_lens[b], max_pages * P);
-  __half* dst = out + ((size_t)b * Hq + h) * D;
-  if (L <= 0) {
-    if (tid < D) dst[tid] = __float2half(0.0f);
-    return;
-  }
-  const int n_pages = (L + P - 1) / P;
-  const int S = min(max_splits, n_pages);
-  const float* recs = ws + ((size_t)b * Hq + h) * max_splits * (D + 2);
-  const int sl = tid / TPS, part = tid % TPS;  // split within the round, 16-dim part
-  float run_m = -INFINITY, run_den = 0.0f, run_acc = 0.0f;  // run_acc: dim tid (tid < D)
-  for (int s0 = 0; s0 < S; s0 += CH) {
-    const int s = s0 + sl;
-    float o[16];
-    float m = -INFINITY, l = 0.0f;
-    if (s < S) {
-      const float* rec = recs + (size_t)s * (D + 2);
-      const float4* src = reinterpret_cast<const float4*>(rec + 16 * part);
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float4 v = src[k];
-        o[4 * k] = v.x;
-        o[4 * k + 1] = v.y;
-        o[4 * k + 2] = v.z;
-        o[4 * k + 3] = v.w;
-      }
-      m = rec[D];
-      l = rec[D + 1];
-    } else {
-#pragma unroll
-      for (int k = 0; k < 16; ++k) o[k] = 0.0f;
-    }
-    // maximum of the round
-    float mx = wave_max((l > 0.0f) ? m : -INFINITY);
-    if (lane == 0) s_red[wave] = mx;
-    __syncthreads();
-    mx = s_red[0];
-#pragma unroll
-    for (int w = 1; w < NW; ++w) mx = fmaxf(mx, s_red[w]);
-    const float M = fmaxf(run_m, mx);
-    const float w_s = (l > 0.0f) ? l * __builtin_amdgcn_exp2f(m - M) : 0.0f;
-#pragma unroll
-    for (int k = 0; k < 16; k += 4)
-      *reinterpret_cast<float4*>(&s_val[sl][16 * part + k]) =
-          make_float4(w_s * o[k], w_s * o[k + 1], w_s * o[k + 2], w_s * o[k + 3]);
-    float den = wave_sum(part == 0 ? w_s : 0.0f);
-    __syncthreads();  // s_val complete; s_red reads done
-    if (lane == 0) s_red[wave] = den;
-    {
-      const int d = tid % D, q = tid / D;
-      float acc = 0.0f;
-#pragma unroll 8
-      for (int k = q; k < CH; k += QP) acc += s_val[k][d];
-      s_part[q][d] = acc;
-    }
-    __syncthreads();
-    den = 0.0f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) den += s_red[w];
-    const float f = (run_m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(run_m - M);
-    run_den = run_den * f + den;
-    if (tid < D) {
-      float acc = 0.0f;
-#pragma unroll
-      for (int q = 0; q < QP; ++q) acc += s_part[q][tid];
-      run_acc = run_acc * f + acc;
-    }
-    run_m = M;
-    __syncthreads();  // before the next round overwrites the shared buffers
-  }
-  if (tid < D) dst[tid] = __float2half_rn(run_den > 0.0f ? run_acc / run_den : 0.0f);
 }
 
 template <int D, int G, int HPB>
@@ -892,18 +905,17 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
   const int gq = Hq / L.num_kv_heads;
   const int n_hchunks = (gq + HPB - 1) / HPB;
   dim3 grid(max_splits, L.num_kv_heads * n_hchunks, B);
+  // completion counters first, then the split records
+  uint32_t* tickets = static_cast<uint32_t*>(ws);
+  float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + jfkv::kDecodeCounterBytes);
   hipLaunchKernelGGL((decode_kernel<D, G, HPB>), grid, dim3(kThreads), 0, stream,
                      static_cast<const uint8_t*>(pool.k_codes),
                      static_cast<const uint32_t*>(pool.k_meta),
                      static_cast<const uint8_t*>(pool.v_codes),
                      static_cast<const uint32_t*>(pool.v_meta), static_cast<const __half*>(q),
-                     bt, lens, static_cast<float*>(ws), Hq, L.num_kv_heads, L.page_size,
-                     L.num_pages, max_pages, max_splits, n_hchunks, scale * kLog2e);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(Hq, B), dim3(kCombineThreads), 0, stream,
-                     static_cast<const float*>(ws), lens, static_cast<__half*>(out), Hq,
-                     L.page_size, max_pages, max_splits);
+                     bt, lens, records, tickets, static_cast<__half*>(out), Hq,
+                     L.num_kv_heads, L.page_size, L.num_pages, max_pages, max_splits, n_hchunks,
+                     scale * kLog2e);
   return hipGetLastError();
 }
 

@@ -367,7 +367,9 @@ jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads, int32_t head
   if (!bytes || B <= 0 || num_q_heads <= 0 || head_dim <= 0 || max_splits <= 0 ||
       max_splits > 1024)
     return fail(JF_ERR_INVALID, "bad argument (max_splits must be 1..1024)");
-  *bytes = (size_t)B * num_q_heads * max_splits * (head_dim + 2) * sizeof(float);
+  if ((int64_t)B * num_q_heads > jfkv::kDecodeMaxHeads)
+    return fail(JF_ERR_UNSUPPORTED, "B * num_q_heads above %d", jfkv::kDecodeMaxHeads);
+  *bytes = jfkv::decode_workspace_bytes(B, num_q_heads, head_dim, max_splits);
   return ok();
 }
 

@@ -10,6 +10,17 @@
 
 namespace jfkv {
 
+// Decode workspace: a fixed region of uint32 completion counters (one per
+// request, KV head and head chunk; room for B * Hq <= kDecodeMaxHeads), then
+// the fp32 split records [B][Hq][max_splits][d + 4] (o/l, m, l; 16-byte
+// aligned records).  The fixed
+// size keeps the counters where no call's records can land.
+constexpr int32_t kDecodeMaxHeads = 65536;
+constexpr size_t kDecodeCounterBytes = (size_t)kDecodeMaxHeads * sizeof(uint32_t);
+inline size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t head_dim, int32_t max_splits) {
+  return kDecodeCounterBytes + (size_t)B * Hq * max_splits * (head_dim + 4) * sizeof(float);
+}
+
 // Geometry accepted by every device entry point (validated on the host).
 bool geometry_supported(const jf_kv_layout& L);
 

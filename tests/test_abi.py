@@ -40,8 +40,12 @@ def test_pool_bytes_closed_form_and_geometry_checks():
 
 
 def test_workspace_bound_is_independent_of_length():
-    assert jfkv.jf_decode_workspace_bytes(1, 32, 128, 64) == 64 * 32 * 130 * 4
-    assert jfkv.jf_decode_workspace_bytes(2, 32, 128, 64) == 2 * 64 * 32 * 130 * 4
+    # a fixed counter region, then fp32 records (o/l, m, l) per split and head
+    assert jfkv.jf_decode_workspace_bytes(1, 32, 128, 64) == 262144 + 64 * 32 * 132 * 4
+    assert jfkv.jf_decode_workspace_bytes(2, 32, 128, 64) == 262144 + 2 * 64 * 32 * 132 * 4
+    with pytest.raises(jfkv.JfError) as e:
+        jfkv.jf_decode_workspace_bytes(4096, 32, 128, 1)
+    assert e.value.status == jfkv.JF_ERR_UNSUPPORTED
     with pytest.raises(jfkv.JfError):
         jfkv.jf_decode_workspace_bytes(1, 32, 128, 0)
     with pytest.raises(jfkv.JfError):

@@ -1,8 +1,9 @@
 """GPU split-K decode over paged 4-bit KV against the CPU oracle.
 
 Tolerance: |o_gpu - o_ref| <= 2e-3 absolute (fp16 output, fp32 accumulation),
-plus relative L2 <= 1e-3 on flat data; the needle variants (|o| up to ~30)
-allow 2e-3 + 2^-11 |o_ref| (fp16 output rounding is 2^-11 relative).
+plus relative L2 <= 2e-3 on flat data (three fp16 roundings per position, see
+gpu_cases.check_tol); the needle variants (|o| up to ~30) allow
+2e-3 + 2^-11 |o_ref| (fp16 output rounding is 2^-11 relative).
 Invariants: page order and head independence bitwise, split count within
 tolerance, ragged batch equal to each request alone (bitwise), determinism.
 """
@@ -154,3 +155,25 @@ def test_invalid_page_entries_are_skipped():
     keep = [p for i, p in enumerate(case.tables[0]) if i not in (0, 5)]
     ref = decode_oracle(case, q, lens=[64 * 10], tables=np.array([keep], np.int32))
     check_tol(got, ref, what="invalid pages")
+
+
+def test_workspace_reuse_across_calls():
+    """One zero-filled workspace serves consecutive calls with different
+    lengths, split counts and batch sizes: the completion counters return to
+    zero after every call."""
+    log("decode workspace reuse")
+    case = build(P=64, hkv=2, d=128, G=64, hq=8, lens=(64 * 30 + 5, 900), seed=81)
+    q = _q(16, 2, 8, 128)
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(2, 8, 128, 64), dtype=torch.uint8,
+                     device="cuda")
+    for lens, splits in [((64 * 30 + 5, 900), 64), ((100, 900), 7), ((64 * 30 + 5, 1), 64),
+                         ((0, 900), 3), ((64 * 30 + 5, 900), 1), ((64 * 30 + 5, 900), 64)]:
+        got = decode_gpu(case, q, max_splits=splits, lens=list(lens), ws=ws)
+        for b in range(2):
+            if lens[b] == 0:
+                assert np.all(got[b] == 0)
+                continue
+            ref = decode_oracle(case, q[b:b + 1], lens=[lens[b]], tables=case.tables[b:b + 1])
+            check_tol(got[b:b + 1], ref, what="reuse lens=%s splits=%d" % (lens, splits))
+    counters = ws[:262144].cpu().numpy()
+    assert np.all(counters == 0), "completion counters not reset"
