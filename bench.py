@@ -248,7 +248,7 @@ def main():
                         "wall": 1e3 * ms_per_step},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
-                     "kernel": "decode (split + combine)",
+                     "kernel": "decode_kernel (split-K partials and the in-kernel combine)",
                      "algorithmic_bytes": dec_bytes},
     }
     if args.cpu_sample > 0:
