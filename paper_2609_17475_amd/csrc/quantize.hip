@@ -7,13 +7,9 @@
 // reusable storage").  The contract is bit-exact; every binary32 step is a
 // separately rounded IEEE operation in the order given in include/jfkv.h.
 //
-// Mapping: one group of G elements is handled by G/8 consecutive lanes, each
-// holding 8 fp16 values (one 16-byte load), so a wave covers 8 groups (G=64)
-// and a wave's loads of a K or V row segment are contiguous.  Min and max
-// reduce over the group's lanes with cross-lane swaps on integer total-order
-// keys of the fp16 bit patterns (exact and independent of order).  Each lane
-// packs its 8 codes into one 32-bit word: one store for the row-major K
-// layout, two 16-bit stores for the position-paired V layout.
+// Min and max use integer total-order keys of the fp16 bit patterns (exact
+// and independent of order); the mapping of rows to waves and lanes is
+// described at the kernel.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -43,101 +39,202 @@ __device__ __forceinline__ uint32_t f2h_up_pos(float x) {
   return h;
 }
 
-__global__ __launch_bounds__(256) void quantize_append_kernel(
+// Margin of the reciprocal shortcut for the code of r = fl(d / s): with
+// q0 = d * rcp(s) (v_rcp_f32 within 1 ulp), |q0 - d/s| <= |d/s| 2^-22 and
+// |fl(d/s) - d/s| <= |d/s| 2^-24, so for |d/s| <= 16 the two differ by less
+// than 2^-17.  Whenever q0 is farther than kNear from every half-integer,
+// rint(q0) == rint(fl(d/s)) exactly (same side of every rounding boundary,
+// and fl(d/s) is no tie).  Quotients near a boundary (or above 16, where the
+// bound is looser) take the exact IEEE division instead.
+constexpr float kNear = 0.5f - 1.0f / 32768.0f;  // 2^-15 of margin
+
+// Row-tiled quantize-append.  A wave handles PW = 64 / (D/64) consecutive new
+// rows of one KV head, K or V; lane (p, part) owns dims 64 part .. 64 part
+// + 63 of row p of the tile, so it reads 128 contiguous bytes and, when the
+// rows are consecutive positions of one page (a bulk append), the wave's
+// stores are contiguous runs: K codes 32 B per lane, V codes as whole 32-bit
+// words of position pairs (the two rows of a pair swap halves by a lane
+// exchange), (scale, bias) words per group.  Rows whose pair partner is not
+// the neighbouring position (single-row appends, odd starts, page or request
+// boundaries) store their V half-words alone.
+template <int D, int G>
+__global__ __launch_bounds__(256) void quantize_rows_kernel(
     uint8_t* __restrict__ k_codes, uint32_t* __restrict__ k_meta,
     uint8_t* __restrict__ v_codes, uint32_t* __restrict__ v_meta,
     const uint4* __restrict__ k_new, const uint4* __restrict__ v_new,
     const int32_t* __restrict__ cu_tok, const int32_t* __restrict__ start_pos,
     const int32_t* __restrict__ block_tables, int32_t B, int32_t max_pages, int32_t total_tok,
-    int32_t P, int32_t Hkv, int32_t D, int32_t G, int32_t NP) {
-  // work layout: [row][K|V][kv][D/8 lanes]; a lane owns dims 8c..8c+7
-  const int32_t lanes_per_row_kind = Hkv * (D / 8);
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = (int64_t)total_tok * 2 * lanes_per_row_kind;
-  const bool active = gid < total;
-  int32_t row = 0, kind = 0, rem = 0;
-  if (active) {
-    row = (int32_t)(gid / (2 * lanes_per_row_kind));
-    int32_t r2 = (int32_t)(gid % (2 * lanes_per_row_kind));
-    kind = r2 / lanes_per_row_kind;
-    rem = r2 % lanes_per_row_kind;
-  }
-  const int32_t kv = rem / (D / 8);
-  const int32_t c8 = rem % (D / 8);  // 8-dim chunk within the head
-  const int32_t lpg = G / 8;         // lanes per group (4, 8 or 16)
+    int32_t P, int32_t Hkv, int32_t NP) {
+  constexpr int LPR = D / 64;                 // lanes per row
+  constexpr int PW = 64 / LPR;                // rows per wave
+  constexpr int NGL = (G >= 64) ? 1 : 64 / G;  // groups within a lane
+  constexpr int EPG = (G >= 64) ? 64 : G;      // elements of a group within a lane
+  constexpr int NG = D / G;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave_id = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int kv = (int)(wave_id % Hkv);
+  const int kind = (int)((wave_id / Hkv) & 1);
+  const int64_t tile = wave_id / (2 * Hkv);
+  if (tile * PW >= total_tok) return;  // wave-uniform
+  const int p = lane / LPR, part = lane % LPR;
+  const int64_t row = tile * PW + p;
+  const bool in_range = row < total_tok;
 
-  uint4 x = make_uint4(0, 0, 0, 0);
-  if (active) x = (kind ? v_new : k_new)[(int64_t)row * (Hkv * D / 8) + kv * (D / 8) + c8];
-  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-
-  uint32_t kmin = 0xffffu, kmax = 0u;
+  uint4 x[8];
+  {
+    const uint4* src = (kind ? v_new : k_new) + (row * Hkv + kv) * (D / 8) + part * 8;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    uint32_t k0 = order_key(w[i] & 0xffffu), k1 = order_key(w[i] >> 16);
-    kmin = min(kmin, min(k0, k1));
-    kmax = max(kmax, max(k0, k1));
+    for (int i = 0; i < 8; ++i) x[i] = in_range ? src[i] : make_uint4(0, 0, 0, 0);
   }
-  // reduce over the lpg lanes of the group (aligned runs of lpg lanes)
-  for (int off = 1; off < lpg; off <<= 1) {
-    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, off));
-    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, off));
-  }
-  if (!active) return;
-
-  // request of this row and its logical position
-  int32_t lo = 0, hi = B;  // largest b with cu_tok[b] <= row
-  while (hi - lo > 1) {
-    int32_t mid = (lo + hi) >> 1;
-    if (cu_tok[mid] <= row) lo = mid; else hi = mid;
-  }
-  const int32_t b = lo;
-  const int64_t pos = (int64_t)start_pos[b] + (row - cu_tok[b]);
-  if (pos < 0) return;
-  const int64_t lp = pos / P;
-  if (lp >= max_pages) return;
-  const int32_t page = block_tables[(int64_t)b * max_pages + lp];
-  if (page < 0 || page >= NP) return;
-  const int32_t slot = (int32_t)(pos % P);
-
-  const uint32_t mn_bits = from_key(kmin), mx_bits = from_key(kmax);
-  const float mn = h2f(mn_bits), mx = h2f(mx_bits);
-  // bias: fp16 of mn rounded toward -inf; mn is an fp16 value, so exact
-  const uint32_t bias_bits = mn_bits;
-  const float range = __fsub_rn(mx, mn);
-  const float step = __fdiv_rn(range, 15.0f);
-  const uint32_t scale_bits = (range == 0.0f) ? 0u : f2h_up_pos(step);
-  const float sf = h2f(scale_bits), bf = h2f(bias_bits);
-
-  uint32_t packed = 0;
+  uint32_t hw[32];  // the lane's 64 fp16 values, two per word
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    uint32_t code = 0;
-    if (scale_bits != 0) {
-      const float xi = h2f((w[i >> 1] >> ((i & 1) * 16)) & 0xffffu);
-      const float r = __fdiv_rn(__fsub_rn(xi, bf), sf);
-      float qf = __builtin_rintf(r);
-      qf = fminf(fmaxf(qf, 0.0f), 15.0f);
-      code = (uint32_t)qf;
-    }
-    packed |= code << (4 * i);
+    hw[4 * i] = x[i].x;
+    hw[4 * i + 1] = x[i].y;
+    hw[4 * i + 2] = x[i].z;
+    hw[4 * i + 3] = x[i].w;
   }
 
-  const int32_t g = (c8 * 8) / G;
-  const int64_t ph = (int64_t)page * Hkv + kv;  // (page, kv head) block
-  if (kind == 0) {
-    uint32_t* dst = reinterpret_cast<uint32_t*>(k_codes + (ph * P + slot) * (D / 2)) + c8;
-    *dst = packed;
-  } else {
-    // dims 8c..8c+3 form 4-dim chunk u = 2c, dims 8c+4..8c+7 chunk 2c+1
-    uint16_t* base = reinterpret_cast<uint16_t*>(v_codes + ph * P * (D / 2) +
-                                                 ((int64_t)(slot >> 1) * (D / 4) + 2 * c8) * 4 +
-                                                 (slot & 1) * 2);
-    base[0] = (uint16_t)(packed & 0xffffu);
-    base[2] = (uint16_t)(packed >> 16);
+  // group minimum and maximum (integer total-order keys: exact, order-free)
+  uint32_t kmin[NGL], kmax[NGL];
+#pragma unroll
+  for (int gl = 0; gl < NGL; ++gl) {
+    kmin[gl] = 0xffffu;
+    kmax[gl] = 0u;
+#pragma unroll
+    for (int w = gl * EPG / 2; w < (gl + 1) * EPG / 2; ++w) {
+      const uint32_t k0 = order_key(hw[w] & 0xffffu), k1 = order_key(hw[w] >> 16);
+      kmin[gl] = min(kmin[gl], min(k0, k1));
+      kmax[gl] = max(kmax[gl], max(k0, k1));
+    }
   }
-  if ((c8 % lpg) == 0) {
-    uint32_t* meta = kind ? v_meta : k_meta;
-    meta[(ph * P + slot) * (D / G) + g] = scale_bits | (bias_bits << 16);
+  if constexpr (G == 128) {  // the group spans this lane and lane ^ 1
+    kmin[0] = min(kmin[0], (uint32_t)__shfl_xor((int)kmin[0], 1));
+    kmax[0] = max(kmax[0], (uint32_t)__shfl_xor((int)kmax[0], 1));
+  }
+
+  // scale and bias per group (the contract's steps, binary32 IEEE ops)
+  uint32_t meta_w[NGL];
+  float sf[NGL], bf[NGL], inv[NGL];
+#pragma unroll
+  for (int gl = 0; gl < NGL; ++gl) {
+    const uint32_t mn_bits = from_key(kmin[gl]), mx_bits = from_key(kmax[gl]);
+    const float mn = h2f(mn_bits), mx = h2f(mx_bits);
+    const float range = __fsub_rn(mx, mn);
+    const float step = __fdiv_rn(range, 15.0f);
+    const uint32_t scale_bits = (range == 0.0f) ? 0u : f2h_up_pos(step);
+    meta_w[gl] = scale_bits | (mn_bits << 16);  // bias = mn (exact in fp16)
+    sf[gl] = h2f(scale_bits);
+    bf[gl] = h2f(mn_bits);
+    inv[gl] = (scale_bits == 0) ? 0.0f : __builtin_amdgcn_rcpf(sf[gl]);
+  }
+
+  // codes: rint of the reciprocal quotient, checked against the margin
+  uint32_t cw[8];  // nibble i of word m = code of element 8m + i
+  float worst = 0.0f;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    uint32_t word = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int e = 8 * m + i, gl = e / EPG;
+      const float xe = h2f((hw[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+      const float q0 = __fsub_rn(xe, bf[gl]) * inv[gl];
+      const float c = __builtin_rintf(q0);
+      worst = fmaxf(worst, fabsf(q0 - c));
+      word |= (uint32_t)fminf(fmaxf(c, 0.0f), 15.0f) << (4 * i);
+    }
+    cw[m] = word;
+  }
+  if (__builtin_amdgcn_ballot_w64(worst > kNear) != 0 && worst > kNear) {
+    // some quotient lies near a rounding boundary: exact division throughout
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+      uint32_t word = 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int e = 8 * m + i, gl = e / EPG;
+        uint32_t code = 0;
+        if (sf[gl] != 0.0f) {
+          const float xe = h2f((hw[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+          const float r = __fdiv_rn(__fsub_rn(xe, bf[gl]), sf[gl]);
+          code = (uint32_t)fminf(fmaxf(__builtin_rintf(r), 0.0f), 15.0f);
+        }
+        word |= code << (4 * i);
+      }
+      cw[m] = word;
+    }
+  }
+
+  // destination of the row: request b (largest with cu_tok[b] <= row), its
+  // logical position, page and slot
+  int32_t page = -1, slot = 0;
+  int64_t pos = -1;
+  if (in_range) {
+    int32_t lo = 0, hi = B;
+    while (hi - lo > 1) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (cu_tok[mid] <= row) lo = mid; else hi = mid;
+    }
+    pos = (int64_t)start_pos[lo] + (row - cu_tok[lo]);
+    const int64_t lp = (pos >= 0) ? pos / P : -1;
+    if (lp >= 0 && lp < max_pages) {
+      const int32_t pg = block_tables[(int64_t)lo * max_pages + lp];
+      if (pg >= 0 && pg < NP) {
+        page = pg;
+        slot = (int32_t)(pos % P);
+      }
+    }
+  }
+  const bool valid = page >= 0;
+
+  // V position pairs: both rows of a pair present and neighbours in one page?
+  const int32_t partner_page = __shfl_xor(page, LPR);
+  const int32_t partner_slot = __shfl_xor(slot, LPR);
+  const bool odd = slot & 1;
+  const bool paired = valid && partner_page == page && partner_slot == (slot ^ 1);
+  uint32_t send[4], recv[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    send[i] = odd ? cw[i] : cw[4 + i];  // the half-words the partner stores
+    recv[i] = (uint32_t)__shfl_xor((int)send[i], LPR);
+  }
+  if (!valid) return;
+
+  const int64_t ph = (int64_t)page * Hkv + kv;  // (page, KV head) block
+  if (kind == 0) {
+    uint4* dst = reinterpret_cast<uint4*>(k_codes + (ph * P + slot) * (D / 2) + 32 * part);
+    dst[0] = make_uint4(cw[0], cw[1], cw[2], cw[3]);
+    dst[1] = make_uint4(cw[4], cw[5], cw[6], cw[7]);
+  } else {
+    // 4-dim chunk u = 16 part + i of the lane: half-word i of cw (16 bits)
+    uint8_t* vbase = v_codes + ph * P * (D / 2) + (int64_t)(slot >> 1) * (D / 4) * 4;
+    if (paired) {
+      // even row: words u = 16 part + 0..7, odd row: 16 part + 8..15; word u =
+      // (even row's chunk) | (odd row's chunk) << 16
+      uint32_t wv[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t mine = (odd ? cw[4 + i / 2] : cw[i / 2]) >> (16 * (i & 1)) & 0xffffu;
+        const uint32_t other = recv[i / 2] >> (16 * (i & 1)) & 0xffffu;
+        wv[i] = odd ? (other | (mine << 16)) : (mine | (other << 16));
+      }
+      uint4* dst = reinterpret_cast<uint4*>(vbase + (16 * part + (odd ? 8 : 0)) * 4);
+      dst[0] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      dst[1] = make_uint4(wv[4], wv[5], wv[6], wv[7]);
+    } else {
+      uint16_t* dst = reinterpret_cast<uint16_t*>(vbase + (16 * part) * 4 + (slot & 1) * 2);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dst[2 * i] = (uint16_t)(cw[i / 2] >> (16 * (i & 1)));
+    }
+  }
+  uint32_t* meta = (kind ? v_meta : k_meta) + (ph * P + slot) * NG;
+  if constexpr (G == 32) {
+    *reinterpret_cast<uint2*>(meta + 2 * part) = make_uint2(meta_w[0], meta_w[1]);
+  } else if constexpr (G == 64) {
+    meta[part] = meta_w[0];
+  } else {
+    if ((part & 1) == 0) meta[part / 2] = meta_w[0];
   }
 }
 
@@ -150,17 +247,32 @@ hipError_t launch_quantize_append(const jf_kv_layout& L, const jf_kv_pool_ptrs& 
                                   const int32_t* cu_tok, const int32_t* start_pos,
                                   const int32_t* block_tables, int32_t B, int32_t max_pages,
                                   int32_t total_tok, hipStream_t stream) {
-  const int64_t lanes = (int64_t)total_tok * 2 * L.num_kv_heads * (L.head_dim / 8);
-  const int threads = 256;
-  const int64_t blocks = (lanes + threads - 1) / threads;
+  const int pw = 64 / (L.head_dim / 64);  // rows per wave
+  const int64_t waves = ((int64_t)total_tok + pw - 1) / pw * 2 * L.num_kv_heads;
+  const int64_t blocks = (waves + 3) / 4;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(quantize_append_kernel, dim3((uint32_t)blocks), dim3(threads), 0, stream,
-                     static_cast<uint8_t*>(pool.k_codes), static_cast<uint32_t*>(pool.k_meta),
-                     static_cast<uint8_t*>(pool.v_codes), static_cast<uint32_t*>(pool.v_meta),
-                     static_cast<const uint4*>(k_new), static_cast<const uint4*>(v_new), cu_tok,
-                     start_pos, block_tables, B, max_pages, total_tok, L.page_size,
-                     L.num_kv_heads, L.head_dim, L.group_size, L.num_pages);
-  return hipGetLastError();
+#define JF_Q_ARGS                                                                          \
+  static_cast<uint8_t*>(pool.k_codes), static_cast<uint32_t*>(pool.k_meta),                \
+      static_cast<uint8_t*>(pool.v_codes), static_cast<uint32_t*>(pool.v_meta),            \
+      static_cast<const uint4*>(k_new), static_cast<const uint4*>(v_new), cu_tok, start_pos, \
+      block_tables, B, max_pages, total_tok, L.page_size, L.num_kv_heads, L.num_pages
+#define JF_Q_CASE(D_, G_)                                                                 \
+  if (L.head_dim == D_ && L.group_size == G_) {                                           \
+    hipLaunchKernelGGL((quantize_rows_kernel<D_, G_>), dim3((uint32_t)blocks), dim3(256), 0, \
+                       stream, JF_Q_ARGS);                                                \
+    return hipGetLastError();                                                             \
+  }
+  JF_Q_CASE(64, 32)
+  JF_Q_CASE(64, 64)
+  JF_Q_CASE(128, 32)
+  JF_Q_CASE(128, 64)
+  JF_Q_CASE(128, 128)
+  JF_Q_CASE(256, 32)
+  JF_Q_CASE(256, 64)
+  JF_Q_CASE(256, 128)
+#undef JF_Q_CASE
+#undef JF_Q_ARGS
+  return hipErrorInvalidValue;
 }
 
 }  // namespace jfkv
