@@ -28,13 +28,17 @@ def test_pool_bytes_bit_exact(P, hkv, d, G, lens, prefix):
 
 
 @pytest.mark.parametrize("dist", ["tiny", "wide", "special"])
-def test_pool_bytes_bit_exact_edge_values(dist):
-    log("quantize edge values %s" % dist)
-    P, hkv, d, G, n = 64, 2, 128, 64, 130
-    lay = jfkv.layout(P, hkv, d, G, 4)
-    case = Case(lay, oracle.layout(P, hkv, d, G, 4), jfkv.KVPool(lay, fill=POISON),
-                oracle.Pool(oracle.layout(P, hkv, d, G, 4), fill=POISON),
-                np.array([[2, 0, 3]], np.int32), [n], hkv, [], [])
+@pytest.mark.parametrize("n", [130, 520])  # below / above the row-tiled kernel's threshold
+def test_pool_bytes_bit_exact_edge_values(dist, n):
+    log("quantize edge values %s n=%d" % (dist, n))
+    P, hkv, d, G = 64, 2, 128, 64
+    n_pages = -(-n // P)
+    NP = n_pages + 2
+    table = np.random.default_rng(n).permutation(NP)[:n_pages].astype(np.int32)[None]
+    lay = jfkv.layout(P, hkv, d, G, NP)
+    case = Case(lay, oracle.layout(P, hkv, d, G, NP), jfkv.KVPool(lay, fill=POISON),
+                oracle.Pool(oracle.layout(P, hkv, d, G, NP), fill=POISON),
+                table, [n], hkv, [], [])
     rng = np.random.default_rng(42)
     if dist == "tiny":  # ranges below 15*2^-14: subnormal fp16 scales
         k = (rng.standard_normal((n, hkv, d)) * 2.0 ** -17).astype(np.float16)
@@ -78,7 +82,9 @@ def test_single_row_appends_equal_bulk_and_skip_invalid_pages():
         append_both(case, k[t:t + 1], v[t:t + 1], [0, 1], [t], tables)
     torch.cuda.synchronize()
     assert pool_bytes_equal(case) == []
-    # entries -1 and out of range are skipped, other rows still land
+    # entries -1 and out of range are skipped, other rows still land (a bulk
+    # append of 150 rows: the small-append kernel; test_invalid_pages_tiled
+    # covers the row-tiled one)
     bad_tables = np.array([[-1, 3, NP + 7]], np.int32)
     dev = "cuda"
     jfkv.jf_kv_quantize_append(gpu, torch.from_numpy(k).to(dev), torch.from_numpy(v).to(dev),
@@ -86,5 +92,37 @@ def test_single_row_appends_equal_bulk_and_skip_invalid_pages():
                                torch.tensor([0], dtype=torch.int32, device=dev),
                                torch.from_numpy(bad_tables).to(dev))
     oracle.quantize_append(host, k[P:2 * P], v[P:2 * P], [0, P], [P], np.array([[0, 3]], np.int32))
+    torch.cuda.synchronize()
+    assert pool_bytes_equal(case) == []
+
+
+def test_invalid_pages_and_odd_start_tiled():
+    """Row-tiled kernel (>= 256 rows): page entries -1 / out of range are
+    skipped; an odd start position makes every V position pair straddle two
+    rows of different tiles; a second request starts mid-page."""
+    log("quantize tiled: invalid pages, odd start, two requests")
+    P, hkv, d, G = 64, 2, 128, 64
+    NP = 16
+    rng = np.random.default_rng(5)
+    n0, n1 = 301, 260
+    k = rng.standard_normal((n0 + n1, hkv, d)).astype(np.float16)
+    v = rng.standard_normal((n0 + n1, hkv, d)).astype(np.float16)
+    tables = np.array([[7, -1, 3, 12, NP + 2, 0, 9, 1],
+                       [2, 4, 5, 6, 8, 10, 11, 13]], np.int32)
+    lay = jfkv.layout(P, hkv, d, G, NP)
+    case = Case(lay, None, jfkv.KVPool(lay, fill=POISON),
+                oracle.Pool(oracle.layout(P, hkv, d, G, NP), fill=POISON), tables, [], hkv, [],
+                [])
+    dev = "cuda"
+    jfkv.jf_kv_quantize_append(case.gpu, torch.from_numpy(k).to(dev), torch.from_numpy(v).to(dev),
+                               torch.tensor([0, n0, n0 + n1], dtype=torch.int32, device=dev),
+                               torch.tensor([3, 37], dtype=torch.int32, device=dev),
+                               torch.from_numpy(tables).to(dev))
+    # the oracle writes only rows on valid pages: request 0's positions 3..63
+    # (rows 0..60) and 128..255 (rows 125..252); request 1 entirely
+    host = case.host
+    oracle.quantize_append(host, k[0:61], v[0:61], [0, 61], [3], tables[:1])
+    oracle.quantize_append(host, k[125:253], v[125:253], [0, 128], [128], tables[:1])
+    oracle.quantize_append(host, k[n0:], v[n0:], [0, n1], [37], tables[1:])
     torch.cuda.synchronize()
     assert pool_bytes_equal(case) == []
