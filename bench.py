@@ -111,6 +111,122 @@ def copy_calibration(n_bytes: int, reps: int):
           flush=True)
 
 
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 / bf16 matrix peak
+
+
+def _timed(calls, warmup, steps, stream):
+    """Mean HIP-event duration (us) of each step's calls, and wall us/step."""
+    import numpy as np
+    import torch
+    for i in range(warmup):
+        for c in calls[i % len(calls)]:
+            c()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls[0]) + 1)]
+          for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s in range(steps):
+        ev[s][0].record(stream)
+        for i, c in enumerate(calls[(warmup + s) % len(calls)]):
+            c()
+            ev[s][i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e6
+    per = [float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1]) * 1e3 for s in range(steps)]))
+           for i in range(len(calls[0]))]
+    return per, wall
+
+
+def bench_prefill(args):
+    """Chunked prefill: a 2,048-row chunk (32 q / 8 KV heads, d 128) attends
+    to a 65,536-position 4-bit prefix in 256 shuffled pages plus itself
+    (causal), then the chunk is appended as 8 pages.  MFMA roofline over the
+    attention kernel: FLOP = 4 d Hq sum_i (p0 + i + 1)."""
+    import torch
+    from paper_2609_17475_amd import jfkv, workloads
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS["prefill_chunk"]
+    P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
+    p0, T = wl.seq_lens[0], wl.chunk
+    lay = jfkv.layout(P, hkv, d, G, wl.pool_pages)
+    pp = jfkv.PagePool(wl.pool_pages, P, shuffle_seed=wl.seed)
+    s = pp.create()
+    pp.reserve(s, p0 + T)
+    table = torch.tensor(pp.export([s], (p0 + T) // P)[0], dtype=torch.int32, device=dev)
+    k, v = workloads.gen_kv_device(wl.seed, p0 + T, hkv, d, wl.n_outlier, dev)
+    q = workloads.gen_q_device(wl.seed + 1, T, hq, d, dev)
+    pool = jfkv.KVPool(lay, device=dev)
+    jfkv.jf_kv_quantize_append(pool, k[:p0], v[:p0], torch.tensor([0, p0], dtype=torch.int32,
+                                                                  device=dev),
+                               torch.tensor([0], dtype=torch.int32, device=dev), table)
+    kc, vc = k[p0:].contiguous(), v[p0:].contiguous()
+    out = torch.empty((T, hq, d), dtype=torch.float16, device=dev)
+    stream = torch.cuda.current_stream()
+    attn = jfkv.bind_prefill(pool, q, kc, vc, table[0].contiguous(), p0, 1.0, out, stream)
+    app = jfkv.bind_quantize_append(pool, kc, vc, torch.tensor([0, T], dtype=torch.int32,
+                                                               device=dev),
+                                    torch.tensor([p0], dtype=torch.int32, device=dev), table,
+                                    stream)
+    steps = max(1, args.steps // 3)
+    (t_attn, t_app), wall = _timed([[attn, app]], args.warmup, steps, stream)
+    flop = 4.0 * d * hq * sum(p0 + i + 1 for i in range(T))
+    achieved = flop / (t_attn * 1e-6) / 1e12
+    assert torch.isfinite(out.float()).all().item(), "non-finite prefill output"
+    print(json.dumps({
+        "metric": "chunked-prefill attention TFLOP/s over a 4-bit paged prefix",
+        "value": flop / (wall * 1e-6) / 1e12, "unit": "TFLOP/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": wall / 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u4 codes x f16 -> f32 (MFMA f16)",
+        "data": "synthetic",
+        "config": {"workload": "prefill_chunk", "chunk": T, "prefix": p0, "num_q_heads": hq,
+                   "num_kv_heads": hkv, "head_dim": d, "page_size": P, "group_size": G},
+        "us_per_step": {"attention": t_attn, "append": t_app, "wall": wall},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_F16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / MFMA_F16_PEAK_TFLOPS, "traffic": None,
+                     "kernel": "prefill_kernel", "algorithmic_flop": flop},
+        "cpu_baseline": None}), flush=True)
+
+
+def bench_quantize_bulk(args):
+    """Bulk quantize-append of 262,143 rows x 8 KV heads (the cache of the
+    256K decode workload) into 1,024 shuffled pages; HBM roofline over the
+    kernel: 2 x 256 B read and 2 x (64 + 8) B written per (row, KV head)."""
+    import torch
+    from paper_2609_17475_amd import jfkv, workloads
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS["decode_256k"]
+    P, hkv, d, G = wl.page_size, wl.num_kv_heads, wl.head_dim, wl.group_size
+    L = wl.seq_lens[0] - 1
+    lay = jfkv.layout(P, hkv, d, G, wl.pool_pages)
+    pp = jfkv.PagePool(wl.pool_pages, P, shuffle_seed=wl.seed)
+    s = pp.create()
+    pp.reserve(s, L + 1)
+    table = torch.tensor(pp.export([s], (L + 1) // P)[0], dtype=torch.int32, device=dev)
+    k, v = workloads.gen_kv_device(wl.seed, L, hkv, d, wl.n_outlier, dev)
+    pools = [jfkv.KVPool(lay, device=dev) for _ in range(4)]
+    cu = torch.tensor([0, L], dtype=torch.int32, device=dev)
+    st = torch.tensor([0], dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    calls = [[jfkv.bind_quantize_append(p, k, v, cu, st, table, stream)] for p in pools]
+    steps = max(1, args.steps // 4)
+    (t_q,), wall = _timed(calls, args.warmup, steps, stream)
+    nbytes = L * hkv * 2 * (2 * d + d // 2 + 4 * d // G)
+    achieved = nbytes / (t_q * 1e-6) / 1e9
+    print(json.dumps({
+        "metric": "bulk quantize-append GB/s (262,143 rows x 8 KV heads)",
+        "value": nbytes / (wall * 1e-6) / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": wall / 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16 -> u4 codes + f16 meta",
+        "data": "synthetic",
+        "config": {"workload": "quantize_bulk", "rows": L, "num_kv_heads": hkv, "head_dim": d,
+                   "page_size": P, "group_size": G},
+        "us_per_step": {"quantize": t_q, "wall": wall},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "quantize_rows_kernel", "algorithmic_bytes": nbytes},
+        "cpu_baseline": None}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -124,6 +240,10 @@ def main():
                     help="repeat the CPU oracle step for at least this long")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
+    ap.add_argument("--workload", default="decode_256k",
+                    choices=["decode_256k", "prefill_chunk", "quantize_bulk"],
+                    help="decode_256k (the headline line); prefill_chunk and quantize_bulk "
+                         "print their own lines")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -131,6 +251,12 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, max(1, args.steps))
+        return
+    if args.workload == "prefill_chunk":
+        bench_prefill(args)
+        return
+    if args.workload == "quantize_bulk":
+        bench_quantize_bulk(args)
         return
 
     import numpy as np
