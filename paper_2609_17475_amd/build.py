@@ -25,6 +25,10 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
 DEVICE = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-munsafe-fp-atomics"]
+# Per-source device flags.  decode.hip: matrix-core results stay in ordinary
+# VGPRs (its rare rescale multiplies them on the VALU; with accumulation
+# registers the compiler copies them out and back around every row).
+EXTRA = {"decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:
@@ -37,7 +41,7 @@ def _compile(src: str) -> str:
     path = os.path.join(CSRC, src)
     cmd = [hipcc(), *COMMON]
     if src.endswith(".hip"):
-        cmd += ["-x", "hip", *DEVICE]
+        cmd += ["-x", "hip", *DEVICE, *EXTRA.get(src, [])]
     else:
         cmd += ["-x", "c++", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
     cmd += ["-c", path, "-o", obj]
