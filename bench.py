@@ -367,6 +367,8 @@ def main():
         "config": {"workload": "decode_256k", "positions": L, "batch": 1, "num_q_heads": hq,
                    "num_kv_heads": hkv, "head_dim": d, "page_size": P, "group_size": G,
                    "pages": L // P, "max_splits": args.max_splits,
+                   "splits_used": min(args.max_splits, L // P, -(-torch.cuda.get_device_properties(
+                       0).multi_processor_count // hkv)),
                    "layers_rotated": args.layers},
         "hbm_GBs": achieved,
         "hbm_pct_of_peak": 100.0 * achieved / HBM_PEAK_GBS,

@@ -36,6 +36,9 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <type_traits>
+
 #include "jfkv_internal.h"
 
 namespace {
@@ -52,11 +55,21 @@ constexpr float kTau = 2.0f;  // lazy-rescale margin, log2 units
 // Initial running maximum: finite, so that positions masked to -inf before
 // any valid one give p = 2^(-inf - kMinit) = 0, not NaN.
 constexpr float kMinit = -1e30f;
-constexpr int kThreads = 256;       // 4 waves: one split
-constexpr int kWaves = kThreads / 64;
+constexpr int kMaxThreads = 512;    // a block: one split, one block per CU
 constexpr int kRowPos = 32;         // positions per row: two 16-position MFMA tiles
 constexpr int kHeadSlots = 4;       // query heads per block
-constexpr int kRingBudget = 81920;  // LDS bytes of a block's rings (two blocks per CU)
+constexpr int kRingBudget = 162816; // LDS bytes of a block's rings (a CU's LDS less 1 KiB)
+// Waves per block: one per SIMD.  (Eight waves stream no faster, and the
+// second wave of a SIMD lags the first, which the block then waits for.)
+#ifndef JF_DECODE_WAVES
+#define JF_DECODE_WAVES 4
+#endif
+#ifndef JF_DECODE_STAGES
+#define JF_DECODE_STAGES 4
+#endif
+template <int D>
+constexpr int waves_for() { return JF_DECODE_WAVES; }
+constexpr int kMaxStages = JF_DECODE_STAGES;  // LDS ring depth per wave (at most)
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
 
@@ -94,11 +107,33 @@ __device__ __forceinline__ float xor_max_from(float v, int from) {
   return v;
 }
 
-__device__ __forceinline__ void dma16(const void* g, void* lds_base) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds_base, 16, 0, 0);
+// HBM -> LDS loads of the page stream: lane i's 16 (or 4) bytes at
+// sbase + voff + IMM land at LDS address lds + LDSOFF + 16 i (or 4 i).  (The
+// instruction's offset applies to the LDS address as well, so M0 gets
+// LDSOFF - IMM.)
+// Non-temporal (nt): each byte is read once per call, and streaming past the
+// caches is markedly faster than allocating the lines.  Written as asm so
+// that the address stays in the scalar-base form (64-bit row pointer in
+// SGPRs, the lane's constant 32-bit offset in a VGPR: no vector address
+// arithmetic) and the LDS address is formed in M0 from one base (no scalar
+// register per stage and load); the s_nop is the wait the M0 write needs
+// before an LDS-DMA load.  The loads write no registers; the kernel waits
+// for them with explicit vmcnt waits.
+template <int IMM, int LDSOFF>
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds) {
+  static_assert(IMM >= 0 && LDSOFF >= IMM && IMM < 4096, "offsets");
+  asm volatile(
+      "s_add_u32 m0, %0, %4\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2 offset:%3 nt"
+      :
+      : "s"(lds), "v"(voff), "s"(sbase), "i"(IMM), "i"(LDSOFF - IMM)
+      : "memory", "m0", "scc");
 }
-__device__ __forceinline__ void dma4(const void* g, void* lds_base) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds_base, 4, 0, 0);
+template <int LDSOFF>
+__device__ __forceinline__ void dma4(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_add_u32 m0, %0, %3\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2 nt"
+               :
+               : "s"(lds), "v"(voff), "s"(sbase), "i"(LDSOFF)
+               : "memory", "m0", "scc");
 }
 
 // Wait until at most N vector-memory operations of this wave are in flight.
@@ -124,6 +159,15 @@ __device__ __forceinline__ h8 v_operand(uint32_t w0, uint32_t w1, uint32_t w2, u
   const u32x4 r = {(w0 >> SH) & M, (w1 >> SH) & M, (w2 >> SH) & M, (w3 >> SH) & M};
   return __builtin_bit_cast(h8, r);
 }
+// f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>), in order.
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
 __device__ __forceinline__ f32x4 mfma(h8 a, h8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
@@ -133,33 +177,33 @@ __device__ __forceinline__ f32x4 mfma(h8 a, h8 b, f32x4 c) {
 // lane: the K codes of its position in both 16-position tiles, the (scale,
 // bias) words of its eight positions for K and for V, and the V words of its
 // four position pairs for each of its 4-dim chunks.  OFF is the stage
-// offset, MB the V meta offset from the K meta.
-template <int OFF, int MB>
-__device__ __forceinline__ void read_row_d128(uint32_t ka, uint32_t ma, uint32_t va0,
-                                              uint32_t va1, uint4& k0, uint4& k1, uint4& km0,
-                                              uint4& km1, uint4& vm0, uint4& vm1,
+// offset; kma and vma address the K and V meta words of the lane's columns.
+template <int OFF>
+__device__ __forceinline__ void read_row_d128(uint32_t ka, uint32_t kma, uint32_t vma,
+                                              uint32_t va0, uint32_t va1, uint4& k0, uint4& k1,
+                                              uint4& km0, uint4& km1, uint4& vm0, uint4& vm1,
                                               uint32_t (&v)[2][4]) {
   asm volatile(
-      "ds_read_b128 %0, %14 offset:%18\n\t"
-      "ds_read_b128 %1, %14 offset:%21\n\t"
-      "ds_read_b128 %2, %15 offset:%18\n\t"
-      "ds_read_b128 %3, %15 offset:%19\n\t"
-      "ds_read_b128 %4, %15 offset:%23\n\t"
-      "ds_read_b128 %5, %15 offset:%24\n\t"
-      "ds_read_b32 %6, %16 offset:%18\n\t"
-      "ds_read_b32 %7, %16 offset:%20\n\t"
-      "ds_read_b32 %8, %16 offset:%21\n\t"
-      "ds_read_b32 %9, %16 offset:%22\n\t"
-      "ds_read_b32 %10, %17 offset:%18\n\t"
-      "ds_read_b32 %11, %17 offset:%20\n\t"
-      "ds_read_b32 %12, %17 offset:%21\n\t"
-      "ds_read_b32 %13, %17 offset:%22\n\t"
+      "ds_read_b128 %0, %14 offset:%19\n\t"
+      "ds_read_b128 %1, %14 offset:%22\n\t"
+      "ds_read_b128 %2, %15 offset:%19\n\t"
+      "ds_read_b128 %3, %15 offset:%20\n\t"
+      "ds_read_b128 %4, %16 offset:%19\n\t"
+      "ds_read_b128 %5, %16 offset:%20\n\t"
+      "ds_read_b32 %6, %17 offset:%19\n\t"
+      "ds_read_b32 %7, %17 offset:%21\n\t"
+      "ds_read_b32 %8, %17 offset:%22\n\t"
+      "ds_read_b32 %9, %17 offset:%23\n\t"
+      "ds_read_b32 %10, %18 offset:%19\n\t"
+      "ds_read_b32 %11, %18 offset:%21\n\t"
+      "ds_read_b32 %12, %18 offset:%22\n\t"
+      "ds_read_b32 %13, %18 offset:%23\n\t"
       "s_waitcnt lgkmcnt(0)"
       : "=&v"(k0), "=&v"(k1), "=&v"(km0), "=&v"(km1), "=&v"(vm0), "=&v"(vm1), "=&v"(v[0][0]),
         "=&v"(v[0][1]), "=&v"(v[0][2]), "=&v"(v[0][3]), "=&v"(v[1][0]), "=&v"(v[1][1]),
         "=&v"(v[1][2]), "=&v"(v[1][3])
-      : "v"(ka), "v"(ma), "v"(va0), "v"(va1), "i"(OFF), "i"(OFF + 16), "i"(OFF + 128),
-        "i"(OFF + 256), "i"(OFF + 384), "i"(OFF + MB), "i"(OFF + MB + 16)
+      : "v"(ka), "v"(kma), "v"(vma), "v"(va0), "v"(va1), "i"(OFF), "i"(OFF + 16),
+        "i"(OFF + 128), "i"(OFF + 256), "i"(OFF + 384)
       : "memory");
 }
 // head_dim 64: 8-byte K quarters; K and V meta at separate bases.
@@ -187,30 +231,29 @@ __device__ __forceinline__ void read_row_d64(uint32_t ka, uint32_t kma, uint32_t
 }
 // head_dim 256: two halves of 128 dims (GOFF: meta offset of the second
 // half's groups); three waits per row.
-template <int OFF, int MB, int GOFF>
-__device__ __forceinline__ void read_row_d256(uint32_t ka, uint32_t ma, uint32_t va,
-                                              uint4 (&k)[2][2], uint4 (&km)[2][2],
+template <int OFF, int GOFF>
+__device__ __forceinline__ void read_row_d256(uint32_t ka, uint32_t kma, uint32_t vma,
+                                              uint32_t va, uint4 (&k)[2][2], uint4 (&km)[2][2],
                                               uint4 (&vm)[2][2], uint32_t (&v)[4][4]) {
   asm volatile(
-      "ds_read_b128 %0, %12 offset:%14\n\t"
-      "ds_read_b128 %1, %12 offset:%15\n\t"
-      "ds_read_b128 %2, %12 offset:%16\n\t"
-      "ds_read_b128 %3, %12 offset:%17\n\t"
-      "ds_read_b128 %4, %13 offset:%14\n\t"
-      "ds_read_b128 %5, %13 offset:%18\n\t"
-      "ds_read_b128 %6, %13 offset:%19\n\t"
-      "ds_read_b128 %7, %13 offset:%20\n\t"
-      "ds_read_b128 %8, %13 offset:%21\n\t"
-      "ds_read_b128 %9, %13 offset:%22\n\t"
-      "ds_read_b128 %10, %13 offset:%23\n\t"
-      "ds_read_b128 %11, %13 offset:%24\n\t"
+      "ds_read_b128 %0, %12 offset:%15\n\t"
+      "ds_read_b128 %1, %12 offset:%16\n\t"
+      "ds_read_b128 %2, %12 offset:%17\n\t"
+      "ds_read_b128 %3, %12 offset:%18\n\t"
+      "ds_read_b128 %4, %13 offset:%15\n\t"
+      "ds_read_b128 %5, %13 offset:%19\n\t"
+      "ds_read_b128 %6, %13 offset:%20\n\t"
+      "ds_read_b128 %7, %13 offset:%21\n\t"
+      "ds_read_b128 %8, %14 offset:%15\n\t"
+      "ds_read_b128 %9, %14 offset:%19\n\t"
+      "ds_read_b128 %10, %14 offset:%20\n\t"
+      "ds_read_b128 %11, %14 offset:%21\n\t"
       "s_waitcnt lgkmcnt(0)"
       : "=&v"(k[0][0]), "=&v"(k[1][0]), "=&v"(k[0][1]), "=&v"(k[1][1]), "=&v"(km[0][0]),
         "=&v"(km[0][1]), "=&v"(km[1][0]), "=&v"(km[1][1]), "=&v"(vm[0][0]), "=&v"(vm[0][1]),
         "=&v"(vm[1][0]), "=&v"(vm[1][1])
-      : "v"(ka), "v"(ma), "i"(OFF), "i"(OFF + 64), "i"(OFF + 512), "i"(OFF + 576),
-        "i"(OFF + 16), "i"(OFF + GOFF), "i"(OFF + GOFF + 16), "i"(OFF + MB), "i"(OFF + MB + 16),
-        "i"(OFF + MB + GOFF), "i"(OFF + MB + GOFF + 16)
+      : "v"(ka), "v"(kma), "v"(vma), "i"(OFF), "i"(OFF + 64), "i"(OFF + 512), "i"(OFF + 576),
+        "i"(OFF + 16), "i"(OFF + GOFF), "i"(OFF + GOFF + 16)
       : "memory");
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2) {
@@ -336,13 +379,15 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
 // Progress: the waves of a block meet only after their row loops; every loop
 // ends after the wave's own rows.
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void decode_kernel(
+__global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     const uint8_t* __restrict__ k_codes, const uint32_t* __restrict__ k_meta,
     const uint8_t* __restrict__ v_codes, const uint32_t* __restrict__ v_meta,
     const __half* __restrict__ q, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, float* __restrict__ ws, uint32_t* __restrict__ tickets,
     __half* __restrict__ out, int Hq, int Hkv, int P, int NP, int max_pages, int max_splits,
-    int n_hchunks, float scale_log2) {
+    int split_cap, int n_hchunks, float scale_log2) {
+  constexpr int kWaves = waves_for<D>();
+  constexpr int kThreads = 64 * kWaves;
   constexpr int NG = D / G;                // scale groups per head
   constexpr int HD = D < 128 ? D : 128;    // dims per half
   constexpr int NHALF = D / HD;            // halves: separate score accumulators
@@ -356,7 +401,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
   constexpr int kMetaBytes = 256 * META_DMAS;  // K or V (scale, bias) words per row
   constexpr int kStageBytes = 2 * KB + 2 * kMetaBytes;
   constexpr int DMAS_PER_ROW = 2 * K_DMAS + 2 * META_DMAS;
-  constexpr int kStages = (kWaves * 4 * kStageBytes + 16 <= kRingBudget) ? 4 : 3;
+  constexpr int kFit = (kRingBudget - 16) / (kWaves * kStageBytes);
+  constexpr int kStages = kFit < kMaxStages ? kFit : kMaxStages;
+  static_assert(kStages >= 2, "ring depth");
   constexpr bool kSwz = (D == 128);
   static_assert(DMAS_PER_ROW * (kStages - 1) < 64, "vmcnt range");
   static_assert(kHeadSlots * D + 2 * kHeadSlots <= kStages * kStageBytes / 4, "merge fits a ring");
@@ -383,7 +430,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     return;
   }
   const int n_pages = (L + P - 1) / P;
-  const int S = min(max_splits, n_pages);
+  const int S = min(split_cap, n_pages);  // split_cap <= max_splits (the record stride)
   if (split >= S) return;
   int pb, pe;
   split_range(n_pages, S, split, pb, pe);
@@ -409,15 +456,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
   int cur_grp = 0;
 
   const int l16 = lane & 15, q4 = lane >> 4;
-  const int hs = l16 & 3, gs = l16 >> 2;  // accumulator column: head slot, quarter slot
+  const int hs = l16 & 3, gs = l16 >> 2;  // accumulator column: head slot, column slot
   const bool head_on = hs < nh;
 
-  // query words of head hs over the dims of quarter gs (loaded with the page
-  // IDs, turned into operands once the first rows' loads are in flight)
+  // query words of head hs over the dims of quarter q4, the lane's k-slots
+  // (loaded with the page IDs, turned into operands once the first rows'
+  // loads are in flight)
   uint4 qraw[NHALF][WQ];
   {
     const uint4* src = reinterpret_cast<const uint4*>(
-        q + ((size_t)b * Hq + h0 + min(hs, nh - 1)) * D + DQ * gs);
+        q + ((size_t)b * Hq + h0 + min(hs, nh - 1)) * D + DQ * q4);
 #pragma unroll
     for (int e = 0; e < NHALF; ++e)
 #pragma unroll
@@ -453,7 +501,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
   int ipk = wave / rows_per_page, irr = wave % rows_per_page;
   const uint8_t* ik = k_codes;
   const uint8_t* iv = v_codes;
-  size_t im = 0;  // byte offset of the row's (scale, bias) words in k_meta / v_meta
+  const uint8_t* ikm = reinterpret_cast<const uint8_t*>(k_meta);
+  const uint8_t* ivm = reinterpret_cast<const uint8_t*>(v_meta);
   bool iok = false;
   auto enter_page = [&]() {
     if ((ipk >> 6) != cur_grp) {  // more than 64 pages per split: next 64 IDs
@@ -464,9 +513,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     int page = __builtin_amdgcn_readlane(pg_grp, ipk & 63);
     iok = (unsigned)page < (unsigned)NP;
     if (!iok) page = 0;  // never read past the pool; the positions are masked
-    ik = k_codes + page * page_codes + kv * head_codes + (size_t)irr * KB;
-    iv = v_codes + page * page_codes + kv * head_codes + (size_t)irr * KB;
-    im = ((((size_t)page * Hkv + kv) * P) + (size_t)irr * kRowPos) * NG * 4;
+    const size_t run = (size_t)page * Hkv + kv;
+    ik = k_codes + run * head_codes + (size_t)irr * KB;
+    iv = v_codes + run * head_codes + (size_t)irr * KB;
+    const size_t mo = (run * P + (size_t)irr * kRowPos) * NG * 4;
+    ikm = reinterpret_cast<const uint8_t*>(k_meta) + mo;
+    ivm = reinterpret_cast<const uint8_t*>(v_meta) + mo;
   };
   bool stage_ok[kStages];
   // Loads of the next row into stage ST; past the wave's last row, loads of
@@ -475,25 +527,29 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
   auto issue = [&](auto st_c, bool real) {
     constexpr int ST = decltype(st_c)::value;
     uint8_t* st = ring + ST * kStageBytes;
+    constexpr int SO = ST * kStageBytes;  // the stage's offset in the ring
     if (real) {
-#pragma unroll
-      for (int c = 0; c < K_DMAS; ++c) dma16(ik + 1024 * c + k_off, st + 1024 * c);
-#pragma unroll
-      for (int c = 0; c < K_DMAS; ++c) dma16(iv + 1024 * c + v_off, st + KB + 1024 * c);
-      const uint8_t* km8 = reinterpret_cast<const uint8_t*>(k_meta) + im;
-      const uint8_t* vm8 = reinterpret_cast<const uint8_t*>(v_meta) + im;
-#pragma unroll
-      for (int i = 0; i < META_DMAS; ++i) {
-        dma4(km8 + meta_off[i], st + 2 * KB + 256 * i);
-        dma4(vm8 + meta_off[i], st + 2 * KB + kMetaBytes + 256 * i);
-      }
+      static_for<K_DMAS>([&](auto c_c) {
+        constexpr int C = decltype(c_c)::value;
+        dma16<1024 * C, SO + 1024 * C>(ik, k_off, ring_lds);
+      });
+      static_for<K_DMAS>([&](auto c_c) {
+        constexpr int C = decltype(c_c)::value;
+        dma16<1024 * C, SO + KB + 1024 * C>(iv, v_off, ring_lds);
+      });
+      static_for<META_DMAS>([&](auto i_c) {
+        constexpr int I = decltype(i_c)::value;
+        dma4<SO + 2 * KB + 256 * I>(ikm, meta_off[I], ring_lds);
+        dma4<SO + 2 * KB + kMetaBytes + 256 * I>(ivm, meta_off[I], ring_lds);
+      });
       stage_ok[ST] = iok;
       // advance the cursor by kWaves rows
       irr += kWaves;
       if (irr < rows_per_page) {
         ik += kWaves * KB;
         iv += kWaves * KB;
-        im += kWaves * kRowPos * NG * 4;
+        ikm += kWaves * kRowPos * NG * 4;
+        ivm += kWaves * kRowPos * NG * 4;
       } else {
         do {
           irr -= rows_per_page;
@@ -501,11 +557,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
         } while (irr >= rows_per_page);
         if (ipk < n_split_pages) enter_page();
       }
-    } else {
-#pragma unroll
-      for (int c = 0; c < 2 * K_DMAS; ++c) dma16(k_codes, st + 1024 * c);
-#pragma unroll
-      for (int i = 0; i < 2 * META_DMAS; ++i) dma4(k_meta, st + 2 * KB + 256 * i);
+    } else {  // past the last row: the first bytes of the pool, never used
+      static_for<2 * K_DMAS>([&](auto c_c) {
+        dma16<0, SO + 1024 * decltype(c_c)::value>(k_codes, 0u, ring_lds);
+      });
+      static_for<2 * META_DMAS>([&](auto i_c) {
+        dma4<SO + 2 * KB + 256 * decltype(i_c)::value>(k_meta, 0u, ring_lds);
+      });
       stage_ok[ST] = false;
     }
   };
@@ -514,16 +572,17 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
   // All stages are in flight while a row is computed: a row's stage is read
   // into registers first and then refilled with the row kStages ahead.
   if (my_rows > 0) {
-    issue(std::integral_constant<int, 0>{}, 0 < my_rows);
-    issue(std::integral_constant<int, 1>{}, 1 < my_rows);
-    issue(std::integral_constant<int, 2>{}, 2 < my_rows);
-    if constexpr (kStages == 4) issue(std::integral_constant<int, 3>{}, 3 < my_rows);
+    static_for<kStages>([&](auto st_c) { issue(st_c, decltype(st_c)::value < my_rows); });
   }
 
-  // ---- Q' operands: k-slots (n0, n4, n1, n5, n2, n6, n3, n7) of each code
-  // word, odd nibbles' dims divided by 16; zero outside quarter gs (and for
-  // unused head slots).  qs: the quarter's query sum (times 2^-24, the code
-  // scale), the bias factor of its group.
+  // ---- Q' operands.  Score column hs + 4 gs holds head hs restricted to the
+  // dims of scale group gs % NGH of each half (columns with equal group are
+  // copies), so each column's sum has one scale; k-slots (n0, n4, n1, n5, n2,
+  // n6, n3, n7) of each code word, odd nibbles' dims divided by 16.  qs: the
+  // group's query sum (times 2^-24, the code scale), its bias factor.
+  constexpr int NGH = HD / G;            // scale groups per half
+  const int gcol = gs % NGH;             // group (within a half) of the score column
+  const bool q_on = head_on && (DQ * q4) / G == gcol;
   h8 qB[NHALF][WQ];
   float qs[NHALF];
 #pragma unroll
@@ -544,10 +603,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
       const _Float16 sixteenth = (_Float16)0.0625f;
       h8 o = {x[0], x[4], x[1] * sixteenth, x[5] * sixteenth,
               x[2], x[6], x[3] * sixteenth, x[7] * sixteenth};
-      if (q4 != gs || !head_on) o = h8{};
+      if (!q_on) o = h8{};
       qB[e][kb] = o;
     }
-    qs[e] = head_on ? s * (1.0f / 16777216.0f) : 0.0f;
+    // the group's query sum: quarter sums of the four lanes l16 + 16 k
+    const float sq[4] = {s, __shfl_xor(s, 16), __shfl_xor(s, 32), __shfl_xor(s, 48)};
+    float g = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if ((DQ * (q4 ^ k)) / G == gcol) g += sq[k];
+    qs[e] = head_on ? g * (1.0f / 16777216.0f) : 0.0f;
   }
   const float kfold = 16777216.0f * scale_log2;  // 2^24: the code scale
 
@@ -573,9 +638,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     ka = ring_lds + 32 * p0 + 8 * q4;
   }
   {
-    const int gk = (DQ * gs) / G;  // group of the lane's score column (first half)
-    kma = ring_lds + 2 * KB + (gk * kRowPos + 8 * q4) * 4;
-    const int gv = min((32 * gs) / G, NG - 1);  // group of its value column
+    kma = ring_lds + 2 * KB + (gcol * kRowPos + 8 * q4) * 4;  // score column's group
+    const int gv = min((32 * gs) / G, NG - 1);  // group of the value column (first half)
     vma = ring_lds + 2 * KB + kMetaBytes + (gv * kRowPos + 8 * q4) * 4;
   }
 #pragma unroll
@@ -605,7 +669,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     if constexpr (D == 128) {
       uint4 k0, k1, km0, km1, vm0, vm1;
       uint32_t v[2][4];
-      read_row_d128<OFF, kMetaBytes>(ka, kma, va[0], va[1], k0, k1, km0, km1, vm0, vm1, v);
+      read_row_d128<OFF>(ka, kma, vma, va[0], va[1], k0, k1, km0, km1, vm0, vm1, v);
       unpack4(k0, kw[0][0]); unpack4(k1, kw[0][1]);
       unpack4(km0, kmw[0][0]); unpack4(km1, kmw[0][1]);
       unpack4(vm0, vmw[0][0]); unpack4(vm1, vmw[0][1]);
@@ -627,7 +691,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     } else {
       uint4 k[2][2], km[2][2], vm[2][2];
       uint32_t v[4][4];
-      read_row_d256<OFF, kMetaBytes, (128 / G) * kRowPos * 4>(ka, kma, va[0], k, km, vm, v);
+      read_row_d256<OFF, (128 / G) * kRowPos * 4>(ka, kma, vma, va[0], k, km, vm, v);
 #pragma unroll
       for (int e = 0; e < 2; ++e)
 #pragma unroll
@@ -657,19 +721,20 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
 #pragma unroll
         for (int t = 0; t < 2; ++t) sacc[e][t] = mfma(k_operand(kw[e][t][kb]), qB[e][kb], sacc[e][t]);
 
-    // ---- logits: fold each column's group scale and bias, sum the four
-    // quarter columns of the head (lanes l16 ^ 4k of the 16-lane row)
+    // ---- logits: fold each column's group scale and bias, sum the distinct
+    // groups of the head (lanes l16 + 4k of the 16-lane row: columns of equal
+    // group are copies, so NGH - 1 rotations suffice), scale
     float sc[2][4];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float z = 0.0f;
+        float a = 0.0f;
 #pragma unroll
-        for (int e = 0; e < NHALF; ++e) z = fold_meta(kmw[e][t][i], sacc[e][t][i], qs[e], z);
-        z = row_ror_add<4>(z);
-        z = row_ror_add<8>(z);
-        sc[t][i] = z * kfold;
+        for (int e = 0; e < NHALF; ++e) a = fold_meta(kmw[e][t][i], sacc[e][t][i], qs[e], a);
+        if constexpr (NGH >= 2) a = row_ror_add<4>(a);
+        if constexpr (NGH >= 4) a = row_ror_add<8>(a);
+        sc[t][i] = a * kfold;
       }
     if (!full) {
 #pragma unroll
@@ -682,8 +747,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
           for (int e = 0; e < NHALF; ++e) vmw[e][t][i] = ok ? vmw[e][t][i] : 0u;
         }
     }
-    float mx = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
-                     fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
+    const float mx = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
+                           fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
     if (__builtin_amdgcn_ballot_w64(mx > thr) != 0) {
       // new running maximum of the head: lanes with equal lane % 4
       const float M = xor_max_from(mx, 4);
@@ -736,11 +801,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     t_row += kWaves * kRowPos;
   };
   for (int r0 = 0; r0 < my_rows; r0 += kStages) {
-    row(std::integral_constant<int, 0>{});
-    if (r0 + 1 < my_rows) row(std::integral_constant<int, 1>{});
-    if (r0 + 2 < my_rows) row(std::integral_constant<int, 2>{});
-    if constexpr (kStages == 4)
-      if (r0 + 3 < my_rows) row(std::integral_constant<int, 3>{});
+    static_for<kStages>([&](auto st_c) {
+      if (r0 + decltype(st_c)::value < my_rows) row(st_c);
+    });
   }
   wait_vm<0>();  // loads issued past the last row have landed (the ring is reused)
 
@@ -832,6 +895,20 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
   combine_splits<D>(ws, out, b, Hq, h0, nh, max_splits, S);
 }
 
+// Compute units of the current device (queried once per device).
+int num_cus() {
+  constexpr int kMaxDevices = 64;
+  static int cached[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < kMaxDevices && cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = 256;
+  if (dev < kMaxDevices) cached[dev] = n;
+  return n;
+}
+
 template <int D, int G>
 hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* q,
                     int32_t B, int32_t Hq, const int32_t* bt, int32_t max_pages,
@@ -839,17 +916,25 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
                     hipStream_t stream) {
   const int gq = Hq / L.num_kv_heads;
   const int n_hchunks = (gq + kHeadSlots - 1) / kHeadSlots;
-  dim3 grid(max_splits, L.num_kv_heads * n_hchunks, B);
+  // Splits per request: enough blocks for one per CU when one request runs
+  // alone, at most max_splits.  The count does not depend on the batch (a
+  // request's output is bitwise the same in any batch) nor on the lengths
+  // (they are on the device).
+  const int64_t per_split = (int64_t)L.num_kv_heads * n_hchunks;
+  const int split_cap =
+      (int)std::max<int64_t>(1, std::min<int64_t>(max_splits, (num_cus() + per_split - 1) / per_split));
+  dim3 grid(split_cap, L.num_kv_heads * n_hchunks, B);
   // completion counters first, then the split records
   uint32_t* tickets = static_cast<uint32_t*>(ws);
   float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + jfkv::kDecodeCounterBytes);
-  hipLaunchKernelGGL((decode_kernel<D, G>), grid, dim3(kThreads), 0, stream,
+  hipLaunchKernelGGL((decode_kernel<D, G>), grid, dim3(64 * waves_for<D>()), 0, stream,
                      static_cast<const uint8_t*>(pool.k_codes),
                      static_cast<const uint32_t*>(pool.k_meta),
                      static_cast<const uint8_t*>(pool.v_codes),
                      static_cast<const uint32_t*>(pool.v_meta), static_cast<const __half*>(q),
                      bt, lens, records, tickets, static_cast<__half*>(out), Hq,
-                     L.num_kv_heads, L.page_size, L.num_pages, max_pages, max_splits, n_hchunks,
+                     L.num_kv_heads, L.page_size, L.num_pages, max_pages, max_splits, split_cap,
+                     n_hchunks,
                      scale * kLog2e);
   return hipGetLastError();
 }
