@@ -234,6 +234,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--layers", type=int, default=8, help="pools rotated across steps")
     ap.add_argument("--max-splits", type=int, default=64)
+    ap.add_argument("--two-calls", action="store_true",
+                    help="decode_256k: append and attend as two launches "
+                         "(jf_kv_quantize_append + jf_decode_attn_q4) instead of jf_decode_step_q4")
     ap.add_argument("--cpu-sample", type=int, default=262144,
                     help="positions in the CPU oracle sample (0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -314,17 +317,25 @@ def main():
     for s in range(n_steps_total):
         pool = pools[s % args.layers]
         row = slice(n_cached + s, n_cached + s + 1)
-        appends.append(jfkv.bind_quantize_append(pool, k[row], v[row], cu, start, t_table, stream))
-        decodes.append(jfkv.bind_decode(pool, q[s:s + 1].view(1, hq, d), t_table, lens, 1.0,
-                                        args.max_splits, ws, out[s], stream))
+        qs = q[s:s + 1].view(1, hq, d)
+        if args.two_calls:
+            appends.append(jfkv.bind_quantize_append(pool, k[row], v[row], cu, start, t_table,
+                                                     stream))
+            decodes.append(jfkv.bind_decode(pool, qs, t_table, lens, 1.0, args.max_splits, ws,
+                                            out[s], stream))
+        else:  # one launch: the row is appended at position L - 1, then attended to
+            appends.append(lambda: None)
+            decodes.append(jfkv.bind_decode_step(pool, k[row], v[row], qs, t_table, lens, 1.0,
+                                                 args.max_splits, ws, out[s], stream))
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
            torch.cuda.Event(enable_timing=True)) for _ in range(n_steps_total)]
 
     def step(s):
         pp.reserve(seq, L)  # host page reservation (already satisfied at the window)
-        ev[s][0].record(stream)
-        appends[s]()
+        if args.two_calls:
+            ev[s][0].record(stream)
+            appends[s]()
         ev[s][1].record(stream)
         decodes[s]()
         ev[s][2].record(stream)
@@ -339,11 +350,14 @@ def main():
     wall = time.perf_counter() - t0
 
     timed = range(args.warmup, n_steps_total)
-    t_app = [ev[s][0].elapsed_time(ev[s][1]) for s in timed]
+    t_app = [ev[s][0].elapsed_time(ev[s][1]) if args.two_calls else 0.0 for s in timed]
     t_dec = [ev[s][1].elapsed_time(ev[s][2]) for s in timed]
     ms_per_step = 1e3 * wall / args.steps
     dec_ms = float(np.mean(t_dec))
-    dec_bytes = L * BYTES_PER_POSITION
+    # the step kernel's algorithmic bytes: the window's codes and (scale,
+    # bias) words, plus, when fused, the new row's fp16 K/V read and its
+    # codes and meta written
+    dec_bytes = L * BYTES_PER_POSITION + (0 if args.two_calls else 2 * hkv * d * 2 + BYTES_PER_POSITION)
     achieved = dec_bytes / (dec_ms * 1e-3) / 1e9
     log("append %.2f us  decode %.2f us (min %.2f)  wall/step %.2f us" % (
         1e3 * np.mean(t_app), 1e3 * dec_ms, 1e3 * np.min(t_dec), 1e3 * ms_per_step))
@@ -369,14 +383,20 @@ def main():
                    "pages": L // P, "max_splits": args.max_splits,
                    "splits_used": min(args.max_splits, L // P, -(-torch.cuda.get_device_properties(
                        0).multi_processor_count // hkv)),
-                   "layers_rotated": args.layers},
+                   "layers_rotated": args.layers,
+                   "step": ("jf_kv_quantize_append + jf_decode_attn_q4" if args.two_calls
+                            else "jf_decode_step_q4 (append + attend, one kernel)")},
         "hbm_GBs": achieved,
         "hbm_pct_of_peak": 100.0 * achieved / HBM_PEAK_GBS,
-        "us_per_step": {"append": 1e3 * float(np.mean(t_app)), "decode": 1e3 * dec_ms,
+        "us_per_step": {"append": (1e3 * float(np.mean(t_app)) if args.two_calls else None),
+                        "decode" if args.two_calls else "step_kernel": 1e3 * dec_ms,
                         "wall": 1e3 * ms_per_step},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
-                     "kernel": "decode_kernel (split-K partials and the in-kernel combine)",
+                     "kernel": ("decode_kernel (split-K partials and the in-kernel combine)"
+                                if args.two_calls else
+                                "decode_kernel, fused step (row append, split-K partials, "
+                                "in-kernel combine)"),
                      "algorithmic_bytes": dec_bytes},
     }
     if args.cpu_sample > 0:

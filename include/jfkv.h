@@ -229,8 +229,11 @@ jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads,
  *                with length <= 0 gets an all-zero output row
  *   softmax_scale  logits = softmax_scale * q . k
  *   max_splits   cap on partials per request and KV head (1..1024); a
- *                request with n pages uses min(max_splits, n) page-aligned
- *                splits of equal page counts, the remainder on the first
+ *                request with n pages uses S = min(max_splits, n,
+ *                ceil(compute units / (num_kv_heads * ceil(Gq / 4))))
+ *                page-aligned splits of equal page counts, the remainder on
+ *                the first (S depends on neither the batch nor the other
+ *                requests, so a request's output is the same in any batch)
  *   workspace    device scratch of at least jf_decode_workspace_bytes().
  *                Its first 262,144 bytes (completion counters) must be zero
  *                before the first call, e.g. by allocating it zero-filled;
@@ -249,6 +252,25 @@ jf_status jf_decode_attn_q4(const jf_kv_layout* layout,
                             size_t workspace_bytes, void* out,
                             hipStream_t stream);
 
+/* One decode step, append then attend, in one kernel: request b's new row
+ * (k_new, v_new: fp16 [B][Hkv][d], device) is quantized into the pool at
+ * logical position seq_lens[b] - 1 exactly as jf_kv_quantize_append would
+ * write it (same codes, scales, biases and placement; a row whose position
+ * is beyond max_pages * page_size or whose page ID is outside
+ * [0, num_pages) is not written), and the query then attends to positions
+ * 0..seq_lens[b]-1, the new row included, as in jf_decode_attn_q4 (same
+ * arguments and workspace).  One launch per decode step instead of two
+ * (append, then attend); the outputs and the pool are the same.  The row's
+ * page must be reserved and not shared. */
+jf_status jf_decode_step_q4(const jf_kv_layout* layout,
+                            const jf_kv_pool_ptrs* pool, const void* k_new,
+                            const void* v_new, const void* q, int32_t B,
+                            int32_t num_q_heads, const int32_t* block_tables,
+                            int32_t max_pages, const int32_t* seq_lens,
+                            float softmax_scale, int32_t max_splits,
+                            void* workspace, size_t workspace_bytes, void* out,
+                            hipStream_t stream);
+
 /* Chunked-prefill attention for one request: query i of the chunk sits at
  * absolute position prefix_len + i and attends to the dequantized prefix
  * positions 0..prefix_len-1 (through block_table) and, causally, to the
@@ -259,7 +281,8 @@ jf_status jf_decode_attn_q4(const jf_kv_layout* layout,
  *   block_table  int32 [max_pages] (device); pages 0..ceil(prefix_len/P)-1
  *                are read; prefix_len must be <= max_pages * page_size
  *   out      fp16 [T][num_q_heads][d] (device)
- * Products run on bf16 matrix cores with fp32 accumulation. */
+ * Products run on fp16 matrix cores with fp32 accumulation (codes enter
+ * exactly; scales and biases are applied to the fp32 results). */
 jf_status jf_prefill_attn_q4(const jf_kv_layout* layout,
                              const jf_kv_pool_ptrs* pool, const void* q,
                              const void* k_chunk, const void* v_chunk,

@@ -40,6 +40,7 @@
 #include <type_traits>
 
 #include "jfkv_internal.h"
+#include "jfkv_quant.h"
 
 namespace {
 
@@ -378,10 +379,17 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
 //           scores never leave their lanes.
 // Progress: the waves of a block meet only after their row loops; every loop
 // ends after the wave's own rows.
-template <int D, int G>
+//
+// APPEND (the fused decode step): the block of each request's last split
+// first quantizes the request's new K/V row (fp16 [B][Hkv][d], one per
+// request, at position seq_lens[b] - 1) for its KV head into the pool, then
+// attends; only that block reads the row's page, and it issues its page
+// loads after the row's stores have completed.
+template <int D, int G, bool APPEND>
 __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
-    const uint8_t* __restrict__ k_codes, const uint32_t* __restrict__ k_meta,
-    const uint8_t* __restrict__ v_codes, const uint32_t* __restrict__ v_meta,
+    uint8_t* __restrict__ k_codes, uint32_t* __restrict__ k_meta,
+    uint8_t* __restrict__ v_codes, uint32_t* __restrict__ v_meta,
+    const uint4* __restrict__ k_new, const uint4* __restrict__ v_new,
     const __half* __restrict__ q, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, float* __restrict__ ws, uint32_t* __restrict__ tickets,
     __half* __restrict__ out, int Hq, int Hkv, int P, int NP, int max_pages, int max_splits,
@@ -432,6 +440,29 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   const int n_pages = (L + P - 1) / P;
   const int S = min(split_cap, n_pages);  // split_cap <= max_splits (the record stride)
   if (split >= S) return;
+  if constexpr (APPEND) {
+    if (split == S - 1) {  // block-uniform: the block holding position seq_lens[b] - 1
+      if (wave == 0) {
+        // lanes 0 .. D/8 - 1: K dims 8 lane ..; lanes D/8 .. D/4 - 1: V
+        const int pos = seq_lens[b] - 1;  // <= L - 1 < max_pages * P unless clamped
+        const int kind = lane / (D / 8), c8 = lane % (D / 8);
+        const bool active = kind < 2 && pos < max_pages * P;
+        uint4 x = make_uint4(0, 0, 0, 0);
+        if (active) x = (kind ? v_new : k_new)[((size_t)b * Hkv + kv) * (D / 8) + c8];
+        uint32_t meta_word;
+        const uint32_t packed = jfkv::quantize8(x, G / 8, meta_word);  // whole wave
+        if (active) {
+          const int page = block_tables[(size_t)b * max_pages + pos / P];
+          if ((unsigned)page < (unsigned)NP)
+            jfkv::store_codes8(kind ? v_codes : k_codes, kind ? v_meta : k_meta, kind != 0,
+                               (int64_t)page * Hkv + kv, P, D, G, pos % P, c8, G / 8, packed,
+                               meta_word);
+        }
+        wait_vm<0>();  // the row's stores have completed
+      }
+      __syncthreads();
+    }
+  }
   int pb, pe;
   split_range(n_pages, S, split, pb, pe);
   const int t_end = min(pe * P, L);
@@ -909,8 +940,9 @@ int num_cus() {
   return n;
 }
 
-template <int D, int G>
-hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* q,
+template <int D, int G, bool APPEND>
+hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
+                    const void* v_new, const void* q,
                     int32_t B, int32_t Hq, const int32_t* bt, int32_t max_pages,
                     const int32_t* lens, float scale, int32_t max_splits, void* ws, void* out,
                     hipStream_t stream) {
@@ -927,11 +959,11 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
   // completion counters first, then the split records
   uint32_t* tickets = static_cast<uint32_t*>(ws);
   float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + jfkv::kDecodeCounterBytes);
-  hipLaunchKernelGGL((decode_kernel<D, G>), grid, dim3(64 * waves_for<D>()), 0, stream,
-                     static_cast<const uint8_t*>(pool.k_codes),
-                     static_cast<const uint32_t*>(pool.k_meta),
-                     static_cast<const uint8_t*>(pool.v_codes),
-                     static_cast<const uint32_t*>(pool.v_meta), static_cast<const __half*>(q),
+  hipLaunchKernelGGL((decode_kernel<D, G, APPEND>), grid, dim3(64 * waves_for<D>()), 0, stream,
+                     static_cast<uint8_t*>(pool.k_codes), static_cast<uint32_t*>(pool.k_meta),
+                     static_cast<uint8_t*>(pool.v_codes), static_cast<uint32_t*>(pool.v_meta),
+                     static_cast<const uint4*>(k_new), static_cast<const uint4*>(v_new),
+                     static_cast<const __half*>(q),
                      bt, lens, records, tickets, static_cast<__half*>(out), Hq,
                      L.num_kv_heads, L.page_size, L.num_pages, max_pages, max_splits, split_cap,
                      n_hchunks,
@@ -943,13 +975,15 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
 
 namespace jfkv {
 
-hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* q,
-                         int32_t B, int32_t Hq, const int32_t* bt, int32_t max_pages,
-                         const int32_t* lens, float scale, int32_t max_splits, void* ws,
-                         void* out, hipStream_t stream) {
-#define JF_ARGS L, pool, q, B, Hq, bt, max_pages, lens, scale, max_splits, ws, out, stream
-#define JF_CASE(D_, G_) \
-  if (L.head_dim == D_ && L.group_size == G_) return launch_t<D_, G_>(JF_ARGS);
+hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
+                         const void* v_new, const void* q, int32_t B, int32_t Hq,
+                         const int32_t* bt, int32_t max_pages, const int32_t* lens, float scale,
+                         int32_t max_splits, void* ws, void* out, hipStream_t stream) {
+#define JF_ARGS L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale, max_splits, ws, out, \
+                stream
+#define JF_CASE(D_, G_)                                              \
+  if (L.head_dim == D_ && L.group_size == G_)                        \
+    return k_new ? launch_t<D_, G_, true>(JF_ARGS) : launch_t<D_, G_, false>(JF_ARGS);
   JF_CASE(64, 32)
   JF_CASE(64, 64)
   JF_CASE(128, 32)

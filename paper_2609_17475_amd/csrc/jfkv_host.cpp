@@ -373,12 +373,13 @@ jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads, int32_t head
   return ok();
 }
 
-jf_status jf_decode_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
-                            const void* q, int32_t B, int32_t num_q_heads,
-                            const int32_t* block_tables, int32_t max_pages,
-                            const int32_t* seq_lens, float softmax_scale, int32_t max_splits,
-                            void* workspace, size_t workspace_bytes, void* out,
-                            hipStream_t stream) {
+namespace {
+
+jf_status decode_common(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                        const void* k_new, const void* v_new, const void* q, int32_t B,
+                        int32_t num_q_heads, const int32_t* block_tables, int32_t max_pages,
+                        const int32_t* seq_lens, float softmax_scale, int32_t max_splits,
+                        void* workspace, size_t workspace_bytes, void* out, hipStream_t stream) {
   jf_status st = check_layout(layout);
   if (st) return st;
   if ((st = check_pool(pool))) return st;
@@ -399,10 +400,35 @@ jf_status jf_decode_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* p
   if (!(softmax_scale == softmax_scale) || softmax_scale == INFINITY ||
       softmax_scale == -INFINITY)
     return fail(JF_ERR_INVALID, "softmax_scale must be finite");
-  return device_status(jfkv::launch_decode(*layout, *pool, q, B, num_q_heads, block_tables,
-                                           max_pages, seq_lens, softmax_scale, max_splits,
-                                           workspace, out, stream),
+  return device_status(jfkv::launch_decode(*layout, *pool, k_new, v_new, q, B, num_q_heads,
+                                           block_tables, max_pages, seq_lens, softmax_scale,
+                                           max_splits, workspace, out, stream),
                        "decode launch");
+}
+
+}  // namespace
+
+jf_status jf_decode_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                            const void* q, int32_t B, int32_t num_q_heads,
+                            const int32_t* block_tables, int32_t max_pages,
+                            const int32_t* seq_lens, float softmax_scale, int32_t max_splits,
+                            void* workspace, size_t workspace_bytes, void* out,
+                            hipStream_t stream) {
+  return decode_common(layout, pool, nullptr, nullptr, q, B, num_q_heads, block_tables,
+                       max_pages, seq_lens, softmax_scale, max_splits, workspace,
+                       workspace_bytes, out, stream);
+}
+
+jf_status jf_decode_step_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                            const void* k_new, const void* v_new, const void* q, int32_t B,
+                            int32_t num_q_heads, const int32_t* block_tables,
+                            int32_t max_pages, const int32_t* seq_lens, float softmax_scale,
+                            int32_t max_splits, void* workspace, size_t workspace_bytes,
+                            void* out, hipStream_t stream) {
+  if (!k_new || !v_new) return fail(JF_ERR_INVALID, "NULL device pointer");
+  return decode_common(layout, pool, k_new, v_new, q, B, num_q_heads, block_tables, max_pages,
+                       seq_lens, softmax_scale, max_splits, workspace, workspace_bytes, out,
+                       stream);
 }
 
 jf_status jf_prefill_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,

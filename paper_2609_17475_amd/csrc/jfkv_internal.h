@@ -33,7 +33,10 @@ hipError_t launch_quantize_append(const jf_kv_layout& L, const jf_kv_pool_ptrs& 
                                   int32_t max_pages, int32_t total_tok,
                                   hipStream_t stream);
 
+// k_new/v_new non-null: the fused decode step (append one row per request
+// at position seq_lens[b] - 1, then attend).
 hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
+                         const void* k_new, const void* v_new,
                          const void* q, int32_t B, int32_t num_q_heads,
                          const int32_t* block_tables, int32_t max_pages,
                          const int32_t* seq_lens, float softmax_scale,

@@ -14,30 +14,17 @@
 #include <hip/hip_runtime.h>
 
 #include "jfkv_internal.h"
+#include "jfkv_quant.h"
 
 #pragma clang fp contract(off)
 
 namespace {
 
-// Monotone unsigned key of an fp16 bit pattern (-0 below +0; finite values).
-__device__ __forceinline__ uint32_t order_key(uint32_t h) {
-  return (h & 0x8000u) ? (~h & 0xffffu) : (h | 0x8000u);
-}
-__device__ __forceinline__ uint32_t from_key(uint32_t k) {
-  return (k & 0x8000u) ? (k & 0x7fffu) : (~k & 0xffffu);
-}
-
-__device__ __forceinline__ float h2f(uint32_t bits) {
-  return __half2float(__ushort_as_half((unsigned short)bits));
-}
-
-// fp16 of a positive binary32 value, rounded toward +inf: round to nearest
-// even, then step up one ulp if that fell below.
-__device__ __forceinline__ uint32_t f2h_up_pos(float x) {
-  uint32_t h = __half_as_ushort(__float2half_rn(x));
-  if (h2f(h) < x) h += 1;  // positive patterns are ordered like their values
-  return h;
-}
+using jfkv::quantize8;
+__device__ __forceinline__ uint32_t order_key(uint32_t h) { return jfkv::q_order_key(h); }
+__device__ __forceinline__ uint32_t from_key(uint32_t k) { return jfkv::q_from_key(k); }
+__device__ __forceinline__ float h2f(uint32_t bits) { return jfkv::q_h2f(bits); }
+__device__ __forceinline__ uint32_t f2h_up_pos(float x) { return jfkv::q_f2h_up_pos(x); }
 
 // Latency-oriented kernel for small appends (a decode step's rows): one
 // group of G elements is handled by G/8 consecutive lanes, each holding 8
@@ -69,20 +56,10 @@ __global__ __launch_bounds__(256) void quantize_small_kernel(
 
   uint4 x = make_uint4(0, 0, 0, 0);
   if (active) x = (kind ? v_new : k_new)[(int64_t)row * (Hkv * D / 8) + kv * (D / 8) + c8];
-  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-
-  uint32_t kmin = 0xffffu, kmax = 0u;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    uint32_t k0 = order_key(w[i] & 0xffffu), k1 = order_key(w[i] >> 16);
-    kmin = min(kmin, min(k0, k1));
-    kmax = max(kmax, max(k0, k1));
-  }
-  // reduce over the lpg lanes of the group (aligned runs of lpg lanes)
-  for (int off = 1; off < lpg; off <<= 1) {
-    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, off));
-    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, off));
-  }
+  // codes and (scale, bias) of the lane's 8 values; the group's lpg lanes
+  // (aligned runs) exchange its minimum and maximum
+  uint32_t meta_word;
+  const uint32_t packed = quantize8(x, lpg, meta_word);
   if (!active) return;
 
   // request of this row and its logical position
@@ -100,46 +77,9 @@ __global__ __launch_bounds__(256) void quantize_small_kernel(
   if (page < 0 || page >= NP) return;
   const int32_t slot = (int32_t)(pos % P);
 
-  const uint32_t mn_bits = from_key(kmin), mx_bits = from_key(kmax);
-  const float mn = h2f(mn_bits), mx = h2f(mx_bits);
-  // bias: fp16 of mn rounded toward -inf; mn is an fp16 value, so exact
-  const uint32_t bias_bits = mn_bits;
-  const float range = __fsub_rn(mx, mn);
-  const float step = __fdiv_rn(range, 15.0f);
-  const uint32_t scale_bits = (range == 0.0f) ? 0u : f2h_up_pos(step);
-  const float sf = h2f(scale_bits), bf = h2f(bias_bits);
-
-  uint32_t packed = 0;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    uint32_t code = 0;
-    if (scale_bits != 0) {
-      const float xi = h2f((w[i >> 1] >> ((i & 1) * 16)) & 0xffffu);
-      const float r = __fdiv_rn(__fsub_rn(xi, bf), sf);
-      float qf = __builtin_rintf(r);
-      qf = fminf(fmaxf(qf, 0.0f), 15.0f);
-      code = (uint32_t)qf;
-    }
-    packed |= code << (4 * i);
-  }
-
-  const int32_t g = (c8 * 8) / G;
-  const int64_t ph = (int64_t)page * Hkv + kv;  // (page, kv head) block
-  if (kind == 0) {
-    uint32_t* dst = reinterpret_cast<uint32_t*>(k_codes + (ph * P + slot) * (D / 2)) + c8;
-    *dst = packed;
-  } else {
-    // dims 8c..8c+3 form 4-dim chunk u = 2c, dims 8c+4..8c+7 chunk 2c+1
-    uint16_t* base = reinterpret_cast<uint16_t*>(v_codes + ph * P * (D / 2) +
-                                                 ((int64_t)(slot >> 1) * (D / 4) + 2 * c8) * 4 +
-                                                 (slot & 1) * 2);
-    base[0] = (uint16_t)(packed & 0xffffu);
-    base[2] = (uint16_t)(packed >> 16);
-  }
-  if ((c8 % lpg) == 0) {
-    uint32_t* meta = kind ? v_meta : k_meta;
-    meta[(ph * P + slot) * (D / G) + g] = scale_bits | (bias_bits << 16);
-  }
+  const int64_t ph = (int64_t)page * Hkv + kv;  // (page, kv head) run
+  jfkv::store_codes8(kind ? v_codes : k_codes, kind ? v_meta : k_meta, kind != 0, ph, P, D, G,
+                     slot, c8, lpg, packed, meta_word);
 }
 
 // Appends of at least this many rows use the row-tiled kernel below.

@@ -27,7 +27,7 @@ EXPORTS = [
     "jf_page_table_set_length", "jf_page_table_release", "jf_page_table_export",
     "jf_page_table_stats", "jf_page_table_info",
     "jf_kv_quantize_append", "jf_decode_workspace_bytes", "jf_decode_attn_q4",
-    "jf_prefill_attn_q4",
+    "jf_decode_step_q4", "jf_prefill_attn_q4",
 ]
 
 
@@ -79,6 +79,8 @@ def _load():
         "jf_decode_workspace_bytes": (st, [i32, i32, i32, i32, ctypes.POINTER(sz)]),
         "jf_decode_attn_q4": (st, [P, P, P, i32, i32, P, i32, P, ctypes.c_float, i32, P, sz, P,
                                    P]),
+        "jf_decode_step_q4": (st, [P, P, P, P, P, i32, i32, P, i32, P, ctypes.c_float, i32, P, sz,
+                                   P, P]),
         "jf_prefill_attn_q4": (st, [P, P, P, P, P, i32, i32, P, i32, i32, ctypes.c_float, P, P]),
     }
     for name, (res, args) in sig.items():
@@ -250,26 +252,51 @@ def jf_decode_workspace_bytes(B: int, num_q_heads: int, head_dim: int, max_split
     return n.value
 
 
-def jf_decode_attn_q4(pool: KVPool, q, block_tables, seq_lens, softmax_scale: float,
-                      max_splits: int, workspace, out, stream=None):
+def _check_decode_args(pool: KVPool, q, block_tables, seq_lens, workspace, out):
     import torch
     _dev_check(q, "q", torch.float16)
     _dev_check(block_tables, "block_tables", torch.int32)
     _dev_check(seq_lens, "seq_lens", torch.int32)
     _dev_check(workspace, "workspace")
     _dev_check(out, "out", torch.float16)
-    lay = pool.layout
     B, Hq, d = q.shape
-    if d != lay.head_dim or out.shape != q.shape:
+    if d != pool.layout.head_dim or out.shape != q.shape:
         raise ValueError("q/out must be [B][Hq][head_dim]")
     if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
         raise ValueError("block_tables [B][max_pages], seq_lens [B]")
+
+
+def jf_decode_attn_q4(pool: KVPool, q, block_tables, seq_lens, softmax_scale: float,
+                      max_splits: int, workspace, out, stream=None):
+    _check_decode_args(pool, q, block_tables, seq_lens, workspace, out)
+    lay = pool.layout
+    B, Hq, d = q.shape
     ptrs = pool.ptrs()
     _check(lib.jf_decode_attn_q4(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), B, Hq,
                                  _ptr(block_tables), block_tables.shape[1], _ptr(seq_lens),
                                  float(softmax_scale), int(max_splits), _ptr(workspace),
                                  workspace.numel() * workspace.element_size(), _ptr(out),
                                  _stream(stream)))
+
+
+def jf_decode_step_q4(pool: KVPool, k_new, v_new, q, block_tables, seq_lens,
+                      softmax_scale: float, max_splits: int, workspace, out, stream=None):
+    """Append request b's row (k_new/v_new fp16 [B][Hkv][d]) at position
+    seq_lens[b] - 1, then attend over seq_lens[b] positions; one kernel."""
+    import torch
+    _dev_check(k_new, "k_new", torch.float16)
+    _dev_check(v_new, "v_new", torch.float16)
+    lay = pool.layout
+    B = q.shape[0]
+    if tuple(k_new.shape) != (B, lay.num_kv_heads, lay.head_dim) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [B][Hkv][head_dim]")
+    _check_decode_args(pool, q, block_tables, seq_lens, workspace, out)
+    ptrs = pool.ptrs()
+    _check(lib.jf_decode_step_q4(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new), _ptr(v_new),
+                                 _ptr(q), B, q.shape[1], _ptr(block_tables), block_tables.shape[1],
+                                 _ptr(seq_lens), float(softmax_scale), int(max_splits),
+                                 _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                 _ptr(out), _stream(stream)))
 
 
 def jf_prefill_attn_q4(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len: int,
@@ -328,6 +355,18 @@ def bind_decode(pool: KVPool, q, block_tables, seq_lens, softmax_scale, max_spli
             _stream(stream))
     return BoundCall(lib.jf_decode_attn_q4, args,
                      (lay, ptrs, pool, q, block_tables, seq_lens, workspace, out))
+
+
+def bind_decode_step(pool: KVPool, k_new, v_new, q, block_tables, seq_lens, softmax_scale,
+                     max_splits, workspace, out, stream=None) -> BoundCall:
+    lay, ptrs = pool.layout, pool.ptrs()
+    B, Hq, _ = q.shape
+    args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new), _ptr(v_new), _ptr(q), B, Hq,
+            _ptr(block_tables), block_tables.shape[1], _ptr(seq_lens), float(softmax_scale),
+            int(max_splits), _ptr(workspace), workspace.numel() * workspace.element_size(),
+            _ptr(out), _stream(stream))
+    return BoundCall(lib.jf_decode_step_q4, args,
+                     (lay, ptrs, pool, k_new, v_new, q, block_tables, seq_lens, workspace, out))
 
 
 def bind_prefill(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len, softmax_scale, out,
