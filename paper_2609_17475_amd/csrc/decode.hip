@@ -307,7 +307,7 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
                                int max_splits, int S) {
   constexpr int CPL = D / 4;      // float4 chunks of a record's o
   constexpr int KP = 64 / CPL;    // lanes per chunk (split parts)
-  constexpr int KCH = 8;          // splits per lane per round
+  constexpr int KCH = 16;         // splits per lane per round
   static_assert(KP >= 1 && 64 % CPL == 0, "");
   const int lane = threadIdx.x & 63, h = threadIdx.x >> 6;
   if (h >= nh) return;
@@ -430,6 +430,40 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int split = blockIdx.x;
 
+  const int l16 = lane & 15, q4 = lane >> 4;
+  const int hs = l16 & 3, gs = l16 >> 2;  // accumulator column: head slot, column slot
+  const bool head_on = hs < nh;
+
+  // Loads issued together, before anything waits for the request's length:
+  // the query words of head hs over the dims of quarter q4 (the lane's
+  // k-slots), the page IDs of this split's range as it is when the request
+  // fills its table (the common case; read again below otherwise), and, in
+  // the fused step, the new row's fp16 values (lanes 0 .. D/8 - 1: K dims
+  // 8 lane ..; lanes D/8 .. D/4 - 1: V) in the block that would hold it.
+  uint4 qraw[NHALF][WQ];
+  {
+    const uint4* src = reinterpret_cast<const uint4*>(
+        q + ((size_t)b * Hq + h0 + min(hs, nh - 1)) * D + DQ * q4);
+#pragma unroll
+    for (int e = 0; e < NHALF; ++e)
+#pragma unroll
+      for (int kb = 0; kb < WQ; ++kb) qraw[e][kb] = src[(HD / 8) * e + kb];
+  }
+  const int S_full = min(split_cap, max_pages);
+  int pb_full, pe_full;
+  split_range(max_pages, S_full, split, pb_full, pe_full);
+  const int pg_full = (split < S_full && lane < pe_full - pb_full)
+                          ? block_tables[(size_t)b * max_pages + pb_full + lane]
+                          : -1;
+  const int app_kind = lane / (D / 8), app_c8 = lane % (D / 8);
+  // (every lane loads, lanes D/4 .. again from K or V, so that the branch
+  // stays block-uniform and the value is not needed before it is used)
+  const uint4* app_src = ((app_kind & 1) ? v_new : k_new) + ((size_t)b * Hkv + kv) * (D / 8) + app_c8;
+  uint4 app_x;
+  if constexpr (APPEND) {
+    if (split == S_full - 1) app_x = *app_src;
+  }
+
   const int L = min(seq_lens[b], max_pages * P);
   if (L <= 0) {  // an empty request: all-zero output rows, written by split 0
     if (split == 0)
@@ -440,29 +474,6 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   const int n_pages = (L + P - 1) / P;
   const int S = min(split_cap, n_pages);  // split_cap <= max_splits (the record stride)
   if (split >= S) return;
-  if constexpr (APPEND) {
-    if (split == S - 1) {  // block-uniform: the block holding position seq_lens[b] - 1
-      if (wave == 0) {
-        // lanes 0 .. D/8 - 1: K dims 8 lane ..; lanes D/8 .. D/4 - 1: V
-        const int pos = seq_lens[b] - 1;  // <= L - 1 < max_pages * P unless clamped
-        const int kind = lane / (D / 8), c8 = lane % (D / 8);
-        const bool active = kind < 2 && pos < max_pages * P;
-        uint4 x = make_uint4(0, 0, 0, 0);
-        if (active) x = (kind ? v_new : k_new)[((size_t)b * Hkv + kv) * (D / 8) + c8];
-        uint32_t meta_word;
-        const uint32_t packed = jfkv::quantize8(x, G / 8, meta_word);  // whole wave
-        if (active) {
-          const int page = block_tables[(size_t)b * max_pages + pos / P];
-          if ((unsigned)page < (unsigned)NP)
-            jfkv::store_codes8(kind ? v_codes : k_codes, kind ? v_meta : k_meta, kind != 0,
-                               (int64_t)page * Hkv + kv, P, D, G, pos % P, c8, G / 8, packed,
-                               meta_word);
-        }
-        wait_vm<0>();  // the row's stores have completed
-      }
-      __syncthreads();
-    }
-  }
   int pb, pe;
   split_range(n_pages, S, split, pb, pe);
   const int t_end = min(pe * P, L);
@@ -483,24 +494,24 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     const int k = 64 * grp + lane;
     return (k < n_split_pages) ? block_tables[(size_t)b * max_pages + pb + k] : -1;
   };
-  int pg_grp = load_group(0);
+  const bool full_table = n_pages == max_pages;  // then pb, pe are pb_full, pe_full
+  int pg_grp = full_table ? pg_full : load_group(0);
   int cur_grp = 0;
 
-  const int l16 = lane & 15, q4 = lane >> 4;
-  const int hs = l16 & 3, gs = l16 >> 2;  // accumulator column: head slot, column slot
-  const bool head_on = hs < nh;
-
-  // query words of head hs over the dims of quarter q4, the lane's k-slots
-  // (loaded with the page IDs, turned into operands once the first rows'
-  // loads are in flight)
-  uint4 qraw[NHALF][WQ];
-  {
-    const uint4* src = reinterpret_cast<const uint4*>(
-        q + ((size_t)b * Hq + h0 + min(hs, nh - 1)) * D + DQ * q4);
-#pragma unroll
-    for (int e = 0; e < NHALF; ++e)
-#pragma unroll
-      for (int kb = 0; kb < WQ; ++kb) qraw[e][kb] = src[(HD / 8) * e + kb];
+  // The fused step's new row, at position seq_lens[b] - 1 = L - 1, lies in
+  // the last row of the last split.  The wave that streams that row
+  // quantizes it (below, once its first page loads are in flight): it
+  // stores the codes and (scale, bias) words to the pool, and writes the
+  // same bytes into its LDS stage after the row's page loads have landed,
+  // since those loads may still see the slot's previous bytes.  Nothing
+  // waits for the stores.
+  int app_pos = -1;  // >= 0: this wave appends the row at that position
+  if constexpr (APPEND) {
+    const int pos = seq_lens[b] - 1;
+    if (split == S - 1 && pos < max_pages * P && ((pos - pb * P) / kRowPos) % kWaves == wave) {
+      app_pos = pos;
+      if (!full_table) app_x = *app_src;
+    }
   }
 
   // Per-lane parts of the load addresses (the row parts are scalar).  A DMA
@@ -606,6 +617,23 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     static_for<kStages>([&](auto st_c) { issue(st_c, decltype(st_c)::value < my_rows); });
   }
 
+  // ---- the fused step's row: quantized by the whole wave (the first page
+  // loads are in flight meanwhile), then stored to the pool
+  uint32_t app_packed = 0, app_meta = 0;
+  if constexpr (APPEND) {
+    if (app_pos >= 0) {
+      app_packed = jfkv::quantize8(app_x, G / 8, app_meta);
+      const int pidx = app_pos / P - pb;  // wave-uniform
+      const int page = ((pidx >> 6) == cur_grp)
+                           ? __builtin_amdgcn_readlane(pg_grp, pidx & 63)
+                           : block_tables[(size_t)b * max_pages + app_pos / P];
+      if (app_kind < 2 && (unsigned)page < (unsigned)NP)
+        jfkv::store_codes8(app_kind ? v_codes : k_codes, app_kind ? v_meta : k_meta,
+                           app_kind != 0, (int64_t)page * Hkv + kv, P, D, G, app_pos % P, app_c8,
+                           G / 8, app_packed, app_meta);
+    }
+  }
+
   // ---- Q' operands.  Score column hs + 4 gs holds head hs restricted to the
   // dims of scale group gs % NGH of each half (columns with equal group are
   // copies), so each column's sum has one scale; k-slots (n0, n4, n1, n5, n2,
@@ -687,6 +715,32 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     constexpr int OFF = ST * kStageBytes;
     // wait until only the kStages - 1 rows after this one are in flight
     wait_vm<DMAS_PER_ROW * (kStages - 1)>();
+    if constexpr (APPEND) {
+      // the fused step's row: its bytes in the stage, laid out as the page
+      // loads place them (K quarter swizzle, V position pairs, meta
+      // transposed to [group][position])
+      if (app_pos >= t_row && app_pos < t_row + kRowPos) {
+        const int p = app_pos - t_row;
+        const uint32_t st = ring_lds + OFF;
+        if (app_kind == 0) {
+          const int qd = app_c8 >> 2;
+          const int f = ((p >> 1) & 1) | (((p >> 3) & 1) << 1);
+          const uint32_t a = st + (D / 2) * p + 16 * (kSwz ? (qd ^ f) : qd) + 4 * (app_c8 & 3);
+          asm volatile("ds_write_b32 %0, %1" : : "v"(a), "v"(app_packed) : "memory");
+        } else if (app_kind == 1) {
+          const int sp = p >> 1, u0 = 2 * app_c8;
+          const int c16 = kSwz ? ((u0 >> 2) ^ (4 * ((sp >> 2) & 1))) : (u0 >> 2);
+          const uint32_t a = st + KB + D * sp + 16 * c16 + 4 * (u0 & 3) + 2 * (p & 1);
+          asm volatile("ds_write_b16 %0, %1\n\tds_write_b16 %0, %2 offset:4"
+                       : : "v"(a), "v"(app_packed & 0xffffu), "v"(app_packed >> 16) : "memory");
+        }
+        if (app_kind < 2 && (app_c8 % (G / 8)) == 0) {
+          const uint32_t a = st + 2 * KB + (app_kind ? kMetaBytes : 0) +
+                             4 * (((app_c8 * 8) / G) * kRowPos + p);
+          asm volatile("ds_write_b32 %0, %1" : : "v"(a), "v"(app_meta) : "memory");
+        }
+      }
+    }
     const bool pg_ok = stage_ok[ST];
     const bool full = pg_ok && t_row + kRowPos <= t_end;  // wave-uniform
 
