@@ -281,8 +281,9 @@ jf_status jf_decode_step_q4(const jf_kv_layout* layout,
  *   block_table  int32 [max_pages] (device); pages 0..ceil(prefix_len/P)-1
  *                are read; prefix_len must be <= max_pages * page_size
  *   out      fp16 [T][num_q_heads][d] (device)
- * Products run on fp16 matrix cores with fp32 accumulation (codes enter
- * exactly; scales and biases are applied to the fp32 results). */
+ * Products run on fp16 matrix cores with fp32 accumulation.  Key codes
+ * enter exactly, with scales and biases applied to the fp32 scores; values
+ * enter as scale * code + bias rounded once to fp16. */
 jf_status jf_prefill_attn_q4(const jf_kv_layout* layout,
                              const jf_kv_pool_ptrs* pool, const void* q,
                              const void* k_chunk, const void* v_chunk,

@@ -1,38 +1,44 @@
 // Chunked-prefill attention over the paged 4-bit prefix plus the chunk's own
 // fp16 rows, on gfx950 matrix cores (v_mfma_f32_16x16x32_f16, fp32
-// accumulate).
+// accumulation).
 //
 // The paper's prefill consumes the compressed history as floating operands
 // of a fused attention (Sec. 3.1, "Decode and prefill need different
 // kernels"; Appendix A, Table codec: page lookup, unpack and reconstruction
 // fused, writing only the operands); eq. layerbytes is the size of those
 // reconstructed operands, which it bounds by processing head groups
-// (eq. groupattention).  Here nothing reconstructed reaches HBM: each block
-// stages one 64-key tile of 4-bit codes at a time into LDS and consumes it.
+// (eq. groupattention).  Here the reconstructed operands never reach HBM:
+// a block of waves shares one KV head and reconstructs one 64-key tile of
+// K and V at a time into LDS, double-buffered, while the previous tile is
+// consumed by the matrix cores.
 //
-// Exactness: the matrix products run on the codes themselves (integers
-// 0..15, exact in fp16) against the exact fp16 query, and the affine
-// per-group scale and bias are folded in afterwards:
-//   q . k^_t = sum_g s_tg (q_g . c_tg) + b_tg * sum(q_g)
-//   sum_t p_t v^_t[i] = sum_t (p_t s_tg) c_t[i] + sum_t p_t b_tg   (i in g)
-// so the only roundings beyond fp32 accumulation are p_t to fp16 and the
-// product p_t * s_tg to fp16 (both 2^-11 relative, unbiased).  Rounding the
-// dequantized values themselves to a 16-bit type instead costs up to half an
-// ulp of |v^|, which for large-magnitude channels exceeds the tolerance.
-// The chunk's own fp16 rows use the same path with scale 1 and bias 0.
+// Operands: a 4-bit code masked into the low nibble of an fp16 half that
+// holds 1024.0 is 1024 + code exactly, so one AND-OR and one packed
+// subtraction give two exact codes.
+//   K: the tile holds the exact codes; the scores of each scale group come
+//      from their own accumulator and are scaled in fp32, and the bias part
+//      (bias_g * sum of the query over group g) is one more product whose
+//      k-slots carry (b_g, b_g) x (hi, lo) of the query's fp32 group sums.
+//      Rounding the reconstructed keys to fp16 instead would move the
+//      scores of large-magnitude channels by up to half an fp16 ulp.
+//   V: the tile holds scale * code + bias rounded once to fp16 (one packed
+//      FMA); its rounding enters the output averaged over the keys.
+// The chunk's own rows are fp16 already: K with scale 1 and bias 0, V as is.
 //
-// Block = 4 waves, 128 query rows; a row is (chunk position i, query head h
-// of the block's KV head), position-major.  Each wave owns 32 rows (two
-// 16-row MFMA tiles).  Per key tile:
-//   S^T = K Q^T (A = codes tile [key][dim] from LDS, B = Q^T in registers),
-//   one accumulator per scale group, folded into S^T; the bias term is one
-//   more MFMA whose k-slots carry (b_g, b_g) x (hi(sum q_g), lo(sum q_g));
-//   online softmax per query row (a lane holds one row of S^T per tile, so
-//   row max and sum need only the 4 lanes sharing lane%16);
-//   O^T += V^T P'^T (A = codes tile [dim][key] from LDS, B = p*s per group).
-// Accumulator layout used (16x16 MFMA): lane l, element r holds row
-// 4*(l/16)+r, column l%16.  Operand k-slots are whatever the hardware pairs
-// between A and B; both sides are filled in the same order.
+// Block = 8 waves sharing KV head kv, 32 query rows per wave (16 at d = 256); a row is
+// (chunk position i, query head h of kv), position-major.  Per 64-key tile:
+//   S^T = K Q^T      (A = K code tile [key][dim] from LDS, B = Q^T in
+//                     registers, per scale group; a lane holds one query
+//                     column, 4 keys per 16-key tile, so row max and sum
+//                     need the 4 lanes sharing lane % 16 only)
+//   online softmax   (one running maximum per query row, raised only when a
+//                     tile's maximum exceeds it by more than kTau, so
+//                     p <= 2^kTau stays well inside fp16 and rescaling of
+//                     the accumulators is rare)
+//   O^T += V^T P^T   (A = V^ tile [dim][key] from LDS, B = p as fp16)
+// Accumulator layout (16x16 MFMA): lane l, element r holds row 4*(l/16)+r,
+// column l%16.  Operand k-slots are whatever the hardware pairs between A
+// and B; both sides are filled in the same order.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -45,79 +51,99 @@ typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kThreads = 256;
-constexpr int kRows = 128;  // query rows per block
-constexpr int kKeys = 64;   // keys per tile
-constexpr int kPad = 8;     // fp16 padding of an LDS tile row
-constexpr int kMaxGroups = 8;
+constexpr int kKeys = 64;          // keys per tile (a page holds whole tiles)
+constexpr float kTau = 8.0f;       // lazy-rescale margin, log2 units
+constexpr float kMinit = -1e30f;   // initial running maximum (finite)
+
+constexpr int kWaves = 8;          // waves per block: two per SIMD
+// 16-row MFMA tiles of query rows per wave (the registers of d = 256 hold one)
+template <int D>
+constexpr int row_tiles() { return D > 128 ? 1 : 2; }
+
+__device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
+__device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uint32_t, v); }
 
 // Position of key k (0..63) inside a V^T row: within each 32-key block the
 // keys 4q..4q+3 and 16+4q..16+4q+3 sit together, so the eight keys one lane
-// feeds to a 32-key MFMA step are contiguous.
+// feeds to a 32-key MFMA step are contiguous (and pairs 2s, 2s+1 adjacent).
 __device__ __forceinline__ int vperm(int k) {
   const int kk = k & 31;
   return (k & 32) + 8 * ((kk & 15) >> 2) + 4 * (kk >> 4) + (kk & 3);
 }
-
-__device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
-__device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uint32_t, v); }
-__device__ __forceinline__ float lo_f(uint32_t u) { return (float)as_h2(u).x; }
-__device__ __forceinline__ float hi_f(uint32_t u) { return (float)as_h2(u).y; }
-
-// Eight 4-bit codes (nibble n at bits 4n) -> fp16 pairs (n0,n4), (n1,n5),
-// (n2,n6), (n3,n7), exact.
-__device__ __forceinline__ void unpack8(uint32_t w, h2 out[4]) {
-  const uint32_t M = 0x64006400u;  // fp16 1024: mantissa ulp 1
-  const uint32_t w8 = w >> 8;
-  const h2 c1024 = {(_Float16)1024.0f, (_Float16)1024.0f};
-  const h2 c64 = {(_Float16)64.0f, (_Float16)64.0f};
-  const h2 c16th = {(_Float16)0.0625f, (_Float16)0.0625f};
-  out[0] = as_h2((w & 0x000F000Fu) | M) - c1024;
-  out[1] = __builtin_elementwise_fma(as_h2((w & 0x00F000F0u) | M), c16th, -c64);
-  out[2] = as_h2((w8 & 0x000F000Fu) | M) - c1024;
-  out[3] = __builtin_elementwise_fma(as_h2((w8 & 0x00F000F0u) | M), c16th, -c64);
-}
-
-// Dims of one 8-dim chunk are stored in K tiles in unpack order.
+// Dims of one 8-dim chunk are stored in K tiles in this order (the order the
+// nibble unpacking produces): slot e holds dim kperm8(e).
 __device__ __forceinline__ int kperm8(int e) { return (e >> 1) + 4 * (e & 1); }
 
+// Nibble 0 of each 16-bit half of w (the caller shifts by 4 n for nibble n):
+// the exact codes as fp16, and scale * code + bias with one rounding.
+__device__ __forceinline__ h2 code2(uint32_t w) {
+  return as_h2((w & 0x000F000Fu) | 0x64006400u) - h2{(_Float16)1024.0f, (_Float16)1024.0f};
+}
+__device__ __forceinline__ h2 deq2(uint32_t w, h2 s, h2 b) {
+  return __builtin_elementwise_fma(code2(w), s, b);
+}
+
+__device__ __forceinline__ f32x4 mfma(h8 a, h8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void prefill_kernel(
+__global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     const uint8_t* __restrict__ k_codes, const uint32_t* __restrict__ k_meta,
     const uint8_t* __restrict__ v_codes, const uint32_t* __restrict__ v_meta,
     const __half* __restrict__ q, const __half* __restrict__ k_chunk,
     const __half* __restrict__ v_chunk, const int32_t* __restrict__ block_table,
-    __half* __restrict__ out, int T, int Hq, int Hkv, int P, int NP, int max_pages,
-    int prefix_len, float scale_log2) {
-  constexpr int KSTEPS = D / 32;  // 32-dim MFMA steps over head_dim
-  constexpr int DT = D / 16;      // 16-dim tiles of O^T
-  constexpr int ng = D / G;       // scale groups per head
-  constexpr int steps_per_group = G / 32;
-  static_assert(ng <= kMaxGroups, "");
-  __shared__ __attribute__((aligned(16))) _Float16 sK[kKeys][D + kPad];
-  __shared__ __attribute__((aligned(16))) _Float16 sV[D][kKeys + kPad];
-  __shared__ __attribute__((aligned(16))) uint32_t sKm[kMaxGroups][kKeys];  // (scale, bias)
-  __shared__ __attribute__((aligned(16))) uint32_t sVm[kMaxGroups][kKeys];
+    __half* __restrict__ out, int T, int Hq, int Hkv, int P, int NP, int prefix_len,
+    float scale_log2) {
+  constexpr int NR = row_tiles<D>();
+  constexpr int kThreads = 64 * kWaves;
+  constexpr int kRowsPerWave = 16 * NR;
+  constexpr int kRows = kRowsPerWave * kWaves;
+  constexpr int KSTEPS = D / 32;           // 32-dim MFMA steps of a score
+  constexpr int DT = D / 16;               // 16-dim tiles of O^T
+  constexpr int NG = D / G;                // scale groups per vector
+  constexpr int KP = D + 8;                // K^ row pitch (fp16)
+  constexpr int VP = kKeys + 8;            // V^T row pitch (fp16)
+  constexpr int QPK = D / 32;              // 16-byte K code chunks per key
+  constexpr int CPV = D / 16;              // 16-byte V code chunks per key pair
+  constexpr int KCH = kKeys * QPK;         // K code chunks per tile
+  constexpr int VCH = (kKeys / 2) * CPV;   // V code chunks per tile
+  constexpr int NCH = (KCH + VCH + kThreads - 1) / kThreads;
+  static_assert(G >= 32, "a K chunk (32 dims) and a V chunk (16 dims) lie in one group");
 
-  const int kv = blockIdx.y;
+  __shared__ __attribute__((aligned(16))) _Float16 sK[2][kKeys][KP];
+  __shared__ __attribute__((aligned(16))) uint32_t sKm[2][NG][kKeys];  // K (scale, bias)
+  __shared__ __attribute__((aligned(16))) _Float16 sV[2][D][VP];
+
+  // KV head fastest: the blocks of one KV head land on one XCD (round-robin
+  // dispatch over the 8 XCDs), so its tiles are shared in that XCD's L2.
+  const int kv = blockIdx.x % Hkv;
+  const int rb = blockIdx.x / Hkv;
   const int gq = Hq / Hkv;
-  const int r0 = blockIdx.x * kRows;
+  const int r0 = rb * kRows;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
+  const size_t head_codes = (size_t)P * (D / 2);
 
-  // ---- Q^T operands (exact fp16, dims in unpack order) and per-group sums
-  h8 qb[2][KSTEPS];
-  h8 qsum_b[2];  // bias-MFMA operand: slots (2g, 2g+1) = hi, lo of sum q_g
-  int row_pos[2];
+  // scores are scaled by |scale| (log2 units) in the exponent; a negative
+  // scale negates the query instead (exact).  A positive floor keeps masked
+  // (-inf) scores at -inf when the scale is 0.
+  const float cabs = fmaxf(fabsf(scale_log2), 1e-30f);
+  const _Float16 qsgn = scale_log2 < 0.0f ? (_Float16)-1.0f : (_Float16)1.0f;
+
+  // ---- Q^T operands (exact fp16, dims in K^ storage order)
+  h8 qb[NR][KSTEPS];
+  h8 qsum_b[NR];  // bias-product operand: slots (2g, 2g+1) = hi, lo of sum q_g
+  int row_i[NR];
 #pragma unroll
-  for (int n = 0; n < 2; ++n) {
-    const int r = r0 + 32 * wave + 16 * n + l16;
+  for (int n = 0; n < NR; ++n) {
+    const int r = r0 + kRowsPerWave * wave + 16 * n + l16;
     const int i = r / gq, hh = r % gq;
-    row_pos[n] = (i < T) ? i : -1;
-    float gs[ng];
+    row_i[n] = i;
+    float gsum[NG];
 #pragma unroll
-    for (int g = 0; g < ng; ++g) gs[g] = 0.0f;
+    for (int g = 0; g < NG; ++g) gsum[g] = 0.0f;
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
       h8 v;
@@ -131,13 +157,11 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(
           e8[2 * e] = as_h2(w[e]).x;
           e8[2 * e + 1] = as_h2(w[e]).y;
         }
-        float part = 0.0f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          v[e] = e8[kperm8(e)];
-          part += (float)e8[e];
+          v[e] = e8[kperm8(e)] * qsgn;
+          gsum[(32 * s) / G] += (float)v[e];
         }
-        gs[(32 * s) / G] += part;
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = (_Float16)0.0f;
@@ -146,300 +170,347 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(
     }
     // complete the group sums over the 4 lanes of this row
 #pragma unroll
-    for (int g = 0; g < ng; ++g) {
-      gs[g] += __shfl_xor(gs[g], 16);
-      gs[g] += __shfl_xor(gs[g], 32);
+    for (int g = 0; g < NG; ++g) {
+      gsum[g] += __shfl_xor(gsum[g], 16);
+      gsum[g] += __shfl_xor(gsum[g], 32);
     }
-    h8 b;
+    h8 bq;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) b[e] = (_Float16)0.0f;
+    for (int e = 0; e < 8; ++e) bq[e] = (_Float16)0.0f;
 #pragma unroll
-    for (int g = 0; g < ng; ++g) {
+    for (int g = 0; g < NG; ++g) {
       if ((g >> 2) == q4) {
-        const _Float16 hi = (_Float16)gs[g];
-        const _Float16 lo = (_Float16)(gs[g] - (float)hi);
-        b[2 * (g & 3)] = hi;
-        b[2 * (g & 3) + 1] = lo;
+        const _Float16 hi = (_Float16)gsum[g];
+        bq[2 * (g & 3)] = hi;
+        bq[2 * (g & 3) + 1] = (_Float16)(gsum[g] - (float)hi);
       }
     }
-    qsum_b[n] = b;
+    qsum_b[n] = bq;
   }
 
-  f32x4 acc_o[DT][2];
+  f32x4 acc_o[DT][NR];
+  float m_run[NR], l_run[NR];
 #pragma unroll
-  for (int t = 0; t < DT; ++t)
+  for (int n = 0; n < NR; ++n) {
+    m_run[n] = kMinit;
+    l_run[n] = 0.0f;
 #pragma unroll
-    for (int n = 0; n < 2; ++n) acc_o[t][n] = f32x4{0, 0, 0, 0};
-  float m_row[2] = {-INFINITY, -INFINITY}, l_row[2] = {0.0f, 0.0f};
-  float bsum[ng][2];
-#pragma unroll
-  for (int g = 0; g < ng; ++g) bsum[g][0] = bsum[g][1] = 0.0f;
+    for (int t = 0; t < DT; ++t) acc_o[t][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
 
-  const int last_i = min(T - 1, (r0 + kRows - 1) / gq);
-  const int n_pre_tiles = (prefix_len + kKeys - 1) / kKeys;
-  const int n_chunk_tiles = (last_i + 1 + kKeys - 1) / kKeys;
-  const size_t head_codes = (size_t)P * (D / 2);
-  const size_t page_codes = (size_t)Hkv * head_codes;
-  const uint32_t kUnitMeta = 0x00003C00u;  // scale 1.0, bias 0
+  const int i_min = r0 / gq;
+  const int i_max = min(T - 1, (r0 + kRows - 1) / gq);
+  const int n_pre = (prefix_len + kKeys - 1) / kKeys;
+  const int n_chk = i_max / kKeys + 1;
+  const int n_tiles = n_pre + n_chk;
 
-  for (int tile = 0; tile < n_pre_tiles + n_chunk_tiles; ++tile) {
-    const bool is_pre = tile < n_pre_tiles;
-    const int key0 = is_pre ? tile * kKeys : (tile - n_pre_tiles) * kKeys;
-    const int key_lim = is_pre ? prefix_len : T;
-
-    // ---- stage K codes (or chunk values) [key][dim, unpack order]
-    for (int task = tid; task < kKeys * (D / 32); task += kThreads) {
-      const int key = task / (D / 32), c = task % (D / 32);
-      const int kk = key0 + key;
-      h2 x[16];
+  // ---- prefix tiles: codes and (scale, bias) words of tile j, one 16-byte
+  // code chunk (and its one or two meta words) per thread and round.  K
+  // chunk c: key c / QPK, dims 32 (c % QPK) ..; V chunk (after the K ones):
+  // key pair p = cv % 32, dims 16 (cv / 32) .. (pairs vary fastest across
+  // lanes, so the transposed LDS stores spread over the banks).
+  uint4 pc[NCH];
+  uint32_t pm[NCH][2];
+  auto tile_page = [&](int j) { return block_table[(j * kKeys) / P]; };
+  auto prefetch = [&](int j, int page) {
+    if ((unsigned)page >= (unsigned)NP) return;  // the tile is skipped
+    const int slot0 = (j * kKeys) % P;
+    const size_t run = (size_t)page * Hkv + kv;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) x[e] = h2{(_Float16)0.0f, (_Float16)0.0f};
-      if (kk < key_lim) {
-        if (is_pre) {
-          const int page = block_table[kk / P];
-          if ((unsigned)page < (unsigned)NP) {
-            const uint4 u = *reinterpret_cast<const uint4*>(
-                k_codes + page * page_codes + kv * head_codes + (size_t)(kk % P) * (D / 2) +
-                16 * c);
-            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    for (int k = 0; k < NCH; ++k) {
+      const int c = tid + k * kThreads;
+      if (c < KCH) {
+        const int key = c / QPK, qd = c % QPK;
+        pc[k] = *reinterpret_cast<const uint4*>(k_codes + run * head_codes +
+                                                (size_t)(slot0 + key) * (D / 2) + 16 * qd);
+        pm[k][0] = k_meta[(run * P + slot0 + key) * NG + (32 * qd) / G];
+      } else if (c < KCH + VCH) {
+        const int cv = c - KCH, pair = cv % (kKeys / 2), u16 = cv / (kKeys / 2);
+        pc[k] = *reinterpret_cast<const uint4*>(v_codes + run * head_codes +
+                                                (size_t)(slot0 / 2 + pair) * D + 16 * u16);
+        const size_t mrow = (run * P + slot0 + 2 * pair) * NG + (16 * u16) / G;
+        pm[k][0] = v_meta[mrow];
+        pm[k][1] = v_meta[mrow + NG];
+      }
+    }
+  };
+  // reconstruct the prefetched tile j into buffer b (keys past the prefix:
+  // scale and bias 0, so they are exact zeros)
+  auto dequant = [&](int j, int page, int b) {
+    if ((unsigned)page >= (unsigned)NP) return;
+    const int key0 = j * kKeys;
 #pragma unroll
-            for (int m = 0; m < 4; ++m) unpack8(w[m], &x[4 * m]);
-          }
-        } else {
-          const uint4* src =
-              reinterpret_cast<const uint4*>(k_chunk + ((size_t)kk * Hkv + kv) * D + 32 * c);
+    for (int k = 0; k < NCH; ++k) {
+      const int c = tid + k * kThreads;
+      const uint32_t w[4] = {pc[k].x, pc[k].y, pc[k].z, pc[k].w};
+      if (c < KCH) {
+        const int key = c / QPK, qd = c % QPK;
+        const bool on = key0 + key < prefix_len;
 #pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const uint4 u = src[m];  // dims 8m..8m+7 as pairs (0,1) (2,3) (4,5) (6,7)
-            const h2 a = as_h2(u.x), b = as_h2(u.y), cc = as_h2(u.z), d = as_h2(u.w);
-            x[4 * m + 0] = h2{a.x, cc.x};   // (d0, d4)
-            x[4 * m + 1] = h2{a.y, cc.y};   // (d1, d5)
-            x[4 * m + 2] = h2{b.x, d.x};    // (d2, d6)
-            x[4 * m + 3] = h2{b.y, d.y};    // (d3, d7)
+        for (int m = 0; m < 4; ++m) {
+          uint4 o;
+          o.x = as_u32(code2(w[m]));
+          o.y = as_u32(code2(w[m] >> 4));
+          o.z = as_u32(code2(w[m] >> 8));
+          o.w = as_u32(code2(w[m] >> 12));
+          *reinterpret_cast<uint4*>(&sK[b][key][32 * qd + 8 * m]) = o;
+        }
+        if ((32 * qd) % G == 0) sKm[b][(32 * qd) / G][key] = on ? pm[k][0] : 0u;
+      } else if (c < KCH + VCH) {
+        const int cv = c - KCH, pair = cv % (kKeys / 2), u16 = cv / (kKeys / 2);
+        const int kk = key0 + 2 * pair;
+        const uint32_t ma = (kk < prefix_len) ? pm[k][0] : 0u;
+        const uint32_t mb = (kk + 1 < prefix_len) ? pm[k][1] : 0u;
+        const h2 s2 = as_h2(__builtin_amdgcn_perm(mb, ma, 0x05040100u));
+        const h2 b2 = as_h2(__builtin_amdgcn_perm(mb, ma, 0x07060302u));
+        const int col = vperm(2 * pair);
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const int d0 = 16 * u16 + 4 * m;
+          *reinterpret_cast<uint32_t*>(&sV[b][d0 + 0][col]) = as_u32(deq2(w[m], s2, b2));
+          *reinterpret_cast<uint32_t*>(&sV[b][d0 + 1][col]) = as_u32(deq2(w[m] >> 4, s2, b2));
+          *reinterpret_cast<uint32_t*>(&sV[b][d0 + 2][col]) = as_u32(deq2(w[m] >> 8, s2, b2));
+          *reinterpret_cast<uint32_t*>(&sV[b][d0 + 3][col]) = as_u32(deq2(w[m] >> 12, s2, b2));
+        }
+      }
+    }
+  };
+  // the chunk's own fp16 rows j*64 .. into buffer b (rows past T: zeros)
+  auto stage_chunk = [&](int j, int b) {
+    const int key0 = j * kKeys;
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const int c = tid + k * kThreads;
+      if (c < KCH) {
+        const int key = c / QPK, qd = c % QPK;
+        const int kk = key0 + key;
+        const uint4* src = reinterpret_cast<const uint4*>(k_chunk + ((size_t)kk * Hkv + kv) * D + 32 * qd);
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const uint4 u = (kk < T) ? src[m] : make_uint4(0, 0, 0, 0);
+          // dims (0,1) (2,3) (4,5) (6,7) -> storage order (0,4) (1,5) (2,6) (3,7)
+          uint4 o;
+          o.x = __builtin_amdgcn_perm(u.z, u.x, 0x05040100u);
+          o.y = __builtin_amdgcn_perm(u.z, u.x, 0x07060302u);
+          o.z = __builtin_amdgcn_perm(u.w, u.y, 0x05040100u);
+          o.w = __builtin_amdgcn_perm(u.w, u.y, 0x07060302u);
+          *reinterpret_cast<uint4*>(&sK[b][key][32 * qd + 8 * m]) = o;
+        }
+        if ((32 * qd) % G == 0) sKm[b][(32 * qd) / G][key] = 0x00003C00u;  // scale 1, bias 0
+      } else if (c < KCH + VCH) {
+        const int cv = c - KCH, pair = cv % (kKeys / 2), u16 = cv / (kKeys / 2);
+        const int kk = key0 + 2 * pair;
+        const uint4* sa = reinterpret_cast<const uint4*>(v_chunk + ((size_t)kk * Hkv + kv) * D + 16 * u16);
+        const uint4* sb = reinterpret_cast<const uint4*>(v_chunk + ((size_t)(kk + 1) * Hkv + kv) * D + 16 * u16);
+        const int col = vperm(2 * pair);
+#pragma unroll
+        for (int hv = 0; hv < 2; ++hv) {
+          const uint4 ua = (kk < T) ? sa[hv] : make_uint4(0, 0, 0, 0);
+          const uint4 ub = (kk + 1 < T) ? sb[hv] : make_uint4(0, 0, 0, 0);
+          const uint32_t wa[4] = {ua.x, ua.y, ua.z, ua.w};
+          const uint32_t wb[4] = {ub.x, ub.y, ub.z, ub.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int d0 = 16 * u16 + 8 * hv + 2 * e;
+            *reinterpret_cast<uint32_t*>(&sV[b][d0][col]) =
+                __builtin_amdgcn_perm(wb[e], wa[e], 0x05040100u);
+            *reinterpret_cast<uint32_t*>(&sV[b][d0 + 1][col]) =
+                __builtin_amdgcn_perm(wb[e], wa[e], 0x07060302u);
           }
         }
       }
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        uint4 v;
-        v.x = as_u32(x[4 * m]);
-        v.y = as_u32(x[4 * m + 1]);
-        v.z = as_u32(x[4 * m + 2]);
-        v.w = as_u32(x[4 * m + 3]);
-        *reinterpret_cast<uint4*>(&sK[key][32 * c + 8 * m]) = v;
-      }
     }
-    // ---- stage V codes (or chunk values) transposed [dim][key, permuted]
-    for (int task = tid; task < (kKeys / 2) * (D / 16); task += kThreads) {
-      const int pair = task / (D / 16), c16 = task % (D / 16);
-      const int ka = key0 + 2 * pair;
-      const bool oka = ka < key_lim, okb = ka + 1 < key_lim;
-      h2 x[16];  // x[e] = (key 2p, key 2p+1) for dim 16*c16 + e
-#pragma unroll
-      for (int e = 0; e < 16; ++e) x[e] = h2{(_Float16)0.0f, (_Float16)0.0f};
-      if (oka) {
-        if (is_pre) {
-          const int page = block_table[ka / P];
-          if ((unsigned)page < (unsigned)NP) {
-            const uint4 u = *reinterpret_cast<const uint4*>(
-                v_codes + page * page_codes + kv * head_codes + (size_t)((ka % P) >> 1) * D +
-                16 * c16);
-            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-            for (int uu = 0; uu < 4; ++uu) unpack8(w[uu], &x[4 * uu]);  // dims 4uu+0..3
-            if (!okb) {  // the odd slot is past the prefix: unwritten
-#pragma unroll
-              for (int e = 0; e < 16; ++e) x[e].y = (_Float16)0.0f;
-            }
-          }
-        } else {
-          const uint4* sa =
-              reinterpret_cast<const uint4*>(v_chunk + ((size_t)ka * Hkv + kv) * D + 16 * c16);
-          const uint4* sb = reinterpret_cast<const uint4*>(
-              v_chunk + ((size_t)(ka + 1) * Hkv + kv) * D + 16 * c16);
-#pragma unroll
-          for (int v4 = 0; v4 < 2; ++v4) {
-            const uint4 ua = sa[v4];
-            const uint4 ub = okb ? sb[v4] : make_uint4(0, 0, 0, 0);
-            const uint32_t wa[4] = {ua.x, ua.y, ua.z, ua.w};
-            const uint32_t wb[4] = {ub.x, ub.y, ub.z, ub.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              x[8 * v4 + 2 * e] = h2{as_h2(wa[e]).x, as_h2(wb[e]).x};
-              x[8 * v4 + 2 * e + 1] = h2{as_h2(wa[e]).y, as_h2(wb[e]).y};
-            }
-          }
-        }
-      }
-      const int col = vperm(2 * pair);  // keys 2p and 2p+1 are adjacent
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        *reinterpret_cast<uint32_t*>(&sV[16 * c16 + e][col]) = as_u32(x[e]);
-    }
-    // ---- stage (scale, bias) per key and group; 0 for keys outside the range
-    for (int task = tid; task < kKeys * ng; task += kThreads) {
-      const int key = task % kKeys, g = task / kKeys;
-      const int kk = key0 + key;
-      uint32_t km = 0u, vm = 0u;
-      if (kk < key_lim) {
-        if (is_pre) {
-          const int page = block_table[kk / P];
-          if ((unsigned)page < (unsigned)NP) {
-            const size_t idx = (((size_t)page * Hkv + kv) * P + kk % P) * ng + g;
-            km = k_meta[idx];
-            vm = v_meta[idx];
-          }
-        } else {
-          km = vm = kUnitMeta;
-        }
-      }
-      sKm[g][key] = km;
-      sVm[g][key] = vm;
-    }
-    __syncthreads();
+  };
 
-    // ---- S^T = sum_g s_g (C_g Q_g^T) + bias term; 4 key tiles x 2 row tiles
-    f32x4 sacc[4][2];
+  // ---- one tile from buffer b: scores, online softmax, value products
+  auto compute = [&](int b, int key0, int key_lim, bool chunk_tile) {
+    // bias part first: key 16 mt + l16, slots (2g, 2g+1) = (b_g, b_g) on
+    // lanes q4 == g / 4; it seeds the folded scores
+    f32x4 sacc[4][NR];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
-      // bias operand: key 16mt + l16, slots (2g, 2g+1) = (b_g, b_g) on lanes q4 == g/4
       h8 kb;
 #pragma unroll
       for (int e = 0; e < 8; ++e) kb[e] = (_Float16)0.0f;
 #pragma unroll
-      for (int g = 0; g < ng; ++g) {
+      for (int g = 0; g < NG; ++g) {
         if ((g >> 2) == q4) {
-          const _Float16 bb = as_h2(sKm[g][16 * mt + l16]).y;
+          const _Float16 bb = as_h2(sKm[b][g][16 * mt + l16]).y;
           kb[2 * (g & 3)] = bb;
           kb[2 * (g & 3) + 1] = bb;
         }
       }
 #pragma unroll
-      for (int n = 0; n < 2; ++n)
-        sacc[mt][n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kb, qsum_b[n], f32x4{0, 0, 0, 0}, 0, 0, 0);
+      for (int n = 0; n < NR; ++n) sacc[mt][n] = mfma(kb, qsum_b[n], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+    }
+    // code products per scale group, scaled in fp32 (two 32-key halves in
+    // turn, to bound the live accumulators)
 #pragma unroll
-      for (int g = 0; g < ng; ++g) {
-        f32x4 acc[2] = {f32x4{0, 0, 0, 0}, f32x4{0, 0, 0, 0}};
+    for (int mh = 0; mh < 2; ++mh) {
 #pragma unroll
-        for (int ss = 0; ss < steps_per_group; ++ss) {
-          const int s = g * steps_per_group + ss;
-          const h8 a = *reinterpret_cast<const h8*>(&sK[16 * mt + l16][32 * s + 8 * q4]);
+      for (int g = 0; g < NG; ++g) {
+        f32x4 acc[2][NR];
 #pragma unroll
-          for (int n = 0; n < 2; ++n)
-            acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, qb[n][s], acc[n], 0, 0, 0);
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+          for (int n = 0; n < NR; ++n) acc[x][n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ss = 0; ss < G / 32; ++ss) {
+          const int s = g * (G / 32) + ss;
+#pragma unroll
+          for (int x = 0; x < 2; ++x) {
+            const h8 a = *reinterpret_cast<const h8*>(&sK[b][16 * (2 * mh + x) + l16][32 * s + 8 * q4]);
+#pragma unroll
+            for (int n = 0; n < NR; ++n) acc[x][n] = mfma(a, qb[n][s], acc[x][n]);
+          }
         }
-        const uint4 mq = *reinterpret_cast<const uint4*>(&sKm[g][16 * mt + 4 * q4]);
-        const float sc[4] = {lo_f(mq.x), lo_f(mq.y), lo_f(mq.z), lo_f(mq.w)};
 #pragma unroll
-        for (int n = 0; n < 2; ++n)
+        for (int x = 0; x < 2; ++x) {
+          const int mt = 2 * mh + x;
+          const uint4 mq = *reinterpret_cast<const uint4*>(&sKm[b][g][16 * mt + 4 * q4]);
+          const float sc[4] = {(float)as_h2(mq.x).x, (float)as_h2(mq.y).x, (float)as_h2(mq.z).x,
+                               (float)as_h2(mq.w).x};
 #pragma unroll
-          for (int r = 0; r < 4; ++r) sacc[mt][n][r] = fmaf(sc[r], acc[n][r], sacc[mt][n][r]);
+          for (int n = 0; n < NR; ++n)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sacc[mt][n][r] = fmaf(sc[r], acc[x][n][r], sacc[mt][n][r]);
+        }
       }
     }
-
-    // ---- mask, online softmax per row (row = lane's l16 within tile n)
-    _Float16 ph[4][2][4];  // p rounded to fp16, the values the products use
-#pragma unroll
-    for (int n = 0; n < 2; ++n) {
-      const int ip = row_pos[n];
-      float mx = -INFINITY;
+    // keys past the limit, and (chunk tiles) keys after the row's position
+    const bool need_mask = key0 + kKeys > key_lim || (chunk_tile && key0 + kKeys - 1 > i_min);
+    if (need_mask) {
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int kk = key0 + 16 * mt + 4 * q4 + r;
-          bool valid = kk < key_lim && ip >= 0;
-          if (!is_pre) valid = valid && kk <= ip;
-          const float sv = valid ? sacc[mt][n][r] * scale_log2 : -INFINITY;
-          sacc[mt][n][r] = sv;
-          mx = fmaxf(mx, sv);
-        }
+        for (int n = 0; n < NR; ++n)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int kk = key0 + 16 * mt + 4 * q4 + r;
+            const bool ok = kk < key_lim && (!chunk_tile || kk <= row_i[n]);
+            sacc[mt][n][r] = ok ? sacc[mt][n][r] : -INFINITY;
+          }
+    }
+    float tmax[NR];
+    bool up = false;
+#pragma unroll
+    for (int n = 0; n < NR; ++n) {
+      float mx = fmaxf(fmaxf(sacc[0][n][0], sacc[0][n][1]), fmaxf(sacc[0][n][2], sacc[0][n][3]));
+#pragma unroll
+      for (int mt = 1; mt < 4; ++mt)
+        mx = fmaxf(mx, fmaxf(fmaxf(sacc[mt][n][0], sacc[mt][n][1]),
+                             fmaxf(sacc[mt][n][2], sacc[mt][n][3])));
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_row[n], mx);
-      const float m_use = (m_new == -INFINITY) ? 0.0f : m_new;
-      const float alpha = exp2f(m_row[n] - m_use);
-      m_row[n] = m_new;
-      float ls = 0.0f;
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const _Float16 p = (_Float16)exp2f(sacc[mt][n][r] - m_use);
-          ph[mt][n][r] = p;
-          ls += (float)p;
-        }
-      ls += __shfl_xor(ls, 16);
-      ls += __shfl_xor(ls, 32);
-      l_row[n] = l_row[n] * alpha + ls;
-#pragma unroll
-      for (int t = 0; t < DT; ++t) acc_o[t][n] *= alpha;
-#pragma unroll
-      for (int g = 0; g < ng; ++g) bsum[g][n] *= alpha;
+      tmax[n] = mx * cabs;
+      up = up || tmax[n] > m_run[n] + kTau;
     }
+    if (__builtin_amdgcn_ballot_w64(up) != 0) {
+#pragma unroll
+      for (int n = 0; n < NR; ++n) {
+        if (tmax[n] > m_run[n] + kTau) {
+          const float alpha = __builtin_amdgcn_exp2f(m_run[n] - tmax[n]);
+          m_run[n] = tmax[n];
+          l_run[n] *= alpha;
+#pragma unroll
+          for (int t = 0; t < DT; ++t) acc_o[t][n] *= alpha;
+        }
+      }
+    }
+    // p = 2^(s |scale| - m) as fp16; P^T operand of 32-key step k: the
+    // lane's keys 4 q4 .. of 16-key tiles 2k and 2k + 1
+    h8 pb[NR][2];
+    const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+    for (int n = 0; n < NR; ++n) {
+      const float mneg = -m_run[n];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[mt][n][0], cabs, mneg));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[mt][n][1], cabs, mneg));
+        const float p2 = __builtin_amdgcn_exp2f(fmaf(sacc[mt][n][2], cabs, mneg));
+        const float p3 = __builtin_amdgcn_exp2f(fmaf(sacc[mt][n][3], cabs, mneg));
+        const h2 a = {(_Float16)p0, (_Float16)p1};
+        const h2 c = {(_Float16)p2, (_Float16)p3};
+        l_run[n] = __builtin_amdgcn_fdot2(a, ones, l_run[n], false);
+        l_run[n] = __builtin_amdgcn_fdot2(c, ones, l_run[n], false);
+        pb[n][mt >> 1][4 * (mt & 1) + 0] = a.x;
+        pb[n][mt >> 1][4 * (mt & 1) + 1] = a.y;
+        pb[n][mt >> 1][4 * (mt & 1) + 2] = c.x;
+        pb[n][mt >> 1][4 * (mt & 1) + 3] = c.y;
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const h8 a = *reinterpret_cast<const h8*>(&sV[b][16 * t + l16][32 * k + 8 * q4]);
+#pragma unroll
+        for (int n = 0; n < NR; ++n) acc_o[t][n] = mfma(a, pb[n][k], acc_o[t][n]);
+      }
+  };
 
-    // ---- bias sums and scaled P' operands per group; O^T += V^T P'^T
-#pragma unroll
-    for (int g = 0; g < ng; ++g) {
-      uint4 vm4[4];
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-        vm4[mt] = *reinterpret_cast<const uint4*>(&sVm[g][16 * mt + 4 * q4]);
-      h8 pb[2][2];  // [n][s]
-#pragma unroll
-      for (int n = 0; n < 2; ++n) {
-        float bs = 0.0f;
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-          const uint32_t mw[4] = {vm4[mt].x, vm4[mt].y, vm4[mt].z, vm4[mt].w};
-#pragma unroll
-          for (int r = 0; r < 4; ++r) bs = fmaf((float)ph[mt][n][r], hi_f(mw[r]), bs);
-          // keys of mt occupy slots (mt&1)*4 .. +3 of step mt>>1
-          const h2 s01 = as_h2(__builtin_amdgcn_perm(mw[1], mw[0], 0x05040100u));
-          const h2 s23 = as_h2(__builtin_amdgcn_perm(mw[3], mw[2], 0x05040100u));
-          const h2 p01 = h2{ph[mt][n][0], ph[mt][n][1]} * s01;
-          const h2 p23 = h2{ph[mt][n][2], ph[mt][n][3]} * s23;
-          pb[n][mt >> 1][4 * (mt & 1) + 0] = p01.x;
-          pb[n][mt >> 1][4 * (mt & 1) + 1] = p01.y;
-          pb[n][mt >> 1][4 * (mt & 1) + 2] = p23.x;
-          pb[n][mt >> 1][4 * (mt & 1) + 3] = p23.y;
-        }
-        bs += __shfl_xor(bs, 16);
-        bs += __shfl_xor(bs, 32);
-        bsum[g][n] += bs;
-      }
-      // dim tiles of group g: 16t .. 16t+15 within [g*G, (g+1)*G)
-#pragma unroll
-      for (int t = 0; t < DT; ++t) {
-        if ((16 * t) / G != g) continue;
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const h8 a = *reinterpret_cast<const h8*>(&sV[16 * t + l16][32 * s + 8 * q4]);
-#pragma unroll
-          for (int n = 0; n < 2; ++n)
-            acc_o[t][n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, pb[n][s], acc_o[t][n], 0, 0, 0);
-        }
+  // ---- tiles 0 .. n_pre - 1 (prefix), then the chunk's; double-buffered:
+  // tile j + 1 is reconstructed and tile j + 2's codes are fetched while
+  // tile j is computed; one barrier per tile
+  int page_pf = -1;     // page of the tile in the prefetch registers
+  int page_buf[2] = {0, 0};
+  if (n_pre > 0) {
+    page_pf = tile_page(0);
+    prefetch(0, page_pf);
+    dequant(0, page_pf, 0);
+    page_buf[0] = page_pf;
+    if (n_pre > 1) {
+      page_pf = tile_page(1);
+      prefetch(1, page_pf);
+    }
+  } else {
+    stage_chunk(0, 0);
+  }
+  __syncthreads();
+  for (int j = 0; j < n_tiles; ++j) {
+    const int b = j & 1;
+    if (j + 1 < n_tiles) {
+      if (j + 1 < n_pre) {
+        dequant(j + 1, page_pf, b ^ 1);
+        page_buf[b ^ 1] = page_pf;
+      } else {
+        stage_chunk(j + 1 - n_pre, b ^ 1);
+        page_buf[b ^ 1] = 0;
       }
     }
+    if (j + 2 < n_pre) {
+      page_pf = tile_page(j + 2);
+      prefetch(j + 2, page_pf);
+    }
+    const bool chunk_tile = j >= n_pre;
+    if (chunk_tile)
+      compute(b, (j - n_pre) * kKeys, T, true);
+    else if ((unsigned)page_buf[b] < (unsigned)NP)  // a tile on an invalid page is skipped
+      compute(b, j * kKeys, prefix_len, false);
     __syncthreads();
   }
 
-  // ---- O = (acc + bias sum of the dim's group) / l, as fp16
+  // ---- O = acc / l, as fp16
 #pragma unroll
-  for (int n = 0; n < 2; ++n) {
-    const int r = r0 + 32 * wave + 16 * n + l16;
+  for (int n = 0; n < NR; ++n) {
+    const int r = r0 + kRowsPerWave * wave + 16 * n + l16;
     const int i = r / gq, hh = r % gq;
+    // the row's sum: the four lanes of a query column hold disjoint keys
+    float l = l_run[n] + __shfl_xor(l_run[n], 16);
+    l += __shfl_xor(l, 32);
     if (i >= T) continue;
-    const float inv = (l_row[n] > 0.0f) ? 1.0f / l_row[n] : 0.0f;
+    const float inv = (l > 0.0f) ? 1.0f / l : 0.0f;
     __half* dst = out + ((size_t)i * Hq + kv * gq + hh) * D;
 #pragma unroll
     for (int t = 0; t < DT; ++t) {
       const int d0 = 16 * t + 4 * q4;
-      const float bg = bsum[(16 * t) / G][n];
-      const __half2 a = __floats2half2_rn((acc_o[t][n][0] + bg) * inv, (acc_o[t][n][1] + bg) * inv);
-      const __half2 b = __floats2half2_rn((acc_o[t][n][2] + bg) * inv, (acc_o[t][n][3] + bg) * inv);
-      *reinterpret_cast<__half2*>(dst + d0) = a;
-      *reinterpret_cast<__half2*>(dst + d0 + 2) = b;
+      const __half2 a = __floats2half2_rn(acc_o[t][n][0] * inv, acc_o[t][n][1] * inv);
+      const __half2 c = __floats2half2_rn(acc_o[t][n][2] * inv, acc_o[t][n][3] * inv);
+      uint2 v;
+      v.x = __builtin_bit_cast(uint32_t, a);
+      v.y = __builtin_bit_cast(uint32_t, c);
+      *reinterpret_cast<uint2*>(dst + d0) = v;
     }
   }
 }
@@ -452,20 +523,22 @@ hipError_t launch_prefill(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, co
                           const void* k_chunk, const void* v_chunk, int32_t T, int32_t Hq,
                           const int32_t* block_table, int32_t max_pages, int32_t prefix_len,
                           float softmax_scale, void* out, hipStream_t stream) {
+  (void)max_pages;  // validated on the host: prefix_len <= max_pages * page_size
   const int gq = Hq / L.num_kv_heads;
   const int64_t rows = (int64_t)T * gq;
-  dim3 grid((uint32_t)((rows + kRows - 1) / kRows), L.num_kv_heads);
 #define JF_PREFILL_CASE(D_, G_)                                                                 \
   if (L.head_dim == D_ && L.group_size == G_) {                                                 \
-    hipLaunchKernelGGL((prefill_kernel<D_, G_>), grid, dim3(kThreads), 0, stream,               \
+    constexpr int kRowsB = 16 * row_tiles<D_>() * kWaves;                                      \
+    const int64_t n_rb = (rows + kRowsB - 1) / kRowsB;                                          \
+    dim3 grid((uint32_t)(n_rb * L.num_kv_heads));                                               \
+    hipLaunchKernelGGL((prefill_kernel<D_, G_>), grid, dim3(64 * kWaves), 0, stream,    \
                        static_cast<const uint8_t*>(pool.k_codes),                               \
                        static_cast<const uint32_t*>(pool.k_meta),                               \
                        static_cast<const uint8_t*>(pool.v_codes),                               \
                        static_cast<const uint32_t*>(pool.v_meta), static_cast<const __half*>(q),\
                        static_cast<const __half*>(k_chunk), static_cast<const __half*>(v_chunk),\
                        block_table, static_cast<__half*>(out), T, Hq, L.num_kv_heads,           \
-                       L.page_size, L.num_pages, max_pages, prefix_len,                          \
-                       softmax_scale * kLog2e);                                                 \
+                       L.page_size, L.num_pages, prefix_len, softmax_scale * kLog2e);           \
     return hipGetLastError();                                                                   \
   }
   JF_PREFILL_CASE(64, 32)

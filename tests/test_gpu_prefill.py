@@ -1,7 +1,9 @@
-"""GPU chunked prefill (bf16 matrix cores) against the CPU oracle.
+"""GPU chunked prefill (fp16 matrix cores) against the CPU oracle.
 
-Tolerance: |o_gpu - o_ref| <= 2e-3 + 2^-8 |o_ref| (bf16 operands carry 8
-significant bits; fp32 accumulation), relative L2 <= 4e-3.
+Tolerance: |o_gpu - o_ref| <= 2e-3 + 2^-8 |o_ref|, relative L2 <= 4e-3.  The
+operands that are rounded are p (fp16) and the reconstructed values
+(scale * code + bias, rounded once to fp16); key codes, scales and biases
+enter the scores exactly, with fp32 accumulation.
 """
 import numpy as np
 import pytest
