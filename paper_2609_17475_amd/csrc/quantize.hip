@@ -21,6 +21,34 @@
 namespace {
 
 using jfkv::quantize8;
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x2 __attribute__((ext_vector_type(2)));
+// Element e of a lane's row slice (two fp16 values per word), as binary32.
+__device__ __forceinline__ float elem(const uint32_t* hw, int e) {
+  const _Float16 h = __builtin_bit_cast(_Float16, (unsigned short)(hw[e >> 1] >> (16 * (e & 1))));
+  return (float)h;
+}
+// Row staging of the tiled kernel: a 1 KiB load block plus 16 bytes, so the
+// lanes reading 128-byte row slices spread over the LDS banks.
+constexpr int kStagePitch = 1040;
+// LDS-DMA: this lane's 16 bytes at src land at LDS address lds + 16 * lane
+// (streaming: each byte is read once).
+__device__ __forceinline__ void dma_row_chunk(const uint8_t* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt"
+               :
+               : "s"(lds), "v"(src)
+               : "memory", "m0");
+}
+// a where mask is set, else b (bitwise; keeps register arrays out of memory).
+__device__ __forceinline__ uint32_t pick(uint32_t mask, uint32_t a, uint32_t b) {
+  return (a & mask) | (b & ~mask);
+}
+// floor(x + 0.5) as an integer (v_cvt_rpi_i32_f32).
+__device__ __forceinline__ int cvt_rpi(float x) {
+  int r;
+  asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
 __device__ __forceinline__ uint32_t order_key(uint32_t h) { return jfkv::q_order_key(h); }
 __device__ __forceinline__ uint32_t from_key(uint32_t k) { return jfkv::q_from_key(k); }
 __device__ __forceinline__ float h2f(uint32_t bits) { return jfkv::q_h2f(bits); }
@@ -126,11 +154,22 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
   const int64_t row = tile * PW + p;
   const bool in_range = row < total_tok;
 
-  uint4 x[8];
+  // The wave's rows reach LDS by LDS-DMA loads whose 64 lanes cover whole
+  // rows (RPI rows of D fp16 per 1 KiB load, every cache line used by one
+  // load); each lane then reads its 128-byte slice from LDS.  Rows past the
+  // end re-read the last row (their results are not stored).
+  constexpr int RPI = 512 / D;   // rows per load
+  constexpr int CPR = D / 8;     // 16-byte chunks per row
+  __shared__ __attribute__((aligned(16))) uint8_t stage[4][8][kStagePitch];
+  const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave in block (scalar)
+  const uint32_t lds_w = (uint32_t)(uintptr_t)&stage[wib][0][0];
   {
-    const uint4* src = (kind ? v_new : k_new) + (row * Hkv + kv) * (D / 8) + part * 8;
+    const uint8_t* gsrc = reinterpret_cast<const uint8_t*>(kind ? v_new : k_new);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = in_range ? src[i] : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < 8; ++i) {
+      const int64_t r = min(tile * PW + i * RPI + lane / CPR, (int64_t)total_tok - 1);
+      dma_row_chunk(gsrc + ((r * Hkv + kv) * D) * 2 + 16 * (lane % CPR), lds_w + i * kStagePitch);
+    }
   }
   // destination of the row (its loads overlap the row loads above): request b (largest with cu_tok[b] <= row), its
   // logical position, page and slot
@@ -154,6 +193,15 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
   }
   const bool valid = page >= 0;
 
+  uint4 x[8];
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the rows are in LDS
+  {
+    const uint4* my = reinterpret_cast<const uint4*>(
+        &stage[wib][p / RPI][(p % RPI) * 2 * D + 128 * part]);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = my[i];
+  }
+
   uint32_t hw[32];  // the lane's 64 fp16 values, two per word
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
@@ -163,18 +211,23 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
     hw[4 * i + 3] = x[i].w;
   }
 
-  // group minimum and maximum (integer total-order keys: exact, order-free)
+  // group minimum and maximum: integer total-order keys of both halves of a
+  // word at once (16-bit lanes: key = h ^ (sign ? 0xffff : 0x8000)), exact
+  // and order-free
   uint32_t kmin[NGL], kmax[NGL];
 #pragma unroll
   for (int gl = 0; gl < NGL; ++gl) {
-    kmin[gl] = 0xffffu;
-    kmax[gl] = 0u;
+    u16x2 lo2 = {0xffff, 0xffff}, hi2 = {0, 0};
 #pragma unroll
     for (int w = gl * EPG / 2; w < (gl + 1) * EPG / 2; ++w) {
-      const uint32_t k0 = order_key(hw[w] & 0xffffu), k1 = order_key(hw[w] >> 16);
-      kmin[gl] = min(kmin[gl], min(k0, k1));
-      kmax[gl] = max(kmax[gl], max(k0, k1));
+      const i16x2 sgn = __builtin_bit_cast(i16x2, hw[w]) >> (short)15;
+      const u16x2 key = __builtin_bit_cast(
+          u16x2, hw[w] ^ (__builtin_bit_cast(uint32_t, sgn) | 0x80008000u));
+      lo2 = __builtin_elementwise_min(lo2, key);
+      hi2 = __builtin_elementwise_max(hi2, key);
     }
+    kmin[gl] = min((uint32_t)lo2.x, (uint32_t)lo2.y);
+    kmax[gl] = max((uint32_t)hi2.x, (uint32_t)hi2.y);
   }
   if constexpr (G == 128) {  // the group spans this lane and lane ^ 1
     kmin[0] = min(kmin[0], (uint32_t)__shfl_xor((int)kmin[0], 1));
@@ -197,7 +250,9 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
     inv[gl] = (scale_bits == 0) ? 0.0f : __builtin_amdgcn_rcpf(sf[gl]);
   }
 
-  // codes: rint of the reciprocal quotient, checked against the margin
+  // codes: the reciprocal quotient rounded half up (v_cvt_rpi), which is
+  // rint whenever the quotient is not within kNear of a half-integer; the
+  // distance to the chosen code is tracked so those quotients can be redone
   uint32_t cw[8];  // nibble i of word m = code of element 8m + i
   float worst = 0.0f;
 #pragma unroll
@@ -206,44 +261,55 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int e = 8 * m + i, gl = e / EPG;
-      const float xe = h2f((hw[e >> 1] >> (16 * (e & 1))) & 0xffffu);
-      const float q0 = __fsub_rn(xe, bf[gl]) * inv[gl];
-      const float c = __builtin_rintf(q0);
-      worst = fmaxf(worst, fabsf(q0 - c));
-      word |= (uint32_t)fminf(fmaxf(c, 0.0f), 15.0f) << (4 * i);
+      const float q0 = __fsub_rn(elem(hw, e), bf[gl]) * inv[gl];
+      const int c = cvt_rpi(q0);
+      worst = fmaxf(worst, fabsf(q0 - (float)c));
+      word |= (uint32_t)min(max(c, 0), 15) << (4 * i);
     }
     cw[m] = word;
   }
-  if (__builtin_amdgcn_ballot_w64(worst > kNear) != 0 && worst > kNear) {
-    // some quotient lies near a rounding boundary: exact division throughout
+  if (__builtin_amdgcn_ballot_w64(worst > kNear) != 0) {
+    // some quotient lies near a rounding boundary: the exact IEEE division
+    // for those elements (rare: each element index is redone only if a lane
+    // of the wave needs it).  The values are passed through an empty asm so
+    // that the quotients are recomputed here, not kept live from above.
+    uint32_t hx[32];
+#pragma unroll
+    for (int w = 0; w < 32; ++w) {
+      hx[w] = hw[w];
+      asm volatile("" : "+v"(hx[w]));
+    }
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
-      uint32_t word = 0;
+      uint32_t word = cw[m];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int e = 8 * m + i, gl = e / EPG;
-        uint32_t code = 0;
-        if (sf[gl] != 0.0f) {
-          const float xe = h2f((hw[e >> 1] >> (16 * (e & 1))) & 0xffffu);
-          const float r = __fdiv_rn(__fsub_rn(xe, bf[gl]), sf[gl]);
-          code = (uint32_t)fminf(fmaxf(__builtin_rintf(r), 0.0f), 15.0f);
+        const float xe = elem(hx, e);
+        const float q0 = __fsub_rn(xe, bf[gl]) * inv[gl];
+        if (fabsf(q0 - (float)cvt_rpi(q0)) > kNear) {
+          uint32_t code = 0;
+          if (sf[gl] != 0.0f) {
+            const float r = __fdiv_rn(__fsub_rn(xe, bf[gl]), sf[gl]);
+            code = (uint32_t)fminf(fmaxf(__builtin_rintf(r), 0.0f), 15.0f);
+          }
+          word = (word & ~(0xfu << (4 * i))) | (code << (4 * i));
         }
-        word |= code << (4 * i);
       }
       cw[m] = word;
     }
   }
 
-
   // V position pairs: both rows of a pair present and neighbours in one page?
   const int32_t partner_page = __shfl_xor(page, LPR);
   const int32_t partner_slot = __shfl_xor(slot, LPR);
   const bool odd = slot & 1;
+  const uint32_t odd_mask = 0u - (uint32_t)odd;  // selects by mask: no indexed access to cw
   const bool paired = valid && partner_page == page && partner_slot == (slot ^ 1);
   uint32_t send[4], recv[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    send[i] = odd ? cw[i] : cw[4 + i];  // the half-words the partner stores
+    send[i] = pick(odd_mask, cw[i], cw[4 + i]);  // the half-words the partner stores
     recv[i] = (uint32_t)__shfl_xor((int)send[i], LPR);
   }
   if (!valid) return;
@@ -262,7 +328,7 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
       uint32_t wv[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const uint32_t mine = (odd ? cw[4 + i / 2] : cw[i / 2]) >> (16 * (i & 1)) & 0xffffu;
+        const uint32_t mine = pick(odd_mask, cw[4 + i / 2], cw[i / 2]) >> (16 * (i & 1)) & 0xffffu;
         const uint32_t other = recv[i / 2] >> (16 * (i & 1)) & 0xffffu;
         wv[i] = odd ? (other | (mine << 16)) : (mine | (other << 16));
       }
