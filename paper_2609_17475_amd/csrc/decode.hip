@@ -11,7 +11,8 @@
 // with a log-sum-exp combine, so the workspace is bounded by the split cap,
 // not by the context length.
 //
-// Data movement: a block of four waves owns one split; its waves take the
+// Data movement: a block of waves (eight at d <= 128) owns one split; its
+// waves take the
 // split's rows (a row = 32 positions of one page) in turn and stream each
 // row into a private LDS ring with global_load_lds (HBM -> LDS without
 // registers), all ring stages in flight while a row is computed.
@@ -60,16 +61,18 @@ constexpr int kMaxThreads = 512;    // a block: one split, one block per CU
 constexpr int kRowPos = 32;         // positions per row: two 16-position MFMA tiles
 constexpr int kHeadSlots = 4;       // query heads per block
 constexpr int kRingBudget = 162816; // LDS bytes of a block's rings (a CU's LDS less 1 KiB)
-// Waves per block: one per SIMD.  (Eight waves stream no faster, and the
-// second wave of a SIMD lags the first, which the block then waits for.)
+// Waves per block: two per SIMD where the LDS rings fit (d <= 128), so one
+// wave computes while the other waits on its page loads; the waves meet at a
+// barrier once per ring cycle, which keeps the two waves of a SIMD in step
+// (otherwise the older one runs ahead and the block waits for the other).
 #ifndef JF_DECODE_WAVES
-#define JF_DECODE_WAVES 4
+#define JF_DECODE_WAVES 8
 #endif
 #ifndef JF_DECODE_STAGES
-#define JF_DECODE_STAGES 4
+#define JF_DECODE_STAGES 3
 #endif
 template <int D>
-constexpr int waves_for() { return JF_DECODE_WAVES; }
+constexpr int waves_for() { return D <= 128 ? JF_DECODE_WAVES : 4; }
 constexpr int kMaxStages = JF_DECODE_STAGES;  // LDS ring depth per wave (at most)
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
@@ -365,7 +368,8 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
   }
 }
 
-// Decode kernel.  Block = 4 waves = one split of one (request, KV head, chunk
+// Decode kernel.  Block = 8 (d <= 128) or 4 waves = one split of one
+// (request, KV head, chunk
 // of up to 4 query heads).  Lane (m, q) = (lane % 16, lane / 16) feeds row m
 // and k-quarter q of the MFMA operands and receives column m, rows 4q..4q+3
 // of the 16x16 results.
@@ -885,17 +889,20 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     }
     t_row += kWaves * kRowPos;
   };
-  for (int r0 = 0; r0 < my_rows; r0 += kStages) {
+  // every wave runs the same number of ring cycles (block barrier per cycle)
+  const int max_rows = (split_rows + kWaves - 1) / kWaves;
+  for (int r0 = 0; r0 < max_rows; r0 += kStages) {
     static_for<kStages>([&](auto st_c) {
       if (r0 + decltype(st_c)::value < my_rows) row(st_c);
     });
+    __syncthreads();
   }
   wait_vm<0>();  // loads issued past the last row have landed (the ring is reused)
 
   // ---- merge.  Each wave writes its unnormalized output (code sums times
   // the code factor plus the bias sums), its maximum and its row sum into its
   // own ring, which is idle now; after one barrier the split's threads add
-  // the four waves' parts, rescaled to the split's maximum.
+  // the waves' parts, rescaled to the split's maximum.
   float* part = reinterpret_cast<float*>(ring);  // [kHeadSlots][D]
   float* part_m = part + kHeadSlots * D;          // [kHeadSlots]
   float* part_l = part_m + kHeadSlots;            // [kHeadSlots]
