@@ -77,20 +77,26 @@ def _cpu_model():
     return None
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "decode_kernel_decode_256k_traffic.md")
-DECODE_SOURCE = os.path.join(ROOT, "paper_2609_17475_amd", "csrc", "decode.hip")
+CSRC = os.path.join(ROOT, "paper_2609_17475_amd", "csrc")
+TRAFFIC_PROFILES = {  # kernel -> (counter profile, source it was taken from)
+    "decode": (os.path.join(ROOT, "profiles", "decode_kernel_decode_256k_traffic.md"), "decode.hip"),
+    "quantize": (os.path.join(ROOT, "profiles", "quantize_rows_kernel_quantize_bulk.md"),
+                 "quantize.hip"),
+}
 
 
-def measured_traffic():
-    """HBM bytes per decode call from the committed counter profile, or None
-    when the decode source has changed since the counters were taken."""
+def measured_traffic(kernel="decode"):
+    """HBM bytes per call from the committed counter profile (FETCH_SIZE and
+    WRITE_SIZE, calibrated), or None when the kernel's source has changed
+    since the counters were taken."""
     import hashlib
+    path, src = TRAFFIC_PROFILES[kernel]
     try:
-        text = open(TRAFFIC_PROFILE).read()
+        text = open(path).read()
     except OSError:
         return None
-    sha = hashlib.sha256(open(DECODE_SOURCE, "rb").read()).hexdigest()
-    m_sha = re.search(r"decode_source_sha256:\s*([0-9a-f]{64})", text)
+    sha = hashlib.sha256(open(os.path.join(CSRC, src), "rb").read()).hexdigest()
+    m_sha = re.search(kernel + r"_source_sha256:\s*([0-9a-f]{64})", text)
     m_b = re.search(r"traffic_bytes_per_call:\s*([0-9]+)", text)
     if not m_sha or not m_b or m_sha.group(1) != sha:
         return None
@@ -222,7 +228,7 @@ def bench_quantize_bulk(args):
                    "page_size": P, "group_size": G},
         "us_per_step": {"quantize": t_q, "wall": wall},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("quantize"),
                      "kernel": "quantize_rows_kernel", "algorithmic_bytes": nbytes},
         "cpu_baseline": None}), flush=True)
 
