@@ -49,6 +49,7 @@ namespace {
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kKeys = 64;          // keys per tile (a page holds whole tiles)
@@ -113,6 +114,10 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
 
   __shared__ __attribute__((aligned(16))) _Float16 sK[2][kKeys][KP];
   __shared__ __attribute__((aligned(16))) uint32_t sKm[2][NG][kKeys];  // K (scale, bias)
+  // the bias product's K operand per key: slots (2g, 2g+1) of lane group
+  // g / 4 hold (b_g, b_g) (groups 0..7; the other slots stay zero)
+  constexpr int NBQ = (NG + 3) / 4;
+  __shared__ __attribute__((aligned(16))) uint32_t sKb[2][kKeys][NBQ][4];
   __shared__ __attribute__((aligned(16))) _Float16 sV[2][D][VP];
 
   // KV head fastest: the blocks of one KV head land on one XCD (round-robin
@@ -255,7 +260,12 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
           o.w = as_u32(code2(w[m] >> 12));
           *reinterpret_cast<uint4*>(&sK[b][key][32 * qd + 8 * m]) = o;
         }
-        if ((32 * qd) % G == 0) sKm[b][(32 * qd) / G][key] = on ? pm[k][0] : 0u;
+        if ((32 * qd) % G == 0) {
+          const int g = (32 * qd) / G;
+          const uint32_t mw = on ? pm[k][0] : 0u;
+          sKm[b][g][key] = mw;
+          sKb[b][key][g >> 2][g & 3] = __builtin_amdgcn_perm(mw, mw, 0x03020302u);
+        }
       } else if (c < KCH + VCH) {
         const int cv = c - KCH, pair = cv % (kKeys / 2), u16 = cv / (kKeys / 2);
         const int kk = key0 + 2 * pair;
@@ -296,7 +306,11 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
           o.w = __builtin_amdgcn_perm(u.w, u.y, 0x07060302u);
           *reinterpret_cast<uint4*>(&sK[b][key][32 * qd + 8 * m]) = o;
         }
-        if ((32 * qd) % G == 0) sKm[b][(32 * qd) / G][key] = 0x00003C00u;  // scale 1, bias 0
+        if ((32 * qd) % G == 0) {
+          const int g = (32 * qd) / G;
+          sKm[b][g][key] = 0x00003C00u;  // scale 1, bias 0
+          sKb[b][key][g >> 2][g & 3] = 0u;
+        }
       } else if (c < KCH + VCH) {
         const int cv = c - KCH, pair = cv % (kKeys / 2), u16 = cv / (kKeys / 2);
         const int kk = key0 + 2 * pair;
@@ -329,17 +343,8 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     f32x4 sacc[4][NR];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
-      h8 kb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) kb[e] = (_Float16)0.0f;
-#pragma unroll
-      for (int g = 0; g < NG; ++g) {
-        if ((g >> 2) == q4) {
-          const _Float16 bb = as_h2(sKm[b][g][16 * mt + l16]).y;
-          kb[2 * (g & 3)] = bb;
-          kb[2 * (g & 3) + 1] = bb;
-        }
-      }
+      const h8 kb = (q4 < NBQ) ? *reinterpret_cast<const h8*>(&sKb[b][16 * mt + l16][q4 < NBQ ? q4 : 0][0])
+                               : h8{};
 #pragma unroll
       for (int n = 0; n < NR; ++n) sacc[mt][n] = mfma(kb, qsum_b[n], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
     }
@@ -420,6 +425,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     // p = 2^(s |scale| - m) as fp16; P^T operand of 32-key step k: the
     // lane's keys 4 q4 .. of 16-key tiles 2k and 2k + 1
     h8 pb[NR][2];
+    u32x4 pw[NR][2];  // the same, as fp16 pairs
     const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
 #pragma unroll
     for (int n = 0; n < NR; ++n) {
@@ -434,12 +440,14 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
         const h2 c = {(_Float16)p2, (_Float16)p3};
         l_run[n] = __builtin_amdgcn_fdot2(a, ones, l_run[n], false);
         l_run[n] = __builtin_amdgcn_fdot2(c, ones, l_run[n], false);
-        pb[n][mt >> 1][4 * (mt & 1) + 0] = a.x;
-        pb[n][mt >> 1][4 * (mt & 1) + 1] = a.y;
-        pb[n][mt >> 1][4 * (mt & 1) + 2] = c.x;
-        pb[n][mt >> 1][4 * (mt & 1) + 3] = c.y;
+        pw[n][mt >> 1][2 * (mt & 1) + 0] = as_u32(a);
+        pw[n][mt >> 1][2 * (mt & 1) + 1] = as_u32(c);
       }
     }
+#pragma unroll
+    for (int n = 0; n < NR; ++n)
+#pragma unroll
+      for (int k = 0; k < 2; ++k) pb[n][k] = __builtin_bit_cast(h8, pw[n][k]);
 #pragma unroll
     for (int t = 0; t < DT; ++t)
 #pragma unroll
@@ -449,6 +457,9 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
         for (int n = 0; n < NR; ++n) acc_o[t][n] = mfma(a, pb[n][k], acc_o[t][n]);
       }
   };
+
+  for (int i = tid; i < 2 * kKeys * NBQ * 4; i += kThreads) (&sKb[0][0][0][0])[i] = 0u;
+  __syncthreads();
 
   // ---- tiles 0 .. n_pre - 1 (prefix), then the chunk's; double-buffered:
   // tile j + 1 is reconstructed and tile j + 2's codes are fetched while
