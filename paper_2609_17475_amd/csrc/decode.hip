@@ -300,19 +300,23 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t records_rsrc(const float* base
 
 // Log-sum-exp combine of the split records of heads h0 .. h0+nh-1 (nh <= 4)
 // of request b: M = max m_s, w_s = l_s 2^(m_s - M), o = sum w_s o_s / sum w_s.
-// Wave w combines head w: lane (c, k) holds dims 4c..4c+3 and the splits
-// s = k, k + KP, ... (KP = 64 / (D/4)), fetched KCH at a time with coherent
-// loads and folded into a running maximum; the KP parts meet by shuffles.
-// Records: [max_splits][D + 4] fp32 per head (o/l in 0..D-1, m at D, l at
-// D+1).
-template <int D>
+// WPH waves per head: wave w combines dims [D/WPH (w % WPH), +D/WPH) of head
+// w / WPH.  Lane (c, k) holds 4 of those dims (chunk c) and the splits
+// s = k, k + KP, ... (KP = lanes per chunk), fetched KCH at a time with
+// coherent loads and folded into a running maximum; the KP parts meet by
+// shuffles.  Records: [max_splits][D + 4] fp32 per head (o/l in 0..D-1, m at
+// D, l at D+1).
+template <int D, int WPH>
 __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int h0, int nh,
                                int max_splits, int S) {
-  constexpr int CPL = D / 4;      // float4 chunks of a record's o
+  constexpr int DW = D / WPH;     // dims per wave
+  constexpr int CPL = DW / 4;     // float4 chunks per wave
   constexpr int KP = 64 / CPL;    // lanes per chunk (split parts)
-  constexpr int KCH = 16;         // splits per lane per round
+  constexpr int KCH = (32 / KP) < 16 ? (32 / KP > 0 ? 32 / KP : 1) : 16;  // splits per lane per round
   static_assert(KP >= 1 && 64 % CPL == 0, "");
-  const int lane = threadIdx.x & 63, h = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // scalar: the records' resource too
+  const int h = w / WPH, d0 = DW * (w % WPH);
   if (h >= nh) return;
   const int c = lane % CPL, k = lane / CPL;
   const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (D + 4);
@@ -325,26 +329,30 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
       const int s = min(s0 + KP * i, S - 1);  // past the end: a valid record, weight 0
-      o[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (s * (D + 4) + 4 * c) * 4, 0, kCpolSc1);
+      o[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (s * (D + 4) + d0 + 4 * c) * 4, 0, kCpolSc1);
       ml[i] = __builtin_amdgcn_raw_buffer_load_b64(rs, (s * (D + 4) + D) * 4, 0, kCpolSc1);
     }
+    // (selects, not branches: the records' validity is per lane)
+    float mv[KCH];
     float mx = m_run;
 #pragma unroll
-    for (int i = 0; i < KCH; ++i)
-      if (s0 + KP * i < S && ml[i].y > 0.0f) mx = fmaxf(mx, ml[i].x);
+    for (int i = 0; i < KCH; ++i) {
+      const bool on = (s0 + KP * i < S) & (ml[i].y > 0.0f);
+      mv[i] = on ? ml[i].x : -INFINITY;
+      mx = fmaxf(mx, mv[i]);
+    }
     const float f = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - mx);
     den *= f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) num[e] *= f;
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
-      const bool on = s0 + KP * i < S && ml[i].y > 0.0f;
-      const float w = on ? ml[i].y * __builtin_amdgcn_exp2f(ml[i].x - mx) : 0.0f;
-      den += w;
-      num[0] = fmaf(w, o[i].x, num[0]);
-      num[1] = fmaf(w, o[i].y, num[1]);
-      num[2] = fmaf(w, o[i].z, num[2]);
-      num[3] = fmaf(w, o[i].w, num[3]);
+      const float wt = (mv[i] == -INFINITY) ? 0.0f : ml[i].y * __builtin_amdgcn_exp2f(mv[i] - mx);
+      den += wt;
+      num[0] = fmaf(wt, o[i].x, num[0]);
+      num[1] = fmaf(wt, o[i].y, num[1]);
+      num[2] = fmaf(wt, o[i].z, num[2]);
+      num[3] = fmaf(wt, o[i].w, num[3]);
     }
     m_run = mx;
   }
@@ -362,7 +370,7 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
   }
   if (k == 0) {
     const float r = den > 0.0f ? 1.0f / den : 0.0f;
-    __half2* dst = reinterpret_cast<__half2*>(out + ((size_t)b * Hq + h0 + h) * D + 4 * c);
+    __half2* dst = reinterpret_cast<__half2*>(out + ((size_t)b * Hq + h0 + h) * D + d0 + 4 * c);
     dst[0] = __floats2half2_rn(num[0] * r, num[1] * r);
     dst[1] = __floats2half2_rn(num[2] * r, num[3] * r);
   }
@@ -416,6 +424,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   constexpr int kFit = (kRingBudget - 16) / (kWaves * kStageBytes);
   constexpr int kStages = kFit < kMaxStages ? kFit : kMaxStages;
   static_assert(kStages >= 2, "ring depth");
+  static_assert(kWaves % kHeadSlots == 0, "whole waves per head in the combine");
   constexpr bool kSwz = (D == 128);
   static_assert(DMAS_PER_ROW * (kStages - 1) < 64, "vmcnt range");
   static_assert(kHeadSlots * D + 2 * kHeadSlots <= kStages * kStageBytes / 4, "merge fits a ring");
@@ -984,7 +993,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   __syncthreads();
   if (s_ticket != (uint32_t)(S - 1)) return;
   if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  combine_splits<D>(ws, out, b, Hq, h0, nh, max_splits, S);
+  combine_splits<D, kWaves / kHeadSlots>(ws, out, b, Hq, h0, nh, max_splits, S);
 }
 
 // Compute units of the current device (queried once per device).
