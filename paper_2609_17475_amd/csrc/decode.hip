@@ -996,20 +996,6 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   combine_splits<D, kWaves / kHeadSlots>(ws, out, b, Hq, h0, nh, max_splits, S);
 }
 
-// Compute units of the current device (queried once per device).
-int num_cus() {
-  constexpr int kMaxDevices = 64;
-  static int cached[kMaxDevices] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
-  if (dev < kMaxDevices && cached[dev] > 0) return cached[dev];
-  int n = 0;
-  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-    n = 256;
-  if (dev < kMaxDevices) cached[dev] = n;
-  return n;
-}
-
 template <int D, int G, bool APPEND>
 hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
                     const void* v_new, const void* q,
@@ -1024,7 +1010,7 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
   // (they are on the device).
   const int64_t per_split = (int64_t)L.num_kv_heads * n_hchunks;
   const int split_cap =
-      (int)std::max<int64_t>(1, std::min<int64_t>(max_splits, (num_cus() + per_split - 1) / per_split));
+      (int)std::max<int64_t>(1, std::min<int64_t>(max_splits, (jfkv::num_cus() + per_split - 1) / per_split));
   dim3 grid(split_cap, L.num_kv_heads * n_hchunks, B);
   // completion counters first, then the split records
   uint32_t* tickets = static_cast<uint32_t*>(ws);
@@ -1044,6 +1030,20 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
 }  // namespace
 
 namespace jfkv {
+
+// Compute units of the current device (queried once per device).
+int num_cus() {
+  constexpr int kMaxDevices = 64;
+  static int cached[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < kMaxDevices && cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = 256;
+  if (dev < kMaxDevices) cached[dev] = n;
+  return n;
+}
 
 hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
                          const void* v_new, const void* q, int32_t B, int32_t Hq,

@@ -21,6 +21,9 @@ inline size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t head_dim, in
   return kDecodeCounterBytes + (size_t)B * Hq * max_splits * (head_dim + 4) * sizeof(float);
 }
 
+// Compute units of the current device (queried once per device).
+int num_cus();
+
 // Geometry accepted by every device entry point (validated on the host).
 bool geometry_supported(const jf_kv_layout& L);
 
