@@ -382,6 +382,9 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
         }
       }
     }
+    // interleave the matrix products with the folds and LDS reads around
+    // them (the scheduler's single-wave MFMA interleaving)
+    __builtin_amdgcn_iglp_opt(1);
     // keys past the limit, and (chunk tiles) keys after the row's position
     const bool need_mask = key0 + kKeys > key_lim || (chunk_tile && key0 + kKeys - 1 > i_min);
     if (need_mask) {
@@ -411,15 +414,16 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
       up = up || tmax[n] > m_run[n] + kTau;
     }
     if (__builtin_amdgcn_ballot_w64(up) != 0) {
+      // (selects, not a per-lane branch: the accumulators are scaled in
+      // place, by 1 in the lanes whose maximum stays)
 #pragma unroll
       for (int n = 0; n < NR; ++n) {
-        if (tmax[n] > m_run[n] + kTau) {
-          const float alpha = __builtin_amdgcn_exp2f(m_run[n] - tmax[n]);
-          m_run[n] = tmax[n];
-          l_run[n] *= alpha;
+        const bool raise = tmax[n] > m_run[n] + kTau;
+        const float alpha = raise ? __builtin_amdgcn_exp2f(m_run[n] - tmax[n]) : 1.0f;
+        m_run[n] = raise ? tmax[n] : m_run[n];
+        l_run[n] *= alpha;
 #pragma unroll
-          for (int t = 0; t < DT; ++t) acc_o[t][n] *= alpha;
-        }
+        for (int t = 0; t < DT; ++t) acc_o[t][n] *= alpha;
       }
     }
     // p = 2^(s |scale| - m) as fp16; P^T operand of 32-key step k: the
@@ -456,6 +460,9 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
 #pragma unroll
         for (int n = 0; n < NR; ++n) acc_o[t][n] = mfma(a, pb[n][k], acc_o[t][n]);
       }
+    // the same interleaving for the value products, the exponentials and the
+    // row sums
+    __builtin_amdgcn_iglp_opt(1);
   };
 
   for (int i = tid; i < 2 * kKeys * NBQ * 4; i += kThreads) (&sKb[0][0][0][0])[i] = 0u;
