@@ -103,8 +103,9 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
   constexpr int KSTEPS = D / 32;           // 32-dim MFMA steps of a score
   constexpr int DT = D / 16;               // 16-dim tiles of O^T
   constexpr int NG = D / G;                // scale groups per vector
-  constexpr int KP = D + 8;                // K^ row pitch (fp16)
-  constexpr int VP = kKeys + 8;            // V^T row pitch (fp16)
+  constexpr int KP = D + 16;               // K^ row pitch (fp16; 32 bytes of padding keep the
+                                           // 16-byte reads of 16 rows on distinct banks)
+  constexpr int VP = kKeys + 16;           // V^T row pitch (fp16; likewise)
   constexpr int QPK = D / 32;              // 16-byte K code chunks per key
   constexpr int CPV = D / 16;              // 16-byte V code chunks per key pair
   constexpr int KCH = kKeys * QPK;         // K code chunks per tile
