@@ -26,6 +26,7 @@ using jfkv::quantize8;
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 // Row staging of the tiled kernel: a 1 KiB load block plus 16 bytes, so the
 // lanes reading 128-byte row slices spread over the LDS banks.
 constexpr int kStagePitch = 1040;
@@ -295,23 +296,23 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
       hw[4 * i + 3] = x[i].w;
     }
 
-    // group minimum and maximum: integer total-order keys of both halves of
-    // a word at once (16-bit lanes: key = h ^ (sign ? 0xffff : 0x8000)),
-    // exact and order-free
+    // group minimum and maximum: IEEE minimum/maximum of packed fp16 pairs
+    // (exact, -0 below +0, so the same total order as the keys below; the
+    // compiler folds them into three-input instructions), taken to integer
+    // total-order keys (key = h ^ (sign ? 0xffff : 0x8000))
     uint32_t kmin[NGL], kmax[NGL];
 #pragma unroll
     for (int gl = 0; gl < NGL; ++gl) {
-      u16x2 lo2 = {0xffff, 0xffff}, hi2 = {0, 0};
+      f16x2 lo2 = __builtin_bit_cast(f16x2, hw[gl * EPG / 2]), hi2 = lo2;
 #pragma unroll
-      for (int w = gl * EPG / 2; w < (gl + 1) * EPG / 2; ++w) {
-        const i16x2 sgn = __builtin_bit_cast(i16x2, hw[w]) >> (short)15;
-        const u16x2 key = __builtin_bit_cast(
-            u16x2, hw[w] ^ (__builtin_bit_cast(uint32_t, sgn) | 0x80008000u));
-        lo2 = __builtin_elementwise_min(lo2, key);
-        hi2 = __builtin_elementwise_max(hi2, key);
+      for (int w = gl * EPG / 2 + 1; w < (gl + 1) * EPG / 2; ++w) {
+        lo2 = __builtin_elementwise_minimum(lo2, __builtin_bit_cast(f16x2, hw[w]));
+        hi2 = __builtin_elementwise_maximum(hi2, __builtin_bit_cast(f16x2, hw[w]));
       }
-      kmin[gl] = min((uint32_t)lo2.x, (uint32_t)lo2.y);
-      kmax[gl] = max((uint32_t)hi2.x, (uint32_t)hi2.y);
+      lo2 = __builtin_elementwise_minimum(lo2, lo2.yx);
+      hi2 = __builtin_elementwise_maximum(hi2, hi2.yx);
+      kmin[gl] = order_key(__builtin_bit_cast(unsigned short, lo2.x));
+      kmax[gl] = order_key(__builtin_bit_cast(unsigned short, hi2.x));
     }
     if constexpr (G == 128) {  // the group spans this lane and lane ^ 1
       kmin[0] = min(kmin[0], (uint32_t)__shfl_xor((int)kmin[0], 1));
