@@ -7,9 +7,10 @@
 // reusable storage").  The contract is bit-exact; every binary32 step is a
 // separately rounded IEEE operation in the order given in include/jfkv.h.
 //
-// Min and max use integer total-order keys of the fp16 bit patterns (exact
-// and independent of order); the mapping of rows to waves and lanes is
-// described at the kernel.
+// Group extremes are exact and independent of the element order (IEEE
+// minimum/maximum of fp16 values and integer total-order keys of their bit
+// patterns, -0 below +0); the mapping of rows to waves and lanes is described
+// at each kernel.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -23,21 +24,11 @@
 namespace {
 
 using jfkv::quantize8;
-typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
-typedef short i16x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 // Row staging of the tiled kernel: a 1 KiB load block plus 16 bytes, so the
 // lanes reading 128-byte row slices spread over the LDS banks.
 constexpr int kStagePitch = 1040;
-// LDS-DMA: this lane's 16 bytes at src land at LDS address lds + 16 * lane
-// (streaming: each byte is read once).
-__device__ __forceinline__ void dma_row_chunk(const uint8_t* src, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt"
-               :
-               : "s"(lds), "v"(src)
-               : "memory", "m0");
-}
 // a where mask is set, else b (bitwise; keeps register arrays out of memory).
 __device__ __forceinline__ uint32_t pick(uint32_t mask, uint32_t a, uint32_t b) {
   return (a & mask) | (b & ~mask);
