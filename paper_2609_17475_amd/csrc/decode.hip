@@ -12,10 +12,10 @@
 // not by the context length.
 //
 // Data movement: a block of waves (eight at d <= 128) owns one split; its
-// waves take the
-// split's rows (a row = 32 positions of one page) in turn and stream each
-// row into a private LDS ring with global_load_lds (HBM -> LDS without
-// registers), all ring stages in flight while a row is computed.
+// waves take the split's rows (a row = 32 positions of one page) in turn and
+// stream each row into a private LDS ring with global_load_lds (HBM -> LDS
+// without registers), all ring stages in flight while a row is computed.
+// The waves meet at a barrier once per ring cycle.
 //
 // Arithmetic (v_mfma_f32_16x16x32_f16, fp32 accumulation): a 4-bit code
 // masked into the low bits of an fp16 half is the subnormal c * 2^-24 (a
@@ -377,8 +377,8 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
 }
 
 // Decode kernel.  Block = 8 (d <= 128) or 4 waves = one split of one
-// (request, KV head, chunk
-// of up to 4 query heads).  Lane (m, q) = (lane % 16, lane / 16) feeds row m
+// (request, KV head, chunk of up to 4 query heads).  Lane (m, q) =
+// (lane % 16, lane / 16) feeds row m
 // and k-quarter q of the MFMA operands and receives column m, rows 4q..4q+3
 // of the 16x16 results.
 //   scores: tile t (0, 1) row m = position 8 (m / 4) + 4 t + m % 4 of the row,
@@ -389,14 +389,16 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
 //           + 7 (the lane's four position pairs) of that dim, B = W of the
 //           same positions (exactly the lane's eight score positions), so the
 //           scores never leave their lanes.
-// Progress: the waves of a block meet only after their row loops; every loop
-// ends after the wave's own rows.
+// Progress: every wave runs the same number of ring cycles (its last ones
+// without rows) and the block's waves meet at a barrier after each cycle.
 //
-// APPEND (the fused decode step): the block of each request's last split
-// first quantizes the request's new K/V row (fp16 [B][Hkv][d], one per
-// request, at position seq_lens[b] - 1) for its KV head into the pool, then
-// attends; only that block reads the row's page, and it issues its page
-// loads after the row's stores have completed.
+// APPEND (the fused decode step): in the block of each request's last split,
+// the wave that streams the row holding position seq_lens[b] - 1 quantizes
+// the request's new K/V row (fp16 [B][Hkv][d], one per request) for its KV
+// head while its first page loads are in flight, stores it to the pool
+// without waiting, and writes the same bytes into its LDS stage once that
+// row's loads have landed (they may still see the slot's previous bytes);
+// no other block reads that page.
 template <int D, int G, bool APPEND>
 __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     uint8_t* __restrict__ k_codes, uint32_t* __restrict__ k_meta,
@@ -492,7 +494,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   const int t_end = min(pe * P, L);
   const int rows_per_page = P / kRowPos;
 
-  // this wave's rows: the split's rows in page order, wave, wave + 4, ...
+  // this wave's rows: the split's rows in page order, wave, wave + kWaves, ...
   const int n_split_pages = pe - pb;
   const int split_rows = n_split_pages * rows_per_page;
   const int my_rows = (split_rows > wave) ? (split_rows - wave + kWaves - 1) / kWaves : 0;
