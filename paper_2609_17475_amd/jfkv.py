@@ -225,8 +225,7 @@ def _dev_check(t, name, dtype=None):
         raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
 
 
-def jf_kv_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_tables,
-                          stream=None):
+def _check_append_args(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_tables):
     import torch
     for t, n, dt in ((k_new, "k_new", torch.float16), (v_new, "v_new", torch.float16),
                      (cu_tok, "cu_tok", torch.int32), (start_pos, "start_pos", torch.int32),
@@ -239,6 +238,14 @@ def jf_kv_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_t
     B = start_pos.shape[0]
     if cu_tok.shape[0] != B + 1 or block_tables.dim() != 2 or block_tables.shape[0] != B:
         raise ValueError("cu_tok [B+1], start_pos [B], block_tables [B][max_pages]")
+
+
+def jf_kv_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_tables,
+                          stream=None):
+    _check_append_args(pool, k_new, v_new, cu_tok, start_pos, block_tables)
+    lay = pool.layout
+    total = k_new.shape[0]
+    B = start_pos.shape[0]
     ptrs = pool.ptrs()
     _check(lib.jf_kv_quantize_append(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new),
                                      _ptr(v_new), _ptr(cu_tok), _ptr(start_pos),
@@ -266,6 +273,17 @@ def _check_decode_args(pool: KVPool, q, block_tables, seq_lens, workspace, out):
         raise ValueError("block_tables [B][max_pages], seq_lens [B]")
 
 
+def _check_step_args(pool: KVPool, k_new, v_new, q, block_tables, seq_lens, workspace, out):
+    import torch
+    _dev_check(k_new, "k_new", torch.float16)
+    _dev_check(v_new, "v_new", torch.float16)
+    lay = pool.layout
+    B = q.shape[0]
+    if tuple(k_new.shape) != (B, lay.num_kv_heads, lay.head_dim) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [B][Hkv][head_dim]")
+    _check_decode_args(pool, q, block_tables, seq_lens, workspace, out)
+
+
 def jf_decode_attn_q4(pool: KVPool, q, block_tables, seq_lens, softmax_scale: float,
                       max_splits: int, workspace, out, stream=None):
     _check_decode_args(pool, q, block_tables, seq_lens, workspace, out)
@@ -283,14 +301,9 @@ def jf_decode_step_q4(pool: KVPool, k_new, v_new, q, block_tables, seq_lens,
                       softmax_scale: float, max_splits: int, workspace, out, stream=None):
     """Append request b's row (k_new/v_new fp16 [B][Hkv][d]) at position
     seq_lens[b] - 1, then attend over seq_lens[b] positions; one kernel."""
-    import torch
-    _dev_check(k_new, "k_new", torch.float16)
-    _dev_check(v_new, "v_new", torch.float16)
+    _check_step_args(pool, k_new, v_new, q, block_tables, seq_lens, workspace, out)
     lay = pool.layout
     B = q.shape[0]
-    if tuple(k_new.shape) != (B, lay.num_kv_heads, lay.head_dim) or v_new.shape != k_new.shape:
-        raise ValueError("k_new/v_new must be [B][Hkv][head_dim]")
-    _check_decode_args(pool, q, block_tables, seq_lens, workspace, out)
     ptrs = pool.ptrs()
     _check(lib.jf_decode_step_q4(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new), _ptr(v_new),
                                  _ptr(q), B, q.shape[1], _ptr(block_tables), block_tables.shape[1],
@@ -299,8 +312,7 @@ def jf_decode_step_q4(pool: KVPool, k_new, v_new, q, block_tables, seq_lens,
                                  _ptr(out), _stream(stream)))
 
 
-def jf_prefill_attn_q4(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len: int,
-                       softmax_scale: float, out, stream=None):
+def _check_prefill_args(pool: KVPool, q, k_chunk, v_chunk, block_table, out):
     import torch
     _dev_check(q, "q", torch.float16)
     _dev_check(k_chunk, "k_chunk", torch.float16)
@@ -313,6 +325,13 @@ def jf_prefill_attn_q4(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_le
         raise ValueError("q/out must be [T][Hq][head_dim]")
     if tuple(k_chunk.shape) != (T, lay.num_kv_heads, d) or v_chunk.shape != k_chunk.shape:
         raise ValueError("k_chunk/v_chunk must be [T][Hkv][head_dim]")
+
+
+def jf_prefill_attn_q4(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len: int,
+                       softmax_scale: float, out, stream=None):
+    _check_prefill_args(pool, q, k_chunk, v_chunk, block_table, out)
+    lay = pool.layout
+    T, Hq, d = q.shape
     ptrs = pool.ptrs()
     _check(lib.jf_prefill_attn_q4(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), _ptr(k_chunk),
                                   _ptr(v_chunk), T, Hq, _ptr(block_table), block_table.shape[-1],
@@ -336,6 +355,7 @@ class BoundCall:
 
 def bind_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_tables,
                          stream=None) -> BoundCall:
+    _check_append_args(pool, k_new, v_new, cu_tok, start_pos, block_tables)
     lay, ptrs = pool.layout, pool.ptrs()
     B = start_pos.shape[0]
     args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new), _ptr(v_new), _ptr(cu_tok),
@@ -347,6 +367,7 @@ def bind_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_ta
 
 def bind_decode(pool: KVPool, q, block_tables, seq_lens, softmax_scale, max_splits, workspace,
                 out, stream=None) -> BoundCall:
+    _check_decode_args(pool, q, block_tables, seq_lens, workspace, out)
     lay, ptrs = pool.layout, pool.ptrs()
     B, Hq, _ = q.shape
     args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), B, Hq, _ptr(block_tables),
@@ -359,6 +380,7 @@ def bind_decode(pool: KVPool, q, block_tables, seq_lens, softmax_scale, max_spli
 
 def bind_decode_step(pool: KVPool, k_new, v_new, q, block_tables, seq_lens, softmax_scale,
                      max_splits, workspace, out, stream=None) -> BoundCall:
+    _check_step_args(pool, k_new, v_new, q, block_tables, seq_lens, workspace, out)
     lay, ptrs = pool.layout, pool.ptrs()
     B, Hq, _ = q.shape
     args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new), _ptr(v_new), _ptr(q), B, Hq,
@@ -371,6 +393,7 @@ def bind_decode_step(pool: KVPool, k_new, v_new, q, block_tables, seq_lens, soft
 
 def bind_prefill(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len, softmax_scale, out,
                  stream=None) -> BoundCall:
+    _check_prefill_args(pool, q, k_chunk, v_chunk, block_table, out)
     lay, ptrs = pool.layout, pool.ptrs()
     T, Hq, _ = q.shape
     args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), _ptr(k_chunk), _ptr(v_chunk), T, Hq,
