@@ -247,6 +247,10 @@ def main():
                     help="positions in the CPU oracle sample (0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="repeat the CPU oracle step for at least this long")
+    ap.add_argument("--positions", type=int, default=0,
+                    help="decode: context length in positions, a multiple of the page size "
+                         "(0 = the 262,144-position window of decode_256k); other lengths "
+                         "print a decode_<positions> line without the counter traffic")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
     ap.add_argument("--workload", default="decode_256k",
@@ -277,10 +281,14 @@ def main():
     torch.cuda.set_device(dev)
     wl = workloads.WORKLOADS["decode_256k"]
     P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
-    L = wl.seq_lens[0]
+    L = args.positions or wl.seq_lens[0]
+    if L < P or L % P:
+        print("--positions must be a positive multiple of the page size (%d)" % P, file=sys.stderr)
+        sys.exit(2)
+    window = L == wl.seq_lens[0]
     n_cached = L - 1
     n_steps_total = args.warmup + args.steps
-    NP = wl.pool_pages
+    NP = L // P + (wl.pool_pages - wl.seq_lens[0] // P)  # the window's pages + spare pages
     lay = jfkv.layout(P, hkv, d, G, NP)
 
     # ---- page table: one request holding the full window (shuffled pages)
@@ -405,7 +413,7 @@ def main():
         "vs_baseline": None,
         "dtype": "u4 codes x f16 -> f32",
         "data": "synthetic",
-        "config": {"workload": "decode_256k", "positions": L, "batch": 1, "num_q_heads": hq,
+        "config": {"workload": "decode_256k" if window else "decode_%d" % L, "positions": L, "batch": 1, "num_q_heads": hq,
                    "num_kv_heads": hkv, "head_dim": d, "page_size": P, "group_size": G,
                    "pages": L // P, "max_splits": args.max_splits,
                    "splits_used": min(args.max_splits, L // P, -(-torch.cuda.get_device_properties(
@@ -420,7 +428,8 @@ def main():
                         "gpu": 1e3 * gpu_ms_per_step,
                         "wall": 1e3 * ms_per_step},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic() if window else None,
                      "kernel": ("decode_kernel (split-K partials and the in-kernel combine)"
                                 if args.two_calls else
                                 "decode_kernel, fused step (row append, split-K partials, "
