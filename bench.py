@@ -233,6 +233,51 @@ def bench_quantize_bulk(args):
         "cpu_baseline": None}), flush=True)
 
 
+def bench_tq4_encode(args):
+    """TQ4 bulk encode-and-append of 262,143 rows x 4 KV heads (d 256, the
+    paper's full-attention geometry) into 1,024 shuffled pages; HBM roofline
+    over the kernel: 512 B read and 128 + 2 B written per vector."""
+    import numpy as np
+    import torch
+    from paper_2609_17475_amd import jfkv
+    dev = torch.device("cuda:0")
+    P, hkv, d, L = 256, 4, 256, 262143
+    NP = L // P + 1 + 8
+    rng = np.random.default_rng(4)
+    table = torch.tensor(rng.permutation(NP)[:L // P + 1][None].astype(np.int32), device=dev)
+    g = torch.Generator(device=dev).manual_seed(4)
+    x = torch.randn((L, hkv, d), generator=g, device=dev, dtype=torch.float32).half()
+    # signs and centroids are inputs of the kernel: any +-1 vector and any
+    # ascending 16 values time the same; these are fixed stand-ins
+    signs = torch.tensor(np.where(rng.random(d) < 0.5, -1.0, 1.0), dtype=torch.float32,
+                         device=dev)
+    cents = torch.linspace(-0.17, 0.17, 16, dtype=torch.float32, device=dev)
+    lay = jfkv.layout(P, hkv, d, 64, NP)
+    pools = [jfkv.TQ4Pool(lay, device=dev) for _ in range(4)]
+    cu = torch.tensor([0, L], dtype=torch.int32, device=dev)
+    st = torch.tensor([0], dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    calls = [[jfkv.bind_tq4_encode_append(p, x, signs, cents, cu, st, table, stream)]
+             for p in pools]
+    steps = max(1, args.steps // 4)
+    (t_e,), wall = _timed(calls, args.warmup, steps, stream)
+    nbytes = L * hkv * (2 * d + d // 2 + 2)
+    achieved = nbytes / (t_e * 1e-6) / 1e9
+    print(json.dumps({
+        "metric": "TQ4 bulk encode-append GB/s (262,143 rows x 4 KV heads, d 256)",
+        "value": nbytes / (wall * 1e-6) / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": wall / 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16 -> u4 indices + f16 norm",
+        "data": "synthetic",
+        "config": {"workload": "tq4_encode_bulk", "rows": L, "num_kv_heads": hkv, "head_dim": d,
+                   "page_size": P},
+        "us_per_step": {"tq4_encode": t_e, "wall": wall},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "tq4_encode_kernel", "algorithmic_bytes": nbytes},
+        "cpu_baseline": None}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -254,7 +299,7 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
     ap.add_argument("--workload", default="decode_256k",
-                    choices=["decode_256k", "prefill_chunk", "quantize_bulk"],
+                    choices=["decode_256k", "prefill_chunk", "quantize_bulk", "tq4_encode_bulk"],
                     help="decode_256k (the headline line); prefill_chunk and quantize_bulk "
                          "print their own lines")
     args = ap.parse_args()
@@ -270,6 +315,9 @@ def main():
         return
     if args.workload == "quantize_bulk":
         bench_quantize_bulk(args)
+        return
+    if args.workload == "tq4_encode_bulk":
+        bench_tq4_encode(args)
         return
 
     import numpy as np

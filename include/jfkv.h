@@ -292,6 +292,48 @@ jf_status jf_prefill_attn_q4(const jf_kv_layout* layout,
                              int32_t prefix_len, float softmax_scale,
                              void* out, hipStream_t stream);
 
+/* ---------------------------------------------------------------- TQ4
+ * The paper's own 4-bit format (Sec. 3.1, eq. codec; Appendix A, Table
+ * codec): a 256-element vector x is stored as the fp16 norm of x and 256
+ * 4-bit indices z, where z_i indexes the one of 16 shared centroids c
+ * (ascending) nearest to coordinate i of the rotated unit vector
+ * y = H_256 S x / (16 |x|) (H_256 the unnormalised Sylvester Hadamard matrix,
+ * S = diag(signs)).  Reconstruction: x_hat = norm * S H_256 c[z] / 16.
+ *
+ * Pool (per layer, per K or V; caller-owned device memory), head-major
+ * pages like the affine pool:
+ *   words  u32  [num_pages][num_kv_heads][page_size][32]  element 8w + k of
+ *               a vector in bits 4k..4k+3 of word w
+ *   norms  fp16 [num_pages][num_kv_heads][page_size]
+ * Only page_size, num_kv_heads, head_dim (256) and num_pages of the layout
+ * are used; group_size is ignored. */
+jf_status jf_tq4_pool_bytes(const jf_kv_layout* layout, size_t* words_bytes,
+                            size_t* norms_bytes);
+
+/* Encode-and-append total_tok rows of K or V (one call per tensor, each
+ * with its own signs) into a TQ4 pool, async on `stream`, one kernel.
+ *   x            fp16 [total_tok][num_kv_heads][256] (device, 8-byte aligned)
+ *   signs        fp32 [256] (device, 16-byte aligned), each +1 or -1
+ *   centroids    fp32 [16] (device), ascending
+ *   cu_tok, start_pos, block_tables, B, max_pages: as in
+ *                jf_kv_quantize_append (row i of request b goes to logical
+ *                position start_pos[b] + i; rows whose position falls outside
+ *                the table or whose page ID is outside [0, num_pages) are
+ *                not written)
+ * Norm: the float32 Euclidean norm, rounded to fp16.  Index of a coordinate:
+ * the number of thresholds (c_j + c_{j+1}) / 2 (float32) it strictly exceeds.
+ * A zero vector gets norm 0 and the indices of coordinate 0.
+ * Errors: NULL or misaligned pointers, B or max_pages <= 0, total_tok < 0
+ * -> JF_ERR_INVALID; head_dim != 256 -> JF_ERR_UNSUPPORTED; no launch on
+ * error. */
+jf_status jf_tq4_encode_append(const jf_kv_layout* layout, void* words,
+                               void* norms, const void* x, const float* signs,
+                               const float* centroids, const int32_t* cu_tok,
+                               const int32_t* start_pos,
+                               const int32_t* block_tables, int32_t B,
+                               int32_t max_pages, int32_t total_tok,
+                               hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -461,4 +461,53 @@ jf_status jf_prefill_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* 
                        "prefill launch");
 }
 
+// ------------------------------------------------------------------ TQ4
+namespace {
+
+jf_status check_tq4_layout(const jf_kv_layout* layout) {
+  if (!layout) return fail(JF_ERR_INVALID, "layout is NULL");
+  if (layout->page_size <= 0 || layout->num_kv_heads <= 0 || layout->num_pages <= 0)
+    return fail(JF_ERR_INVALID, "page_size, num_kv_heads and num_pages must be positive");
+  if (layout->head_dim != 256)
+    return fail(JF_ERR_UNSUPPORTED, "TQ4 head_dim must be 256, got %d", layout->head_dim);
+  if ((int64_t)layout->num_pages * layout->num_kv_heads * layout->page_size > INT32_MAX)
+    return fail(JF_ERR_INVALID, "pool has more than INT32_MAX vectors");
+  return ok();
+}
+
+}  // namespace
+
+jf_status jf_tq4_pool_bytes(const jf_kv_layout* layout, size_t* words_bytes,
+                            size_t* norms_bytes) {
+  jf_status st = check_tq4_layout(layout);
+  if (st) return st;
+  if (!words_bytes || !norms_bytes) return fail(JF_ERR_INVALID, "NULL output pointer");
+  const size_t vecs = (size_t)layout->num_pages * layout->num_kv_heads * layout->page_size;
+  *words_bytes = vecs * (layout->head_dim / 2);
+  *norms_bytes = vecs * 2;
+  return ok();
+}
+
+jf_status jf_tq4_encode_append(const jf_kv_layout* layout, void* words, void* norms,
+                               const void* x, const float* signs, const float* centroids,
+                               const int32_t* cu_tok, const int32_t* start_pos,
+                               const int32_t* block_tables, int32_t B, int32_t max_pages,
+                               int32_t total_tok, hipStream_t stream) {
+  jf_status st = check_tq4_layout(layout);
+  if (st) return st;
+  if (B <= 0 || max_pages <= 0 || total_tok < 0)
+    return fail(JF_ERR_INVALID, "B and max_pages must be positive, total_tok >= 0");
+  if (!words || !norms) return fail(JF_ERR_INVALID, "NULL pool pointer");
+  if (total_tok == 0) return ok();
+  if (!x || !signs || !centroids || !cu_tok || !start_pos || !block_tables)
+    return fail(JF_ERR_INVALID, "NULL device pointer");
+  if (((uintptr_t)x & 7) || ((uintptr_t)signs & 15) || ((uintptr_t)words & 3) ||
+      ((uintptr_t)norms & 1))
+    return fail(JF_ERR_INVALID, "x must be 8-byte, signs 16-byte, words 4-byte, norms 2-byte aligned");
+  return device_status(jfkv::launch_tq4_encode(*layout, words, norms, x, signs, centroids, cu_tok,
+                                               start_pos, block_tables, B, max_pages, total_tok,
+                                               stream),
+                       "tq4_encode launch");
+}
+
 }  // extern "C"

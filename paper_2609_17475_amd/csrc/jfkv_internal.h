@@ -53,4 +53,9 @@ hipError_t launch_prefill(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
                           int32_t prefix_len, float softmax_scale, void* out,
                           hipStream_t stream);
 
+hipError_t launch_tq4_encode(const jf_kv_layout& L, void* words, void* norms, const void* x,
+                             const float* signs, const float* centroids, const int32_t* cu_tok,
+                             const int32_t* start_pos, const int32_t* block_tables, int32_t B,
+                             int32_t max_pages, int32_t total_tok, hipStream_t stream);
+
 }  // namespace jfkv

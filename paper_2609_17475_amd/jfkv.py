@@ -27,7 +27,7 @@ EXPORTS = [
     "jf_page_table_set_length", "jf_page_table_release", "jf_page_table_export",
     "jf_page_table_stats", "jf_page_table_info",
     "jf_kv_quantize_append", "jf_decode_workspace_bytes", "jf_decode_attn_q4",
-    "jf_decode_step_q4", "jf_prefill_attn_q4",
+    "jf_decode_step_q4", "jf_prefill_attn_q4", "jf_tq4_pool_bytes", "jf_tq4_encode_append",
 ]
 
 
@@ -82,6 +82,8 @@ def _load():
         "jf_decode_step_q4": (st, [P, P, P, P, P, i32, i32, P, i32, P, ctypes.c_float, i32, P, sz,
                                    P, P]),
         "jf_prefill_attn_q4": (st, [P, P, P, P, P, i32, i32, P, i32, i32, ctypes.c_float, P, P]),
+        "jf_tq4_pool_bytes": (st, [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
+        "jf_tq4_encode_append": (st, [P, P, P, P, P, P, P, P, P, i32, i32, i32, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -401,3 +403,69 @@ def bind_prefill(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len, sof
             _ptr(out), _stream(stream))
     return BoundCall(lib.jf_prefill_attn_q4, args,
                      (lay, ptrs, pool, q, k_chunk, v_chunk, block_table, out))
+
+
+# ---------------------------------------------------------------- TQ4 format
+def tq4_pool_bytes(lay: Layout):
+    w, n = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib.jf_tq4_pool_bytes(ctypes.byref(lay), ctypes.byref(w), ctypes.byref(n)))
+    return w.value, n.value
+
+
+class TQ4Pool:
+    """One layer's TQ4 pool for K or V in device memory: index words (u32 bit
+    patterns held as int32) [num_pages][num_kv_heads][page_size][head_dim/8]
+    and fp16 norms [num_pages][num_kv_heads][page_size]."""
+
+    def __init__(self, lay: Layout, device="cuda", fill: Optional[int] = None):
+        import torch
+        self.layout = lay
+        wb, nb = tq4_pool_bytes(lay)
+        w = torch.empty(wb, dtype=torch.uint8, device=device)
+        n = torch.empty(nb, dtype=torch.uint8, device=device)
+        if fill is not None:
+            w.fill_(fill)
+            n.fill_(fill)
+        shape = (lay.num_pages, lay.num_kv_heads, lay.page_size)
+        self.words = w.view(torch.int32).view(*shape, lay.head_dim // 8)
+        self.norms = n.view(torch.float16).view(*shape)
+
+
+def _check_tq4_args(pool: TQ4Pool, x, signs, centroids, cu_tok, start_pos, block_tables):
+    import torch
+    for t, n, dt in ((x, "x", torch.float16), (signs, "signs", torch.float32),
+                     (centroids, "centroids", torch.float32), (cu_tok, "cu_tok", torch.int32),
+                     (start_pos, "start_pos", torch.int32),
+                     (block_tables, "block_tables", torch.int32)):
+        _dev_check(t, n, dt)
+    lay = pool.layout
+    if x.dim() != 3 or tuple(x.shape[1:]) != (lay.num_kv_heads, lay.head_dim):
+        raise ValueError("x must be [total_tok][Hkv][head_dim]")
+    if signs.numel() != lay.head_dim or centroids.numel() != 16:
+        raise ValueError("signs [head_dim], centroids [16]")
+    B = start_pos.shape[0]
+    if cu_tok.shape[0] != B + 1 or block_tables.dim() != 2 or block_tables.shape[0] != B:
+        raise ValueError("cu_tok [B+1], start_pos [B], block_tables [B][max_pages]")
+
+
+def jf_tq4_encode_append(pool: TQ4Pool, x, signs, centroids, cu_tok, start_pos, block_tables,
+                         stream=None):
+    """Encode rows x [total_tok][Hkv][256] (fp16) into a TQ4 pool at their
+    logical positions (see include/jfkv.h)."""
+    _check_tq4_args(pool, x, signs, centroids, cu_tok, start_pos, block_tables)
+    _check(lib.jf_tq4_encode_append(ctypes.byref(pool.layout), _ptr(pool.words), _ptr(pool.norms),
+                                    _ptr(x), _ptr(signs), _ptr(centroids), _ptr(cu_tok),
+                                    _ptr(start_pos), _ptr(block_tables), start_pos.shape[0],
+                                    block_tables.shape[1], x.shape[0], _stream(stream)))
+
+
+def bind_tq4_encode_append(pool: TQ4Pool, x, signs, centroids, cu_tok, start_pos, block_tables,
+                           stream=None) -> "BoundCall":
+    """jf_tq4_encode_append with its arguments checked and marshalled once."""
+    _check_tq4_args(pool, x, signs, centroids, cu_tok, start_pos, block_tables)
+    lay = pool.layout
+    args = (ctypes.byref(lay), _ptr(pool.words), _ptr(pool.norms), _ptr(x), _ptr(signs),
+            _ptr(centroids), _ptr(cu_tok), _ptr(start_pos), _ptr(block_tables),
+            start_pos.shape[0], block_tables.shape[1], x.shape[0], _stream(stream))
+    return BoundCall(lib.jf_tq4_encode_append, args,
+                     (lay, pool, x, signs, centroids, cu_tok, start_pos, block_tables))

@@ -89,3 +89,24 @@ def test_prefill_and_append_validation():
     st = L.jf_kv_quantize_append(ctypes.byref(lay), ctypes.byref(ptrs), 1, 1, 1, 1, 1, 1, 4, 0,
                                  None)
     assert st == jfkv.JF_OK  # nothing to append
+
+
+def test_tq4_pool_bytes_and_validation():
+    lay = jfkv.layout(256, 4, 256, 64, 10)
+    # 128 packed bytes and a 2-byte norm per vector (Background, TQ4 payload)
+    assert jfkv.tq4_pool_bytes(lay) == (10 * 4 * 256 * 128, 10 * 4 * 256 * 2)
+    with pytest.raises(jfkv.JfError) as e:
+        jfkv.tq4_pool_bytes(jfkv.layout(256, 4, 128, 64, 10))
+    assert e.value.status == 4  # JF_ERR_UNSUPPORTED
+    L = jfkv.lib
+    # rejected before any launch: NULL pool, B = 0, misaligned x (no device touched)
+    assert L.jf_tq4_encode_append(ctypes.byref(lay), None, 16, 16, 16, 16, 16, 16, 16, 1, 4, 1,
+                                  None) == 1
+    assert L.jf_tq4_encode_append(ctypes.byref(lay), 16, 16, 16, 16, 16, 16, 16, 16, 0, 4, 1,
+                                  None) == 1
+    assert L.jf_tq4_encode_append(ctypes.byref(lay), 16, 16, 17, 16, 16, 16, 16, 16, 1, 4, 1,
+                                  None) == 1
+    assert b"aligned" in L.jf_last_error()
+    # nothing to encode: success without a launch
+    assert L.jf_tq4_encode_append(ctypes.byref(lay), 16, 16, None, None, None, None, None, None,
+                                  1, 4, 0, None) == 0
