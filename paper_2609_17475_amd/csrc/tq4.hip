@@ -5,8 +5,9 @@
 // u32 word and stored with the fp16 norm at the vector's page slot
 // (Appendix A, Table codec; Background, page table).
 //
-// One wave per vector.  Lane l holds elements 4l .. 4l + 3 (one 8-byte load:
-// the 64 lanes read the vector's 512 bytes in one coalesced access).  The
+// One wave per vector at a time, four vectors per wave (their loads issued
+// together).  Lane l holds elements 4l .. 4l + 3 (one 8-byte load: the 64
+// lanes read the vector's 512 bytes in one coalesced access).  The
 // Walsh-Hadamard transform takes the first two of its eight butterfly stages
 // inside each lane (element index bits 0 and 1) and the other six across
 // lanes (index bits 2..7 are lane bits 0..5), with one exchange per stage and
@@ -15,7 +16,9 @@
 //
 // Index of a coordinate: the number of midpoint thresholds between adjacent
 // centroids that it strictly exceeds (a coordinate on a threshold keeps the
-// lower index).  The thresholds are the float32 midpoints (c_j + c_{j+1}) / 2.
+// lower index), found by a 4-step binary search over the float32 midpoints
+// (c_j + c_{j+1}) / 2 held in LDS.  y is the transformed vector times one
+// correctly rounded reciprocal of 16 rho.
 // A vector of norm 0 has every coordinate 0.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -28,6 +31,7 @@ namespace {
 
 constexpr int kD = 256;          // head dimension of the format
 constexpr int kWavesPerBlock = 4;
+constexpr int kVecPerWave = 4;   // vectors per wave, their loads issued together
 constexpr int kLevels = 16;
 
 __device__ __forceinline__ float2 h2_to_f2(uint32_t u) {
@@ -40,74 +44,93 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
     const int32_t* __restrict__ cu_tok, const int32_t* __restrict__ start_pos,
     const int32_t* __restrict__ block_tables, int B, int max_pages, int Hkv, int P, int NP,
     int64_t n_vec) {
+  // thresholds for a 4-step binary search: entry 15 is +inf (never passed)
+  __shared__ float thr[kLevels];
+  if (threadIdx.x < kLevels)
+    thr[threadIdx.x] = threadIdx.x < kLevels - 1
+                           ? (centroids[threadIdx.x] + centroids[threadIdx.x + 1]) * 0.5f
+                           : INFINITY;
+  __syncthreads();
+
   const int lane = threadIdx.x & 63;
-  const int64_t vec = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-  if (vec >= n_vec) return;  // the whole wave: one vector per wave
-  const int64_t row = vec / Hkv;
-  const int kv = (int)(vec - row * Hkv);
+  const int64_t vec0 = ((int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kVecPerWave;
+  if (vec0 >= n_vec) return;  // the whole wave
+  const int nv = (int)min<int64_t>(kVecPerWave, n_vec - vec0);
 
-  const uint2 raw = x[vec * (kD / 4) + lane];
+  const uint64_t* xw = reinterpret_cast<const uint64_t*>(x);
+  uint64_t raw[kVecPerWave];
+#pragma unroll
+  for (int v = 0; v < kVecPerWave; ++v)
+    if (v < nv) raw[v] = __builtin_nontemporal_load(&xw[(vec0 + v) * (kD / 4) + lane]);
   const float4 s = reinterpret_cast<const float4*>(signs)[lane];
-  const float2 f01 = h2_to_f2(raw.x), f23 = h2_to_f2(raw.y);
+  // butterfly sign of each cross-lane stage: the lane with the index bit set
+  // takes partner - own, the other own + partner (fma by +-1 is exact)
+  float sg[6];
+#pragma unroll
+  for (int k = 0; k < 6; ++k) sg[k] = (lane >> k) & 1 ? -1.0f : 1.0f;
 
-  // norm: squares of fp16 values are exact in float32
-  float ss = f01.x * f01.x + f01.y * f01.y + f23.x * f23.x + f23.y * f23.y;
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
-  const float rho = sqrtf(ss);
+  for (int v = 0; v < kVecPerWave; ++v) {
+    if (v >= nv) break;
+    const int64_t vec = vec0 + v;
+    const float2 f01 = h2_to_f2((uint32_t)raw[v]), f23 = h2_to_f2((uint32_t)(raw[v] >> 32));
 
-  // H_256 S x: two stages in the lane, six across lanes
-  float v0 = s.x * f01.x, v1 = s.y * f01.y, v2 = s.z * f23.x, v3 = s.w * f23.y;
-  {
-    const float a0 = v0 + v1, a1 = v0 - v1, a2 = v2 + v3, a3 = v2 - v3;
-    v0 = a0 + a2; v1 = a1 + a3; v2 = a0 - a2; v3 = a1 - a3;
-  }
+    // norm: squares of fp16 values are exact in float32
+    float ss = f01.x * f01.x + f01.y * f01.y + f23.x * f23.x + f23.y * f23.y;
 #pragma unroll
-  for (int m = 1; m < 64; m <<= 1) {
-    const bool hi = (lane & m) != 0;
-    const float p0 = __shfl_xor(v0, m, 64), p1 = __shfl_xor(v1, m, 64);
-    const float p2 = __shfl_xor(v2, m, 64), p3 = __shfl_xor(v3, m, 64);
-    v0 = hi ? p0 - v0 : v0 + p0;
-    v1 = hi ? p1 - v1 : v1 + p1;
-    v2 = hi ? p2 - v2 : v2 + p2;
-    v3 = hi ? p3 - v3 : v3 + p3;
-  }
-  // rotated unit vector y = H S x / (16 rho)
-  const float den = rho * 16.0f;
-  float y[4] = {v0, v1, v2, v3};
-#pragma unroll
-  for (int j = 0; j < 4; ++j) y[j] = rho > 0.0f ? __fdiv_rn(y[j], den) : 0.0f;
+    for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+    const float rho = sqrtf(ss);
 
-  uint32_t q = 0;  // four 4-bit indices: element 4 lane + j at bits 4j
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    uint32_t idx = 0;
-#pragma unroll
-    for (int t = 0; t < kLevels - 1; ++t) {
-      const float thr = (centroids[t] + centroids[t + 1]) * 0.5f;
-      idx += y[j] > thr ? 1u : 0u;
+    // H_256 S x: two stages in the lane, six across lanes
+    float e0 = s.x * f01.x, e1 = s.y * f01.y, e2 = s.z * f23.x, e3 = s.w * f23.y;
+    {
+      const float a0 = e0 + e1, a1 = e0 - e1, a2 = e2 + e3, a3 = e2 - e3;
+      e0 = a0 + a2; e1 = a1 + a3; e2 = a0 - a2; e3 = a1 - a3;
     }
-    q |= idx << (4 * j);
-  }
-  // word w = elements 8w .. 8w + 7: lanes 2w (low half) and 2w + 1
-  const uint32_t partner = (uint32_t)__shfl_xor((int)q, 1, 64);
-  const uint32_t word = q | (partner << 16);
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+      const int m = 1 << k;
+      const float p0 = __shfl_xor(e0, m, 64), p1 = __shfl_xor(e1, m, 64);
+      const float p2 = __shfl_xor(e2, m, 64), p3 = __shfl_xor(e3, m, 64);
+      e0 = fmaf(sg[k], e0, p0);
+      e1 = fmaf(sg[k], e1, p1);
+      e2 = fmaf(sg[k], e2, p2);
+      e3 = fmaf(sg[k], e3, p3);
+    }
+    // rotated unit vector y = H S x / (16 rho), by one rounded reciprocal
+    const float inv = rho > 0.0f ? __fdiv_rn(1.0f, rho * 16.0f) : 0.0f;
+    const float y[4] = {e0 * inv, e1 * inv, e2 * inv, e3 * inv};
 
-  // request of this row and its logical position
-  int32_t lo = 0, hi = B;  // largest b with cu_tok[b] <= row
-  while (hi - lo > 1) {
-    const int32_t mid = (lo + hi) >> 1;
-    if (cu_tok[mid] <= row) lo = mid; else hi = mid;
+    uint32_t q = 0;  // four 4-bit indices: element 4 lane + j at bits 4j
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int idx = 0;  // number of thresholds strictly below y[j]
+#pragma unroll
+      for (int step = 8; step >= 1; step >>= 1) idx += y[j] > thr[idx + step - 1] ? step : 0;
+      q |= (uint32_t)idx << (4 * j);
+    }
+    // word w = elements 8w .. 8w + 7: lanes 2w (low half) and 2w + 1
+    const uint32_t partner = (uint32_t)__shfl_xor((int)q, 1, 64);
+    const uint32_t word = q | (partner << 16);
+
+    // request of this row and its logical position
+    const int64_t row = vec / Hkv;
+    const int kv = (int)(vec - row * Hkv);
+    int32_t lo = 0, hi = B;  // largest b with cu_tok[b] <= row
+    while (hi - lo > 1) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (cu_tok[mid] <= row) lo = mid; else hi = mid;
+    }
+    const int64_t pos = (int64_t)start_pos[lo] + (row - cu_tok[lo]);
+    if (pos < 0) continue;
+    const int64_t lp = pos / P;
+    if (lp >= max_pages) continue;
+    const int32_t page = block_tables[(int64_t)lo * max_pages + lp];
+    if (page < 0 || page >= NP) continue;
+    const int64_t slot = ((int64_t)page * Hkv + kv) * P + (pos - lp * P);
+    if ((lane & 1) == 0) words[slot * (kD / 8) + (lane >> 1)] = word;
+    if (lane == 0) norms[slot] = __float2half_rn(rho);
   }
-  const int64_t pos = (int64_t)start_pos[lo] + (row - cu_tok[lo]);
-  if (pos < 0) return;
-  const int64_t lp = pos / P;
-  if (lp >= max_pages) return;
-  const int32_t page = block_tables[(int64_t)lo * max_pages + lp];
-  if (page < 0 || page >= NP) return;
-  const int64_t slot = ((int64_t)page * Hkv + kv) * P + (pos - lp * P);
-  if ((lane & 1) == 0) words[slot * (kD / 8) + (lane >> 1)] = word;
-  if (lane == 0) norms[slot] = __float2half_rn(rho);
 }
 
 }  // namespace
@@ -119,7 +142,8 @@ hipError_t launch_tq4_encode(const jf_kv_layout& L, void* words, void* norms, co
                              const int32_t* start_pos, const int32_t* block_tables, int32_t B,
                              int32_t max_pages, int32_t total_tok, hipStream_t stream) {
   const int64_t n_vec = (int64_t)total_tok * L.num_kv_heads;
-  const int64_t blocks = (n_vec + kWavesPerBlock - 1) / kWavesPerBlock;
+  constexpr int kPerBlock = kWavesPerBlock * kVecPerWave;
+  const int64_t blocks = (n_vec + kPerBlock - 1) / kPerBlock;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
   hipLaunchKernelGGL(tq4_encode_kernel, dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0,
                      stream, static_cast<uint32_t*>(words), static_cast<__half*>(norms),
