@@ -11,7 +11,7 @@
 // Walsh-Hadamard transform takes the first two of its eight butterfly stages
 // inside each lane (element index bits 0 and 1) and the other six across
 // lanes (index bits 2..7 are lane bits 0..5), with one exchange per stage and
-// value.  The norm is a wave-wide sum of squares: IEEE addition commutes, so
+// value (DPP, swizzle or lane permute: no LDS addresses).  The norm is a wave-wide sum of squares: IEEE addition commutes, so
 // every lane of the butterfly reduction ends with the same sum.
 //
 // Index of a coordinate: the number of midpoint thresholds between adjacent
@@ -36,6 +36,35 @@ constexpr int kLevels = 16;
 
 __device__ __forceinline__ float2 h2_to_f2(uint32_t u) {
   return __half22float2(__builtin_bit_cast(__half2, u));
+}
+
+// The value of lane ^ M (M = 1 .. 32) of the same wave: a DPP quad
+// permutation for M = 1, 2 (a VALU move), a bit-mask swizzle within each
+// 32-lane half for M = 4, 8, 16, a lane permute for M = 32.
+template <int M>
+__device__ __forceinline__ float xor_lane(float v) {
+  const int i = __builtin_bit_cast(int, v);
+  if constexpr (M == 1)
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(i, 0xB1, 0xF, 0xF, true));
+  else if constexpr (M == 2)
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(i, 0x4E, 0xF, 0xF, true));
+  else if constexpr (M < 32)
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(i, (M << 10) | 0x1F));
+  else
+    return __shfl_xor(v, M, 64);
+}
+
+// One cross-lane butterfly stage on lane bit log2(M): the lane with the bit
+// set takes partner - own, the other own + partner (an fma by +-1 is exact).
+template <int M>
+__device__ __forceinline__ void stage(float& e0, float& e1, float& e2, float& e3, int lane) {
+  const float sg = (lane & M) ? -1.0f : 1.0f;
+  const float p0 = xor_lane<M>(e0), p1 = xor_lane<M>(e1);
+  const float p2 = xor_lane<M>(e2), p3 = xor_lane<M>(e3);
+  e0 = fmaf(sg, e0, p0);
+  e1 = fmaf(sg, e1, p1);
+  e2 = fmaf(sg, e2, p2);
+  e3 = fmaf(sg, e3, p3);
 }
 
 __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
@@ -63,11 +92,6 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
   for (int v = 0; v < kVecPerWave; ++v)
     if (v < nv) raw[v] = __builtin_nontemporal_load(&xw[(vec0 + v) * (kD / 4) + lane]);
   const float4 s = reinterpret_cast<const float4*>(signs)[lane];
-  // butterfly sign of each cross-lane stage: the lane with the index bit set
-  // takes partner - own, the other own + partner (fma by +-1 is exact)
-  float sg[6];
-#pragma unroll
-  for (int k = 0; k < 6; ++k) sg[k] = (lane >> k) & 1 ? -1.0f : 1.0f;
 
 #pragma unroll
   for (int v = 0; v < kVecPerWave; ++v) {
@@ -77,8 +101,12 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
 
     // norm: squares of fp16 values are exact in float32
     float ss = f01.x * f01.x + f01.y * f01.y + f23.x * f23.x + f23.y * f23.y;
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+    ss += xor_lane<32>(ss);
+    ss += xor_lane<16>(ss);
+    ss += xor_lane<8>(ss);
+    ss += xor_lane<4>(ss);
+    ss += xor_lane<2>(ss);
+    ss += xor_lane<1>(ss);
     const float rho = sqrtf(ss);
 
     // H_256 S x: two stages in the lane, six across lanes
@@ -87,16 +115,12 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
       const float a0 = e0 + e1, a1 = e0 - e1, a2 = e2 + e3, a3 = e2 - e3;
       e0 = a0 + a2; e1 = a1 + a3; e2 = a0 - a2; e3 = a1 - a3;
     }
-#pragma unroll
-    for (int k = 0; k < 6; ++k) {
-      const int m = 1 << k;
-      const float p0 = __shfl_xor(e0, m, 64), p1 = __shfl_xor(e1, m, 64);
-      const float p2 = __shfl_xor(e2, m, 64), p3 = __shfl_xor(e3, m, 64);
-      e0 = fmaf(sg[k], e0, p0);
-      e1 = fmaf(sg[k], e1, p1);
-      e2 = fmaf(sg[k], e2, p2);
-      e3 = fmaf(sg[k], e3, p3);
-    }
+    stage<1>(e0, e1, e2, e3, lane);
+    stage<2>(e0, e1, e2, e3, lane);
+    stage<4>(e0, e1, e2, e3, lane);
+    stage<8>(e0, e1, e2, e3, lane);
+    stage<16>(e0, e1, e2, e3, lane);
+    stage<32>(e0, e1, e2, e3, lane);
     // rotated unit vector y = H S x / (16 rho), by one rounded reciprocal
     const float inv = rho > 0.0f ? __fdiv_rn(1.0f, rho * 16.0f) : 0.0f;
     const float y[4] = {e0 * inv, e1 * inv, e2 * inv, e3 * inv};
@@ -110,7 +134,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
       q |= (uint32_t)idx << (4 * j);
     }
     // word w = elements 8w .. 8w + 7: lanes 2w (low half) and 2w + 1
-    const uint32_t partner = (uint32_t)__shfl_xor((int)q, 1, 64);
+    const uint32_t partner = __builtin_bit_cast(uint32_t, xor_lane<1>(__builtin_bit_cast(float, q)));
     const uint32_t word = q | (partner << 16);
 
     // request of this row and its logical position
