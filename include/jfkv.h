@@ -323,9 +323,10 @@ jf_status jf_tq4_pool_bytes(const jf_kv_layout* layout, size_t* words_bytes,
  * Norm: the float32 Euclidean norm, rounded to fp16.  Index of a coordinate:
  * the number of thresholds (c_j + c_{j+1}) / 2 (float32) it strictly exceeds.
  * A zero vector gets norm 0 and the indices of coordinate 0.
- * Errors: NULL or misaligned pointers, B or max_pages <= 0, total_tok < 0
- * -> JF_ERR_INVALID; head_dim != 256 -> JF_ERR_UNSUPPORTED; no launch on
- * error. */
+ * Errors: NULL or misaligned pointers, B or max_pages <= 0, total_tok < 0,
+ * max_pages * page_size above INT32_MAX -> JF_ERR_INVALID; head_dim != 256
+ * or total_tok * num_kv_heads above INT32_MAX -> JF_ERR_UNSUPPORTED; no
+ * launch on error. */
 jf_status jf_tq4_encode_append(const jf_kv_layout* layout, void* words,
                                void* norms, const void* x, const float* signs,
                                const float* centroids, const int32_t* cu_tok,

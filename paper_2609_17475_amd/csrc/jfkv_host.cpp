@@ -499,6 +499,10 @@ jf_status jf_tq4_encode_append(const jf_kv_layout* layout, void* words, void* no
     return fail(JF_ERR_INVALID, "B and max_pages must be positive, total_tok >= 0");
   if (!words || !norms) return fail(JF_ERR_INVALID, "NULL pool pointer");
   if (total_tok == 0) return ok();
+  if ((int64_t)total_tok * layout->num_kv_heads > INT32_MAX)
+    return fail(JF_ERR_UNSUPPORTED, "total_tok * num_kv_heads above INT32_MAX vectors");
+  if ((int64_t)max_pages * layout->page_size > INT32_MAX)
+    return fail(JF_ERR_INVALID, "max_pages * page_size overflows int32");
   if (!x || !signs || !centroids || !cu_tok || !start_pos || !block_tables)
     return fail(JF_ERR_INVALID, "NULL device pointer");
   if (((uintptr_t)x & 7) || ((uintptr_t)signs & 15) || ((uintptr_t)words & 3) ||

@@ -72,7 +72,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
     const float* __restrict__ signs, const float* __restrict__ centroids,
     const int32_t* __restrict__ cu_tok, const int32_t* __restrict__ start_pos,
     const int32_t* __restrict__ block_tables, int B, int max_pages, int Hkv, int P, int NP,
-    int64_t n_vec) {
+    int n_vec) {
   // thresholds for a 4-step binary search: entry 15 is +inf (never passed)
   __shared__ float thr[kLevels];
   if (threadIdx.x < kLevels)
@@ -82,21 +82,24 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
-  const int64_t vec0 = ((int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6)) * kVecPerWave;
+  // wave-uniform from here to the stores: the vector, its request, page and
+  // slot are scalar values (the host bounds n_vec by INT32_MAX)
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int vec0 = ((int)blockIdx.x * kWavesPerBlock + wave) * kVecPerWave;
   if (vec0 >= n_vec) return;  // the whole wave
-  const int nv = (int)min<int64_t>(kVecPerWave, n_vec - vec0);
+  const int nv = min(kVecPerWave, n_vec - vec0);
 
   const uint64_t* xw = reinterpret_cast<const uint64_t*>(x);
   uint64_t raw[kVecPerWave];
 #pragma unroll
   for (int v = 0; v < kVecPerWave; ++v)
-    if (v < nv) raw[v] = __builtin_nontemporal_load(&xw[(vec0 + v) * (kD / 4) + lane]);
+    if (v < nv) raw[v] = __builtin_nontemporal_load(&xw[(int64_t)(vec0 + v) * (kD / 4) + lane]);
   const float4 s = reinterpret_cast<const float4*>(signs)[lane];
 
 #pragma unroll
   for (int v = 0; v < kVecPerWave; ++v) {
     if (v >= nv) break;
-    const int64_t vec = vec0 + v;
+    const int vec = vec0 + v;
     const float2 f01 = h2_to_f2((uint32_t)raw[v]), f23 = h2_to_f2((uint32_t)(raw[v] >> 32));
 
     // norm: squares of fp16 values are exact in float32
@@ -138,20 +141,19 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
     const uint32_t word = q | (partner << 16);
 
     // request of this row and its logical position
-    const int64_t row = vec / Hkv;
-    const int kv = (int)(vec - row * Hkv);
+    const int row = vec / Hkv;
+    const int kv = vec - row * Hkv;
     int32_t lo = 0, hi = B;  // largest b with cu_tok[b] <= row
     while (hi - lo > 1) {
       const int32_t mid = (lo + hi) >> 1;
       if (cu_tok[mid] <= row) lo = mid; else hi = mid;
     }
     const int64_t pos = (int64_t)start_pos[lo] + (row - cu_tok[lo]);
-    if (pos < 0) continue;
-    const int64_t lp = pos / P;
-    if (lp >= max_pages) continue;
+    if (pos < 0 || pos >= (int64_t)max_pages * P) continue;
+    const int lp = (int)pos / P;
     const int32_t page = block_tables[(int64_t)lo * max_pages + lp];
     if (page < 0 || page >= NP) continue;
-    const int64_t slot = ((int64_t)page * Hkv + kv) * P + (pos - lp * P);
+    const int64_t slot = ((int64_t)page * Hkv + kv) * P + ((int)pos - lp * P);
     if ((lane & 1) == 0) words[slot * (kD / 8) + (lane >> 1)] = word;
     if (lane == 0) norms[slot] = __float2half_rn(rho);
   }
@@ -168,11 +170,12 @@ hipError_t launch_tq4_encode(const jf_kv_layout& L, void* words, void* norms, co
   const int64_t n_vec = (int64_t)total_tok * L.num_kv_heads;
   constexpr int kPerBlock = kWavesPerBlock * kVecPerWave;
   const int64_t blocks = (n_vec + kPerBlock - 1) / kPerBlock;
-  if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+  if (n_vec > 0x7fffffffLL) return hipErrorInvalidValue;
   hipLaunchKernelGGL(tq4_encode_kernel, dim3((unsigned)blocks), dim3(64 * kWavesPerBlock), 0,
                      stream, static_cast<uint32_t*>(words), static_cast<__half*>(norms),
                      static_cast<const uint2*>(x), signs, centroids, cu_tok, start_pos,
-                     block_tables, B, max_pages, L.num_kv_heads, L.page_size, L.num_pages, n_vec);
+                     block_tables, B, max_pages, L.num_kv_heads, L.page_size, L.num_pages,
+                     (int)n_vec);
   return hipGetLastError();
 }
 
