@@ -131,10 +131,17 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
     uint32_t q = 0;  // four 4-bit indices: element 4 lane + j at bits 4j
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      int idx = 0;  // number of thresholds strictly below y[j]
+      // off = 4 x the number of thresholds strictly below y[j] found so far
+      // (a byte offset, so each level's read takes its constant part as the
+      // instruction's offset)
+      int off = 0;
 #pragma unroll
-      for (int step = 8; step >= 1; step >>= 1) idx += y[j] > thr[idx + step - 1] ? step : 0;
-      q |= (uint32_t)idx << (4 * j);
+      for (int step = 8; step >= 1; step >>= 1) {
+        const float t = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(thr) + off +
+                                                        4 * (step - 1));
+        off += y[j] > t ? 4 * step : 0;
+      }
+      q |= (uint32_t)(off >> 2) << (4 * j);
     }
     // word w = elements 8w .. 8w + 7: lanes 2w (low half) and 2w + 1
     const uint32_t partner = __builtin_bit_cast(uint32_t, xor_lane<1>(__builtin_bit_cast(float, q)));
