@@ -5,7 +5,7 @@
 // u32 word and stored with the fp16 norm at the vector's page slot
 // (Appendix A, Table codec; Background, page table).
 //
-// One wave per vector at a time, four vectors per wave (their loads issued
+// One wave per vector at a time, eight vectors per wave (their loads issued
 // together).  Lane l holds elements 4l .. 4l + 3 (one 8-byte load: the 64
 // lanes read the vector's 512 bytes in one coalesced access).  The
 // Walsh-Hadamard transform takes the first two of its eight butterfly stages
@@ -31,7 +31,7 @@ namespace {
 
 constexpr int kD = 256;          // head dimension of the format
 constexpr int kWavesPerBlock = 4;
-constexpr int kVecPerWave = 4;   // vectors per wave, their loads issued together
+constexpr int kVecPerWave = 8;   // vectors per wave, their loads issued together
 constexpr int kLevels = 16;
 
 __device__ __forceinline__ float2 h2_to_f2(uint32_t u) {
