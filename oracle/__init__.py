@@ -65,6 +65,8 @@ def lib():
             L.jfo_float_to_half.restype = ctypes.c_uint16
             L.jfo_quantize_group.argtypes = [P, i32, P, P, P]
             L.jfo_quantize_group.restype = None
+            L.jfo_quantize_groups.argtypes = [P, ctypes.c_int64, i32, P, P, P]
+            L.jfo_quantize_groups.restype = None
             L.jfo_codes_bytes.argtypes = [P]
             L.jfo_codes_bytes.restype = ctypes.c_size_t
             L.jfo_meta_elems.argtypes = [P]
@@ -124,6 +126,17 @@ def quantize_group(x: np.ndarray):
     b = np.zeros(1, np.uint16)
     lib().jfo_quantize_group(_ptr(x), G, _ptr(codes), _ptr(s), _ptr(b))
     return codes, s.view(np.float16)[0], b.view(np.float16)[0]
+
+
+def quantize_groups(x: np.ndarray):
+    """x: fp16 [n][G] -> (codes uint8 [n][G], scales fp16 [n], biases fp16 [n])."""
+    x = _u16(x)
+    n, G = x.shape
+    codes = np.zeros((n, G), np.uint8)
+    s = np.zeros(n, np.uint16)
+    b = np.zeros(n, np.uint16)
+    lib().jfo_quantize_groups(_ptr(x), n, G, _ptr(codes), _ptr(s), _ptr(b))
+    return codes, s.view(np.float16), b.view(np.float16)
 
 
 class Pool:

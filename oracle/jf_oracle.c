@@ -141,6 +141,12 @@ void jfo_quantize_group(const uint16_t* x, int32_t G, uint8_t* codes,
   }
 }
 
+void jfo_quantize_groups(const uint16_t* x, int64_t n, int32_t G,
+                         uint8_t* codes, uint16_t* scales, uint16_t* biases) {
+  for (int64_t i = 0; i < n; ++i)
+    jfo_quantize_group(x + i * G, G, codes + i * G, scales + i, biases + i);
+}
+
 /* ------------------------------------------------------------------------
  * Pool layout (jf_oracle.h).  Offsets are in bytes for codes, in fp16
  * elements for meta.

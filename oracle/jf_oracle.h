@@ -52,6 +52,11 @@ uint16_t jfo_float_to_half(float f, int mode);
 void jfo_quantize_group(const uint16_t* x, int32_t G, uint8_t* codes,
                         uint16_t* scale, uint16_t* bias);
 
+/* n consecutive groups: x [n][G] -> codes [n][G], scales [n], biases [n]
+ * (jfo_quantize_group on each; for tests that compare many groups). */
+void jfo_quantize_groups(const uint16_t* x, int64_t n, int32_t G,
+                         uint8_t* codes, uint16_t* scales, uint16_t* biases);
+
 /* ---- pool byte layout ----------------------------------------------------
  * Per layer, one pool each for K and V:
  *   k_codes: uint8 [NP][Hkv][P][d/2]  row-major per position;
