@@ -27,9 +27,19 @@
 //           of lane quarter "slot" (zero elsewhere), so every column belongs
 //           to one scale group; logit = sum over slots of
 //           (scale_g * S^T + bias_g * sum(q over the slot's dims)) * 2^24;
-//   values  O^T[dim][col] += V codes [dim][pos] x W [pos][col] with
+//   values  O^T[dim][col] += (V codes - 8) [dim][pos] x W [pos][col] with
 //           W = p * scale_g (fp16) of the group that column's slot stands
-//           for; the bias part sum(p * bias_g) is accumulated separately.
+//           for; the rest of the value, sum(p * (bias_g + 8 scale_g)), is
+//           accumulated separately in fp32 from the exact products p * bias
+//           and p * scale.  The codes enter centred: where an outlier
+//           channel widens a group's range, the other channels' codes sit
+//           near the middle and scale * code and bias are large and of
+//           opposite sign while the value is small, so uncentred sums would
+//           cancel and the matrix cores' fp32 accumulation (and the fp16
+//           rounding of W) would be amplified by |scale * code| / |o|;
+//           centred, the summands are of the size of the values themselves.
+//           A centred code is formed exactly: the nibble ORed into the
+//           mantissa of 1024 (fp16) minus 1032.
 // Online softmax keeps one running maximum per head; it is raised only when
 // a logit exceeds it by more than 2 (log2 units), so p <= 4 and p * scale
 // stays within fp16 for any scale the quantizer produces (at most 65504 * 2
@@ -155,13 +165,38 @@ __device__ __forceinline__ h8 k_operand(uint32_t w) {
   return __builtin_bit_cast(h8, r);
 }
 // Dim K of a 4-dim chunk at eight positions from four position-pair V words
-// (word r: positions 2r and 2r+1): k-slots in position order; K odd: 16x.
+// (word r: positions 2r and 2r+1), centred: code - 8 (K even) or
+// 16 (code - 8) (K odd: the high nibble of its byte), exact in fp16 (the
+// nibble ORed into 1024.0 gives 1024 + code, or 1024 + 16 code; subtracting
+// 1032, or 1152, is exact); k-slots in position order.  vk holds the masks
+// and the magic number in registers (see opaque), so that mask-and-OR is one
+// v_and_or_b32.
+struct VConsts {
+  uint32_t m_lo, m_hi, magic;
+};
 template <int K>
-__device__ __forceinline__ h8 v_operand(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+__device__ __forceinline__ h8 v_operand(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
+                                        const VConsts& vk) {
   constexpr int SH = (K >= 2) ? 8 : 0;
-  constexpr uint32_t M = (K & 1) ? 0x00F000F0u : 0x000F000Fu;
-  const u32x4 r = {(w0 >> SH) & M, (w1 >> SH) & M, (w2 >> SH) & M, (w3 >> SH) & M};
-  return __builtin_bit_cast(h8, r);
+  const uint32_t M = (K & 1) ? vk.m_hi : vk.m_lo;
+  constexpr _Float16 kOff = (K & 1) ? (_Float16)1152.0f : (_Float16)1032.0f;
+  const h2 off = {kOff, kOff};
+  const uint32_t ws[4] = {w0, w1, w2, w3};
+  h8 r;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const h2 c = as_h2(((ws[j] >> SH) & M) | vk.magic) - off;
+    r[2 * j] = c.x;
+    r[2 * j + 1] = c.y;
+  }
+  return r;
+}
+// A value the compiler cannot see through (no instruction is emitted): a
+// constant passed through it stays in a register instead of being folded
+// into a literal operand.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
 }
 // f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>), in order.
 template <int N, int I = 0, typename F>
@@ -657,6 +692,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   constexpr int NGH = HD / G;            // scale groups per half
   const int gcol = gs % NGH;             // group (within a half) of the score column
   const bool q_on = head_on && (DQ * q4) / G == gcol;
+  // a negative softmax scale negates the query (exact) and leaves |scale|
+  const uint32_t qneg = scale_log2 < 0.0f ? 0x80008000u : 0u;
   h8 qB[NHALF][WQ];
   float qs[NHALF];
 #pragma unroll
@@ -665,7 +702,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
 #pragma unroll
     for (int kb = 0; kb < WQ; ++kb) {
       const uint4 u = qraw[e][kb];
-      const uint32_t wq[4] = {u.x, u.y, u.z, u.w};
+      const uint32_t wq[4] = {u.x ^ qneg, u.y ^ qneg, u.z ^ qneg, u.w ^ qneg};
       _Float16 x[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -688,7 +725,9 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
       if ((DQ * (q4 ^ k)) / G == gcol) g += sq[k];
     qs[e] = head_on ? g * (1.0f / 16777216.0f) : 0.0f;
   }
-  const float kfold = 16777216.0f * scale_log2;  // 2^24: the code scale
+  // 2^24 (the code scale) times |scale| in log2 units; a positive floor keeps
+  // masked (-inf) scores at -inf when the scale is 0
+  const float kfold = 16777216.0f * fmaxf(fabsf(scale_log2), 1e-30f);
 
   f32x4 acc_o[NC][4];
 #pragma unroll
@@ -696,9 +735,9 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
 #pragma unroll
     for (int k = 0; k < 4; ++k) acc_o[c][k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   float m_run = kMinit, thr = kMinit, l_run = 0.0f;
-  float bacc[NHALF];
+  float bacc[NHALF], sacc8[NHALF];  // sums of p * bias and of p * scale (value groups)
 #pragma unroll
-  for (int e = 0; e < NHALF; ++e) bacc[e] = 0.0f;
+  for (int e = 0; e < NHALF; ++e) bacc[e] = sacc8[e] = 0.0f;
 
   // LDS read bases (stage 0)
   const int p0 = 8 * (l16 >> 2) + (l16 & 3);  // tile-0 position of row m = l16
@@ -725,6 +764,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   int t_row = pb * P + wave * kRowPos;  // first logical position of the row
   int issued_rows = kStages;            // rows whose loads were issued (incl. past the end)
   const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
+  const VConsts vk = {opaque(0x000F000Fu), opaque(0x00F000F0u), opaque(0x64006400u)};
   auto row = [&](auto st_c) {
     constexpr int ST = decltype(st_c)::value;
     constexpr int OFF = ST * kStageBytes;
@@ -834,9 +874,12 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         for (int e = 0; e < NHALF; ++e) a = fold_meta(kmw[e][t][i], sacc[e][t][i], qs[e], a);
         if constexpr (NGH >= 2) a = row_ror_add<4>(a);
         if constexpr (NGH >= 4) a = row_ror_add<8>(a);
-        sc[t][i] = a * kfold;
+        sc[t][i] = a;  // (scaled by kfold in the exponent)
       }
     if (!full) {
+      // (an empty volatile statement keeps this a branch: the compiler would
+      // otherwise compute the masks as selects on every row)
+      asm volatile("" ::: "memory");
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -847,8 +890,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
           for (int e = 0; e < NHALF; ++e) vmw[e][t][i] = ok ? vmw[e][t][i] : 0u;
         }
     }
-    const float mx = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
-                           fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
+    const float mx = kfold * fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
+                                   fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
     if (__builtin_amdgcn_ballot_w64(mx > thr) != 0) {
       // new running maximum of the head: lanes with equal lane % 4
       const float M = xor_max_from(mx, 4);
@@ -858,7 +901,10 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         thr = M + kTau;
         l_run *= alpha;
 #pragma unroll
-        for (int e = 0; e < NHALF; ++e) bacc[e] *= alpha;
+        for (int e = 0; e < NHALF; ++e) {
+          bacc[e] *= alpha;
+          sacc8[e] *= alpha;
+        }
 #pragma unroll
         for (int c = 0; c < NC; ++c)
 #pragma unroll
@@ -870,8 +916,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int t = r >> 1, i = 2 * (r & 1);
-      pk[r] = h2{(_Float16)__builtin_amdgcn_exp2f(sc[t][i] - m_run),
-                 (_Float16)__builtin_amdgcn_exp2f(sc[t][i + 1] - m_run)};
+      pk[r] = h2{(_Float16)__builtin_amdgcn_exp2f(fmaf(sc[t][i], kfold, -m_run)),
+                 (_Float16)__builtin_amdgcn_exp2f(fmaf(sc[t][i + 1], kfold, -m_run))};
       l_run = __builtin_amdgcn_fdot2(pk[r], ones, l_run, false);
     }
     h8 W[NHALF];
@@ -887,16 +933,17 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         W[e][2 * r] = w.x;
         W[e][2 * r + 1] = w.y;
         bacc[e] = __builtin_amdgcn_fdot2(pk[r], bv, bacc[e], false);
+        sacc8[e] = __builtin_amdgcn_fdot2(pk[r], sv, sacc8[e], false);
       }
     }
     // ---- values: O^T += V codes x W, dims 4 (16 c + m) + k
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const h8 w = W[c >> 1 < NHALF ? c >> 1 : 0];
-      acc_o[c][0] = mfma(v_operand<0>(vw[c][0], vw[c][1], vw[c][2], vw[c][3]), w, acc_o[c][0]);
-      acc_o[c][1] = mfma(v_operand<1>(vw[c][0], vw[c][1], vw[c][2], vw[c][3]), w, acc_o[c][1]);
-      acc_o[c][2] = mfma(v_operand<2>(vw[c][0], vw[c][1], vw[c][2], vw[c][3]), w, acc_o[c][2]);
-      acc_o[c][3] = mfma(v_operand<3>(vw[c][0], vw[c][1], vw[c][2], vw[c][3]), w, acc_o[c][3]);
+      acc_o[c][0] = mfma(v_operand<0>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vk), w, acc_o[c][0]);
+      acc_o[c][1] = mfma(v_operand<1>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vk), w, acc_o[c][1]);
+      acc_o[c][2] = mfma(v_operand<2>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vk), w, acc_o[c][2]);
+      acc_o[c][3] = mfma(v_operand<3>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vk), w, acc_o[c][3]);
     }
     t_row += kWaves * kRowPos;
   };
@@ -924,8 +971,13 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     float bsum[NHALF];
 #pragma unroll
     for (int e = 0; e < NHALF; ++e) {
-      bsum[e] = bacc[e] + __shfl_xor(bacc[e], 16);
-      bsum[e] += __shfl_xor(bsum[e], 32);
+      // the value groups' sums of p * (bias + 8 scale): the centred codes'
+      // offset restored with the exact products p * scale
+      float bq = bacc[e] + __shfl_xor(bacc[e], 16);
+      bq += __shfl_xor(bq, 32);
+      float sq8 = sacc8[e] + __shfl_xor(sacc8[e], 16);
+      sq8 += __shfl_xor(sq8, 32);
+      bsum[e] = fmaf(8.0f, sq8, bq);
     }
     float lsum = l_run + __shfl_xor(l_run, 16);
     lsum += __shfl_xor(lsum, 32);
@@ -937,10 +989,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         const float bg = bsum[(c >> 1) < NHALF ? (c >> 1) : 0];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float4 o4 = make_float4(fmaf(acc_o[c][0][i], 16777216.0f, bg),
-                                        fmaf(acc_o[c][1][i], 1048576.0f, bg),
-                                        fmaf(acc_o[c][2][i], 16777216.0f, bg),
-                                        fmaf(acc_o[c][3][i], 1048576.0f, bg));
+          const float4 o4 = make_float4(acc_o[c][0][i] + bg, fmaf(acc_o[c][1][i], 0.0625f, bg),
+                                        acc_o[c][2][i] + bg, fmaf(acc_o[c][3][i], 0.0625f, bg));
           *reinterpret_cast<float4*>(part + hse * D + 4 * (16 * c + 4 * qe + i)) = o4;
         }
       }

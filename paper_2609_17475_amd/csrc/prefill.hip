@@ -21,9 +21,15 @@
 //      k-slots carry (b_g, b_g) x (hi, lo) of the query's fp32 group sums.
 //      Rounding the reconstructed keys to fp16 instead would move the
 //      scores of large-magnitude channels by up to half an fp16 ulp.
-//   V: the tile holds scale * code + bias rounded once to fp16 (one packed
-//      FMA); its rounding enters the output averaged over the keys.
-// The chunk's own rows are fp16 already: K with scale 1 and bias 0, V as is.
+//   V: two tiles hold (scale * code + bias) / 2 as an fp16 high part (one
+//      packed FMA) and an fp16 low part (the high part's rounding error,
+//      from the fp32 value), and each value product runs once per tile;
+//      together they carry the reconstructed value to ~2^-21 relative, and
+//      the halving keeps every group in fp16 range (with the scale rounded
+//      up, bias + 15 * scale may exceed the fp16 maximum by up to 15 ulps
+//      of the scale).  The output is doubled at the end.
+// The chunk's own rows are fp16 already: K with scale 1 and bias 0, V halved
+// (exact but for the last bit of a subnormal), with no low part.
 //
 // Block = 8 waves sharing KV head kv, 32 query rows per wave (16 at d = 256); a row is
 // (chunk position i, query head h of kv), position-major.  Per 64-key tile:
@@ -35,7 +41,8 @@
 //                     tile's maximum exceeds it by more than kTau, so
 //                     p <= 2^kTau stays well inside fp16 and rescaling of
 //                     the accumulators is rare)
-//   O^T += V^T P^T   (A = V^ tile [dim][key] from LDS, B = p as fp16)
+//   O^T += V^T P^T   (A = V^ high and low tiles [dim][key] from LDS,
+//                     B = p as fp16)
 // Accumulator layout (16x16 MFMA): lane l, element r holds row 4*(l/16)+r,
 // column l%16.  Operand k-slots are whatever the hardware pairs between A
 // and B; both sides are filled in the same order.
@@ -52,7 +59,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kKeys = 64;          // keys per tile (a page holds whole tiles)
+// Keys per tile (a page holds whole tiles): 64, or 32 at d = 256, where the
+// double-buffered K and two V tiles of 64 keys would not fit in LDS.
+template <int D>
+constexpr int keys_per_tile() { return D > 128 ? 32 : 64; }
 constexpr float kTau = 8.0f;       // lazy-rescale margin, log2 units
 constexpr float kMinit = -1e30f;   // initial running maximum (finite)
 
@@ -80,8 +90,17 @@ __device__ __forceinline__ int kperm8(int e) { return (e >> 1) + 4 * (e & 1); }
 __device__ __forceinline__ h2 code2(uint32_t w) {
   return as_h2((w & 0x000F000Fu) | 0x64006400u) - h2{(_Float16)1024.0f, (_Float16)1024.0f};
 }
-__device__ __forceinline__ h2 deq2(uint32_t w, h2 s, h2 b) {
-  return __builtin_elementwise_fma(code2(w), s, b);
+// (scale * code + bias) / 2 for the two codes: the high part from the
+// halved scale and bias in one packed fp16 FMA, the low part as the fp16
+// rounding of the exact value's difference from it (the fp32 FMA of fp16
+// operands rounds once, and the difference is exact).
+__device__ __forceinline__ h2 deq2hl(uint32_t w, h2 s, h2 b, h2 sh, h2 bh, h2& lo) {
+  const h2 c = code2(w);
+  const h2 hi = __builtin_elementwise_fma(c, sh, bh);
+  const float t0 = fmaf((float)c.x, (float)s.x, (float)b.x);
+  const float t1 = fmaf((float)c.y, (float)s.y, (float)b.y);
+  lo = h2{(_Float16)fmaf(t0, 0.5f, -(float)hi.x), (_Float16)fmaf(t1, 0.5f, -(float)hi.y)};
+  return hi;
 }
 
 __device__ __forceinline__ f32x4 mfma(h8 a, h8 b, f32x4 c) {
@@ -105,21 +124,25 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
   constexpr int NG = D / G;                // scale groups per vector
   constexpr int KP = D + 16;               // K^ row pitch (fp16; 32 bytes of padding keep the
                                            // 16-byte reads of 16 rows on distinct banks)
-  constexpr int VP = kKeys + 16;           // V^T row pitch (fp16; likewise)
+  constexpr int KT = keys_per_tile<D>();   // keys per tile
+  constexpr int MT = KT / 16;              // 16-key MFMA tiles per tile
+  constexpr int KS = KT / 32;              // 32-key MFMA steps per tile
+  constexpr int VP = KT + 16;              // V^T row pitch (fp16; likewise)
   constexpr int QPK = D / 32;              // 16-byte K code chunks per key
   constexpr int CPV = D / 16;              // 16-byte V code chunks per key pair
-  constexpr int KCH = kKeys * QPK;         // K code chunks per tile
-  constexpr int VCH = (kKeys / 2) * CPV;   // V code chunks per tile
+  constexpr int KCH = KT * QPK;         // K code chunks per tile
+  constexpr int VCH = (KT / 2) * CPV;   // V code chunks per tile
   constexpr int NCH = (KCH + VCH + kThreads - 1) / kThreads;
   static_assert(G >= 32, "a K chunk (32 dims) and a V chunk (16 dims) lie in one group");
 
-  __shared__ __attribute__((aligned(16))) _Float16 sK[2][kKeys][KP];
-  __shared__ __attribute__((aligned(16))) uint32_t sKm[2][NG][kKeys];  // K (scale, bias)
+  __shared__ __attribute__((aligned(16))) _Float16 sK[2][KT][KP];
+  __shared__ __attribute__((aligned(16))) uint32_t sKm[2][NG][KT];  // K (scale, bias)
   // the bias product's K operand per key: slots (2g, 2g+1) of lane group
   // g / 4 hold (b_g, b_g) (groups 0..7; the other slots stay zero)
   constexpr int NBQ = (NG + 3) / 4;
-  __shared__ __attribute__((aligned(16))) uint32_t sKb[2][kKeys][NBQ][4];
-  __shared__ __attribute__((aligned(16))) _Float16 sV[2][D][VP];
+  __shared__ __attribute__((aligned(16))) uint32_t sKb[2][KT][NBQ][4];
+  __shared__ __attribute__((aligned(16))) _Float16 sV[2][D][VP];   // V^ / 2, high part
+  __shared__ __attribute__((aligned(16))) _Float16 sVl[2][D][VP];  // low part (prefix tiles)
 
   // KV head fastest: the blocks of one KV head land on one XCD (round-robin
   // dispatch over the 8 XCDs), so its tiles are shared in that XCD's L2.
@@ -206,8 +229,8 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
 
   const int i_min = r0 / gq;
   const int i_max = min(T - 1, (r0 + kRows - 1) / gq);
-  const int n_pre = (prefix_len + kKeys - 1) / kKeys;
-  const int n_chk = i_max / kKeys + 1;
+  const int n_pre = (prefix_len + KT - 1) / KT;
+  const int n_chk = i_max / KT + 1;
   const int n_tiles = n_pre + n_chk;
 
   // ---- prefix tiles: codes and (scale, bias) words of tile j, one 16-byte
@@ -217,10 +240,10 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
   // lanes, so the transposed LDS stores spread over the banks).
   uint4 pc[NCH];
   uint32_t pm[NCH][2];
-  auto tile_page = [&](int j) { return block_table[(j * kKeys) / P]; };
+  auto tile_page = [&](int j) { return block_table[(j * KT) / P]; };
   auto prefetch = [&](int j, int page) {
     if ((unsigned)page >= (unsigned)NP) return;  // the tile is skipped
-    const int slot0 = (j * kKeys) % P;
+    const int slot0 = (j * KT) % P;
     const size_t run = (size_t)page * Hkv + kv;
 #pragma unroll
     for (int k = 0; k < NCH; ++k) {
@@ -231,7 +254,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
                                                 (size_t)(slot0 + key) * (D / 2) + 16 * qd);
         pm[k][0] = k_meta[(run * P + slot0 + key) * NG + (32 * qd) / G];
       } else if (c < KCH + VCH) {
-        const int cv = c - KCH, pair = cv % (kKeys / 2), u16 = cv / (kKeys / 2);
+        const int cv = c - KCH, pair = cv % (KT / 2), u16 = cv / (KT / 2);
         pc[k] = *reinterpret_cast<const uint4*>(v_codes + run * head_codes +
                                                 (size_t)(slot0 / 2 + pair) * D + 16 * u16);
         const size_t mrow = (run * P + slot0 + 2 * pair) * NG + (16 * u16) / G;
@@ -244,7 +267,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
   // scale and bias 0, so they are exact zeros)
   auto dequant = [&](int j, int page, int b) {
     if ((unsigned)page >= (unsigned)NP) return;
-    const int key0 = j * kKeys;
+    const int key0 = j * KT;
 #pragma unroll
     for (int k = 0; k < NCH; ++k) {
       const int c = tid + k * kThreads;
@@ -268,27 +291,32 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
           sKb[b][key][g >> 2][g & 3] = __builtin_amdgcn_perm(mw, mw, 0x03020302u);
         }
       } else if (c < KCH + VCH) {
-        const int cv = c - KCH, pair = cv % (kKeys / 2), u16 = cv / (kKeys / 2);
+        const int cv = c - KCH, pair = cv % (KT / 2), u16 = cv / (KT / 2);
         const int kk = key0 + 2 * pair;
         const uint32_t ma = (kk < prefix_len) ? pm[k][0] : 0u;
         const uint32_t mb = (kk + 1 < prefix_len) ? pm[k][1] : 0u;
         const h2 s2 = as_h2(__builtin_amdgcn_perm(mb, ma, 0x05040100u));
         const h2 b2 = as_h2(__builtin_amdgcn_perm(mb, ma, 0x07060302u));
+        const h2 half = {(_Float16)0.5f, (_Float16)0.5f};
+        const h2 s2h = s2 * half, b2h = b2 * half;
         const int col = vperm(2 * pair);
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
           const int d0 = 16 * u16 + 4 * m;
-          *reinterpret_cast<uint32_t*>(&sV[b][d0 + 0][col]) = as_u32(deq2(w[m], s2, b2));
-          *reinterpret_cast<uint32_t*>(&sV[b][d0 + 1][col]) = as_u32(deq2(w[m] >> 4, s2, b2));
-          *reinterpret_cast<uint32_t*>(&sV[b][d0 + 2][col]) = as_u32(deq2(w[m] >> 8, s2, b2));
-          *reinterpret_cast<uint32_t*>(&sV[b][d0 + 3][col]) = as_u32(deq2(w[m] >> 12, s2, b2));
+#pragma unroll
+          for (int n = 0; n < 4; ++n) {
+            h2 lo;
+            const h2 hi = deq2hl(w[m] >> (4 * n), s2, b2, s2h, b2h, lo);
+            *reinterpret_cast<uint32_t*>(&sV[b][d0 + n][col]) = as_u32(hi);
+            *reinterpret_cast<uint32_t*>(&sVl[b][d0 + n][col]) = as_u32(lo);
+          }
         }
       }
     }
   };
   // the chunk's own fp16 rows j*64 .. into buffer b (rows past T: zeros)
   auto stage_chunk = [&](int j, int b) {
-    const int key0 = j * kKeys;
+    const int key0 = j * KT;
 #pragma unroll
     for (int k = 0; k < NCH; ++k) {
       const int c = tid + k * kThreads;
@@ -313,7 +341,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
           sKb[b][key][g >> 2][g & 3] = 0u;
         }
       } else if (c < KCH + VCH) {
-        const int cv = c - KCH, pair = cv % (kKeys / 2), u16 = cv / (kKeys / 2);
+        const int cv = c - KCH, pair = cv % (KT / 2), u16 = cv / (KT / 2);
         const int kk = key0 + 2 * pair;
         const uint4* sa = reinterpret_cast<const uint4*>(v_chunk + ((size_t)kk * Hkv + kv) * D + 16 * u16);
         const uint4* sb = reinterpret_cast<const uint4*>(v_chunk + ((size_t)(kk + 1) * Hkv + kv) * D + 16 * u16);
@@ -324,13 +352,14 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
           const uint4 ub = (kk + 1 < T) ? sb[hv] : make_uint4(0, 0, 0, 0);
           const uint32_t wa[4] = {ua.x, ua.y, ua.z, ua.w};
           const uint32_t wb[4] = {ub.x, ub.y, ub.z, ub.w};
+          const h2 half = {(_Float16)0.5f, (_Float16)0.5f};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int d0 = 16 * u16 + 8 * hv + 2 * e;
             *reinterpret_cast<uint32_t*>(&sV[b][d0][col]) =
-                __builtin_amdgcn_perm(wb[e], wa[e], 0x05040100u);
+                as_u32(as_h2(__builtin_amdgcn_perm(wb[e], wa[e], 0x05040100u)) * half);
             *reinterpret_cast<uint32_t*>(&sV[b][d0 + 1][col]) =
-                __builtin_amdgcn_perm(wb[e], wa[e], 0x07060302u);
+                as_u32(as_h2(__builtin_amdgcn_perm(wb[e], wa[e], 0x07060302u)) * half);
           }
         }
       }
@@ -341,18 +370,18 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
   auto compute = [&](int b, int key0, int key_lim, bool chunk_tile) {
     // bias part first: key 16 mt + l16, slots (2g, 2g+1) = (b_g, b_g) on
     // lanes q4 == g / 4; it seeds the folded scores
-    f32x4 sacc[4][NR];
+    f32x4 sacc[MT][NR];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
+    for (int mt = 0; mt < MT; ++mt) {
       const h8 kb = (q4 < NBQ) ? *reinterpret_cast<const h8*>(&sKb[b][16 * mt + l16][q4 < NBQ ? q4 : 0][0])
                                : h8{};
 #pragma unroll
       for (int n = 0; n < NR; ++n) sacc[mt][n] = mfma(kb, qsum_b[n], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
     }
-    // code products per scale group, scaled in fp32 (two 32-key halves in
-    // turn, to bound the live accumulators)
+    // code products per scale group, scaled in fp32 (32-key halves in turn,
+    // to bound the live accumulators)
 #pragma unroll
-    for (int mh = 0; mh < 2; ++mh) {
+    for (int mh = 0; mh < KS; ++mh) {
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
         f32x4 acc[2][NR];
@@ -387,10 +416,10 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     // them (the scheduler's single-wave MFMA interleaving)
     __builtin_amdgcn_iglp_opt(1);
     // keys past the limit, and (chunk tiles) keys after the row's position
-    const bool need_mask = key0 + kKeys > key_lim || (chunk_tile && key0 + kKeys - 1 > i_min);
+    const bool need_mask = key0 + KT > key_lim || (chunk_tile && key0 + KT - 1 > i_min);
     if (need_mask) {
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int n = 0; n < NR; ++n)
 #pragma unroll
@@ -406,7 +435,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     for (int n = 0; n < NR; ++n) {
       float mx = fmaxf(fmaxf(sacc[0][n][0], sacc[0][n][1]), fmaxf(sacc[0][n][2], sacc[0][n][3]));
 #pragma unroll
-      for (int mt = 1; mt < 4; ++mt)
+      for (int mt = 1; mt < MT; ++mt)
         mx = fmaxf(mx, fmaxf(fmaxf(sacc[mt][n][0], sacc[mt][n][1]),
                              fmaxf(sacc[mt][n][2], sacc[mt][n][3])));
       mx = fmaxf(mx, __shfl_xor(mx, 16));
@@ -429,14 +458,14 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     }
     // p = 2^(s |scale| - m) as fp16; P^T operand of 32-key step k: the
     // lane's keys 4 q4 .. of 16-key tiles 2k and 2k + 1
-    h8 pb[NR][2];
-    u32x4 pw[NR][2];  // the same, as fp16 pairs
+    h8 pb[NR][KS];
+    u32x4 pw[NR][KS];  // the same, as fp16 pairs
     const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
 #pragma unroll
     for (int n = 0; n < NR; ++n) {
       const float mneg = -m_run[n];
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
+      for (int mt = 0; mt < MT; ++mt) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[mt][n][0], cabs, mneg));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[mt][n][1], cabs, mneg));
         const float p2 = __builtin_amdgcn_exp2f(fmaf(sacc[mt][n][2], cabs, mneg));
@@ -452,21 +481,31 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
 #pragma unroll
     for (int n = 0; n < NR; ++n)
 #pragma unroll
-      for (int k = 0; k < 2; ++k) pb[n][k] = __builtin_bit_cast(h8, pw[n][k]);
+      for (int k = 0; k < KS; ++k) pb[n][k] = __builtin_bit_cast(h8, pw[n][k]);
 #pragma unroll
     for (int t = 0; t < DT; ++t)
 #pragma unroll
-      for (int k = 0; k < 2; ++k) {
+      for (int k = 0; k < KS; ++k) {
         const h8 a = *reinterpret_cast<const h8*>(&sV[b][16 * t + l16][32 * k + 8 * q4]);
 #pragma unroll
         for (int n = 0; n < NR; ++n) acc_o[t][n] = mfma(a, pb[n][k], acc_o[t][n]);
       }
+    if (!chunk_tile) {  // the low parts of reconstructed values (block-uniform)
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+          const h8 a = *reinterpret_cast<const h8*>(&sVl[b][16 * t + l16][32 * k + 8 * q4]);
+#pragma unroll
+          for (int n = 0; n < NR; ++n) acc_o[t][n] = mfma(a, pb[n][k], acc_o[t][n]);
+        }
+    }
     // the same interleaving for the value products, the exponentials and the
     // row sums
     __builtin_amdgcn_iglp_opt(1);
   };
 
-  for (int i = tid; i < 2 * kKeys * NBQ * 4; i += kThreads) (&sKb[0][0][0][0])[i] = 0u;
+  for (int i = tid; i < 2 * KT * NBQ * 4; i += kThreads) (&sKb[0][0][0][0])[i] = 0u;
   __syncthreads();
 
   // ---- tiles 0 .. n_pre - 1 (prefix), then the chunk's; double-buffered:
@@ -504,9 +543,9 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     }
     const bool chunk_tile = j >= n_pre;
     if (chunk_tile)
-      compute(b, (j - n_pre) * kKeys, T, true);
+      compute(b, (j - n_pre) * KT, T, true);
     else if ((unsigned)page_buf[b] < (unsigned)NP)  // a tile on an invalid page is skipped
-      compute(b, j * kKeys, prefix_len, false);
+      compute(b, j * KT, prefix_len, false);
     __syncthreads();
   }
 
@@ -519,7 +558,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     float l = l_run[n] + __shfl_xor(l_run[n], 16);
     l += __shfl_xor(l, 32);
     if (i >= T) continue;
-    const float inv = (l > 0.0f) ? 1.0f / l : 0.0f;
+    const float inv = (l > 0.0f) ? 2.0f / l : 0.0f;  // (the value tiles hold V / 2)
     __half* dst = out + ((size_t)i * Hq + kv * gq + hh) * D;
 #pragma unroll
     for (int t = 0; t < DT; ++t) {

@@ -137,16 +137,18 @@ def decode_oracle(case: Case, q: np.ndarray, scale=1.0, lens=None, tables=None):
     return oracle.decode(case.host, q, tables, lens, scale)
 
 
-def check_tol(got16: np.ndarray, ref: np.ndarray, atol=2e-3, rel_l2=2e-3, rel_elem=0.0,
+def check_tol(got16: np.ndarray, ref: np.ndarray, atol=2e-3, rel_l2=1e-3, rel_elem=0.0,
               what=""):
     """|got - ref| <= atol + rel_elem*|ref| elementwise (atol 2e-3 is the bound
     for fp16 outputs with fp32 accumulation), and relative L2 error <= rel_l2.
 
-    The relative L2 cap follows from the decode arithmetic: per position the
-    probability p and the product p * scale are fp16 (relative rounding
-    <= 2^-11, rms 2^-11/sqrt(3) = 2.8e-4 each) and the output is rounded to
-    fp16 once more; three independent roundings give ~4.9e-4 rms relative
-    error, and small flat cases spread to ~1.2e-3 (measured), so 2e-3."""
+    The relative L2 cap of 1e-3 follows from the decode arithmetic: the
+    probabilities p are fp16, but the same rounded p enter the numerator and
+    the denominator, so their rounding only perturbs the weights (relative
+    2^-11 each, averaged over positions); p * scale enters as an fp16 high
+    part plus an fp16 low part (error ~2^-22); biases are summed in fp32; the
+    output is rounded to fp16 once (rms ~2^-11 / sqrt(3) = 2.8e-4 relative).
+    What remains is ~3e-4, so 1e-3 leaves a factor three."""
     got = got16.astype(np.float64)
     err = np.abs(got - ref)
     lim = atol + rel_elem * np.abs(ref)

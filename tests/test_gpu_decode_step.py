@@ -56,7 +56,7 @@ def _setup(P, hkv, d, G, hq, L0, n_steps, B, seed):
     return gpu, host, tables, new_k, new_v
 
 
-def _run_steps(P, hkv, d, G, hq, L0, n_steps, seed, bad=None):
+def _run_steps(P, hkv, d, G, hq, L0, n_steps, seed, bad=None, max_splits=64):
     B = len(L0)
     gpu, host, tables, new_k, new_v = _setup(P, hkv, d, G, hq, L0, n_steps, B, seed)
     # a twin pool for the two-call path
@@ -65,7 +65,8 @@ def _run_steps(P, hkv, d, G, hq, L0, n_steps, seed, bad=None):
         getattr(twin, n).copy_(getattr(gpu, n))
     gtab = torch.from_numpy(tables).to(DEV)
     rng = np.random.default_rng(seed + 7)
-    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(B, hq, d, 64), dtype=torch.uint8, device=DEV)
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(B, hq, d, max_splits), dtype=torch.uint8,
+                     device=DEV)
     ws2 = torch.zeros_like(ws)
     for s in range(n_steps):
         lens = [L + s + 1 for L in L0]
@@ -82,14 +83,14 @@ def _run_steps(P, hkv, d, G, hq, L0, n_steps, seed, bad=None):
         qt = torch.from_numpy(q).to(DEV)
         lt = torch.tensor(lens, dtype=torch.int32, device=DEV)
         out = torch.empty((B, hq, d), dtype=torch.float16, device=DEV)
-        jfkv.jf_decode_step_q4(gpu, kn, vn, qt, use_gtab, lt, 1.0, 64, ws, out)
+        jfkv.jf_decode_step_q4(gpu, kn, vn, qt, use_gtab, lt, 1.0, max_splits, ws, out)
         # two-call path on the twin pool
         out2 = torch.empty_like(out)
         jfkv.jf_kv_quantize_append(twin, kn, vn,
                                    torch.arange(B + 1, dtype=torch.int32, device=DEV),
                                    torch.tensor([L - 1 for L in lens], dtype=torch.int32,
                                                 device=DEV), use_gtab)
-        jfkv.jf_decode_attn_q4(twin, qt, use_gtab, lt, 1.0, 64, ws2, out2)
+        jfkv.jf_decode_attn_q4(twin, qt, use_gtab, lt, 1.0, max_splits, ws2, out2)
         # oracle: append the rows whose page entry is valid, then decode
         for b in range(B):
             if use_tab[b, (lens[b] - 1) // P] >= 0:
@@ -138,3 +139,18 @@ def test_ragged_batch_with_an_invalid_page_entry():
 @pytest.mark.parametrize("d,G", [(64, 32), (128, 32), (128, 128), (256, 64)])
 def test_other_geometries(d, G):
     _run_steps(P=64, hkv=2, d=d, G=G, hq=6, L0=(130,), n_steps=2, seed=6)
+
+
+# One split (max_splits = 1) of 21 to 70 pages: every wave runs many ring
+# cycles, and past 64 pages the split's page IDs take a second group.  A row
+# r of the split is streamed by wave r % 8 into ring stage (r / 8) % 3 (eight
+# waves, three stages at d = 128), so these lengths put the step's row into
+# stages 0, 1 and 2, inside and beyond the first 64 pages (there its page ID
+# is read from the table, not from the wave's current group).
+@pytest.mark.parametrize("L0", [70 * 256 - 1, 65 * 256 - 101, 66 * 256 - 1, 20 * 256 + 5,
+                                40 * 256 + 31])
+def test_long_split_many_ring_cycles(L0):
+    pos = L0
+    log("long split: new row at %d, split row %d, wave %d, stage %d" % (
+        pos, pos // 32, (pos // 32) % 8, (pos // 32 // 8) % 3))
+    _run_steps(P=256, hkv=1, d=128, G=64, hq=4, L0=(L0,), n_steps=2, seed=9, max_splits=1)
