@@ -271,6 +271,32 @@ jf_status jf_decode_step_q4(const jf_kv_layout* layout,
                             void* workspace, size_t workspace_bytes, void* out,
                             hipStream_t stream);
 
+/* jf_decode_step_q4 without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The step's completion counters and
+ * split records live in a device array inside the library: 8 MiB per device
+ * (64 KiB of counters, then records), held until the process ends; its
+ * address is looked up once per device (hipGetSymbolAddress, which
+ * allocates nothing), and the first call on a device also enqueues a small
+ * kernel that zeroes the counters.  The call allocates and frees nothing.
+ * Arguments, outputs and pool writes are those of jf_decode_step_q4 with the
+ * same max_splits (the outputs are bitwise the same).
+ * Limits: B * num_kv_heads * ceil(Gq / 4) <= 16,384 counters and
+ * B * num_q_heads * max_splits * (head_dim + 4) * 4 <= 8,323,072 bytes of
+ * records; larger requests return JF_ERR_INVALID (nothing launched).
+ * Every call on a device shares that device's array and keeps its last
+ * contents: calls that may overlap in time on one device (other streams,
+ * other threads) race and must not be issued. */
+jf_status jf_decode_step_q4_static(const jf_kv_layout* layout,
+                                   const jf_kv_pool_ptrs* pool,
+                                   const void* k_new, const void* v_new,
+                                   const void* q, int32_t B,
+                                   int32_t num_q_heads,
+                                   const int32_t* block_tables,
+                                   int32_t max_pages, const int32_t* seq_lens,
+                                   float softmax_scale, int32_t max_splits,
+                                   void* out, hipStream_t stream);
+
 /* Chunked-prefill attention for one request: query i of the chunk sits at
  * absolute position prefix_len + i and attends to the dequantized prefix
  * positions 0..prefix_len-1 (through block_table) and, causally, to the

@@ -48,10 +48,17 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "jfkv_internal.h"
 #include "jfkv_quant.h"
+
+// Device scratch of the allocation-free decode step (jf_decode_step_q4_static):
+// completion counters, then split records; one copy per device, held until
+// the process ends.  Host code uses the address hipGetSymbolAddress returns,
+// never this name.
+static __device__ __align__(256) uint8_t scratch[jfkv::kStaticScratchBytes];
 
 namespace {
 
@@ -1052,8 +1059,8 @@ template <int D, int G, bool APPEND>
 hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
                     const void* v_new, const void* q,
                     int32_t B, int32_t Hq, const int32_t* bt, int32_t max_pages,
-                    const int32_t* lens, float scale, int32_t max_splits, void* ws, void* out,
-                    hipStream_t stream) {
+                    const int32_t* lens, float scale, int32_t max_splits, uint32_t* tickets,
+                    float* records, void* out, hipStream_t stream) {
   const int gq = Hq / L.num_kv_heads;
   const int n_hchunks = (gq + kHeadSlots - 1) / kHeadSlots;
   // Splits per request: enough blocks for one per CU when one request runs
@@ -1064,9 +1071,6 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
   const int split_cap =
       (int)std::max<int64_t>(1, std::min<int64_t>(max_splits, (jfkv::num_cus() + per_split - 1) / per_split));
   dim3 grid(split_cap, L.num_kv_heads * n_hchunks, B);
-  // completion counters first, then the split records
-  uint32_t* tickets = static_cast<uint32_t*>(ws);
-  float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + jfkv::kDecodeCounterBytes);
   hipLaunchKernelGGL((decode_kernel<D, G, APPEND>), grid, dim3(64 * waves_for<D>()), 0, stream,
                      static_cast<uint8_t*>(pool.k_codes), static_cast<uint32_t*>(pool.k_meta),
                      static_cast<uint8_t*>(pool.v_codes), static_cast<uint32_t*>(pool.v_meta),
@@ -1097,12 +1101,13 @@ int num_cus() {
   return n;
 }
 
-hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
-                         const void* v_new, const void* q, int32_t B, int32_t Hq,
-                         const int32_t* bt, int32_t max_pages, const int32_t* lens, float scale,
-                         int32_t max_splits, void* ws, void* out, hipStream_t stream) {
-#define JF_ARGS L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale, max_splits, ws, out, \
-                stream
+namespace {
+hipError_t dispatch(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
+                    const void* v_new, const void* q, int32_t B, int32_t Hq, const int32_t* bt,
+                    int32_t max_pages, const int32_t* lens, float scale, int32_t max_splits,
+                    uint32_t* tickets, float* records, void* out, hipStream_t stream) {
+#define JF_ARGS L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale, max_splits, tickets, \
+                records, out, stream
 #define JF_CASE(D_, G_)                                              \
   if (L.head_dim == D_ && L.group_size == G_)                        \
     return k_new ? launch_t<D_, G_, true>(JF_ARGS) : launch_t<D_, G_, false>(JF_ARGS);
@@ -1117,6 +1122,70 @@ hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, con
 #undef JF_CASE
 #undef JF_ARGS
   return hipErrorInvalidValue;
+}
+}  // namespace
+
+hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
+                         const void* v_new, const void* q, int32_t B, int32_t Hq,
+                         const int32_t* bt, int32_t max_pages, const int32_t* lens, float scale,
+                         int32_t max_splits, void* ws, void* out, hipStream_t stream) {
+  // completion counters first, then the split records
+  uint32_t* tickets = static_cast<uint32_t*>(ws);
+  float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kDecodeCounterBytes);
+  return dispatch(L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale, max_splits,
+                  tickets, records, out, stream);
+}
+
+// ---- the decode step without a caller workspace: its completion counters
+// and split records live in `scratch`, one copy per device, addressed through
+// hipGetSymbolAddress once per device.  The counters must start at zero: a
+// small fill kernel clears them on the first call on each device (every call
+// that completes leaves them zero again).
+namespace {
+__global__ void zero_words(uint32_t* p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+}  // namespace
+
+hipError_t static_scratch(void** out, bool* first_use) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* ptrs[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  *first_use = ptrs[dev] == nullptr;
+  if (*first_use) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    ptrs[dev] = p;
+  }
+  *out = ptrs[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_decode_static(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
+                                const void* k_new, const void* v_new, const void* q, int32_t B,
+                                int32_t Hq, const int32_t* bt, int32_t max_pages,
+                                const int32_t* lens, float scale, int32_t max_splits, void* out,
+                                hipStream_t stream) {
+  void* base = nullptr;
+  bool first = false;
+  hipError_t e = static_scratch(&base, &first);
+  if (e != hipSuccess) return e;
+  uint32_t* tickets = static_cast<uint32_t*>(base);
+  float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(base) + kStaticTicketBytes);
+  if (first) {
+    hipLaunchKernelGGL(zero_words, dim3(16), dim3(256), 0, stream, tickets,
+                       (int)(kStaticTicketBytes / sizeof(uint32_t)));
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return dispatch(L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale, max_splits,
+                  tickets, records, out, stream);
 }
 
 }  // namespace jfkv

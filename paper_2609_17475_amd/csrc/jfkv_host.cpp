@@ -375,6 +375,32 @@ jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads, int32_t head
 
 namespace {
 
+// Arguments every decode entry point shares (everything but the workspace).
+jf_status check_decode_args(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                            const void* q, int32_t B, int32_t num_q_heads,
+                            const int32_t* block_tables, int32_t max_pages,
+                            const int32_t* seq_lens, float softmax_scale, int32_t max_splits,
+                            void* out) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if ((st = check_pool(pool))) return st;
+  if (!q || !block_tables || !seq_lens || !out)
+    return fail(JF_ERR_INVALID, "NULL device pointer");
+  if (B <= 0 || num_q_heads <= 0 || max_pages <= 0)
+    return fail(JF_ERR_INVALID, "B, num_q_heads and max_pages must be positive");
+  if (num_q_heads % layout->num_kv_heads)
+    return fail(JF_ERR_INVALID, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                num_q_heads, layout->num_kv_heads);
+  if ((int64_t)max_pages * layout->page_size > INT32_MAX)
+    return fail(JF_ERR_INVALID, "max_pages * page_size overflows int32");
+  if (max_splits <= 0 || max_splits > 1024)
+    return fail(JF_ERR_INVALID, "max_splits must be 1..1024");
+  if (!(softmax_scale == softmax_scale) || softmax_scale == INFINITY ||
+      softmax_scale == -INFINITY)
+    return fail(JF_ERR_INVALID, "softmax_scale must be finite");
+  return ok();
+}
+
 jf_status decode_common(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
                         const void* k_new, const void* v_new, const void* q, int32_t B,
                         int32_t num_q_heads, const int32_t* block_tables, int32_t max_pages,
@@ -429,6 +455,35 @@ jf_status jf_decode_step_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* p
   return decode_common(layout, pool, k_new, v_new, q, B, num_q_heads, block_tables, max_pages,
                        seq_lens, softmax_scale, max_splits, workspace, workspace_bytes, out,
                        stream);
+}
+
+jf_status jf_decode_step_q4_static(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                                   const void* k_new, const void* v_new, const void* q,
+                                   int32_t B, int32_t num_q_heads, const int32_t* block_tables,
+                                   int32_t max_pages, const int32_t* seq_lens,
+                                   float softmax_scale, int32_t max_splits, void* out,
+                                   hipStream_t stream) {
+  if (!k_new || !v_new) return fail(JF_ERR_INVALID, "NULL device pointer");
+  jf_status st = check_decode_args(layout, pool, q, B, num_q_heads, block_tables, max_pages,
+                                   seq_lens, softmax_scale, max_splits, out);
+  if (st) return st;
+  const int64_t gq = num_q_heads / layout->num_kv_heads;
+  const int64_t tickets = (int64_t)B * layout->num_kv_heads * ((gq + 3) / 4);
+  const int64_t records = (int64_t)B * num_q_heads * max_splits * (layout->head_dim + 4) *
+                          (int64_t)sizeof(float);
+  const int64_t room = (int64_t)(jfkv::kStaticScratchBytes - jfkv::kStaticTicketBytes);
+  if (tickets > jfkv::kStaticTickets || records > room)
+    return fail(JF_ERR_INVALID,
+                "jf_decode_step_q4_static: B = %d, num_q_heads = %d, max_splits = %d need %lld "
+                "counters and %lld bytes of split records; the static scratch holds %lld "
+                "counters and %lld bytes (use jf_decode_step_q4 with a workspace)",
+                B, num_q_heads, max_splits, (long long)tickets, (long long)records,
+                (long long)jfkv::kStaticTickets, (long long)room);
+  return device_status(jfkv::launch_decode_static(*layout, *pool, k_new, v_new, q, B,
+                                                  num_q_heads, block_tables, max_pages,
+                                                  seq_lens, softmax_scale, max_splits, out,
+                                                  stream),
+                       "decode launch (static scratch)");
 }
 
 jf_status jf_prefill_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,

@@ -21,6 +21,14 @@ inline size_t decode_workspace_bytes(int32_t B, int32_t Hq, int32_t head_dim, in
   return kDecodeCounterBytes + (size_t)B * Hq * max_splits * (head_dim + 4) * sizeof(float);
 }
 
+// Allocation-free decode step: a device array of kStaticScratchBytes per
+// device, its first kStaticTicketBytes completion counters (room for
+// B * Hkv * ceil(Gq / 4) <= kStaticTickets), then split records
+// [B][Hq][max_splits][d + 4] fp32.
+constexpr size_t kStaticScratchBytes = (size_t)8 << 20;
+constexpr size_t kStaticTicketBytes = 65536;
+constexpr int64_t kStaticTickets = (int64_t)(kStaticTicketBytes / sizeof(uint32_t));
+
 // Compute units of the current device (queried once per device).
 int num_cus();
 
@@ -45,6 +53,14 @@ hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
                          const int32_t* seq_lens, float softmax_scale,
                          int32_t max_splits, void* workspace, void* out,
                          hipStream_t stream);
+
+// The same step with its counters and records in the library's static
+// device array (the caller passes no workspace).
+hipError_t launch_decode_static(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
+                                const void* k_new, const void* v_new, const void* q, int32_t B,
+                                int32_t num_q_heads, const int32_t* block_tables,
+                                int32_t max_pages, const int32_t* seq_lens, float softmax_scale,
+                                int32_t max_splits, void* out, hipStream_t stream);
 
 hipError_t launch_prefill(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
                           const void* q, const void* k_chunk, const void* v_chunk,

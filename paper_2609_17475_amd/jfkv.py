@@ -27,7 +27,8 @@ EXPORTS = [
     "jf_page_table_set_length", "jf_page_table_release", "jf_page_table_export",
     "jf_page_table_stats", "jf_page_table_info",
     "jf_kv_quantize_append", "jf_decode_workspace_bytes", "jf_decode_attn_q4",
-    "jf_decode_step_q4", "jf_prefill_attn_q4", "jf_tq4_pool_bytes", "jf_tq4_encode_append",
+    "jf_decode_step_q4", "jf_decode_step_q4_static", "jf_prefill_attn_q4",
+    "jf_tq4_pool_bytes", "jf_tq4_encode_append",
 ]
 
 
@@ -81,6 +82,8 @@ def _load():
                                    P]),
         "jf_decode_step_q4": (st, [P, P, P, P, P, i32, i32, P, i32, P, ctypes.c_float, i32, P, sz,
                                    P, P]),
+        "jf_decode_step_q4_static": (st, [P, P, P, P, P, i32, i32, P, i32, P, ctypes.c_float,
+                                          i32, P, P]),
         "jf_prefill_attn_q4": (st, [P, P, P, P, P, i32, i32, P, i32, i32, ctypes.c_float, P, P]),
         "jf_tq4_pool_bytes": (st, [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
         "jf_tq4_encode_append": (st, [P, P, P, P, P, P, P, P, P, i32, i32, i32, P]),
@@ -312,6 +315,33 @@ def jf_decode_step_q4(pool: KVPool, k_new, v_new, q, block_tables, seq_lens,
                                  _ptr(seq_lens), float(softmax_scale), int(max_splits),
                                  _ptr(workspace), workspace.numel() * workspace.element_size(),
                                  _ptr(out), _stream(stream)))
+
+
+def jf_decode_step_q4_static(pool: KVPool, k_new, v_new, q, block_tables, seq_lens,
+                             softmax_scale: float, max_splits: int, out, stream=None):
+    """jf_decode_step_q4 with the library's static device scratch in place of a
+    workspace (for callers that cannot allocate); see include/jfkv.h."""
+    import torch
+    _dev_check(k_new, "k_new", torch.float16)
+    _dev_check(v_new, "v_new", torch.float16)
+    _dev_check(q, "q", torch.float16)
+    _dev_check(block_tables, "block_tables", torch.int32)
+    _dev_check(seq_lens, "seq_lens", torch.int32)
+    _dev_check(out, "out", torch.float16)
+    lay = pool.layout
+    B, Hq, d = q.shape
+    if d != lay.head_dim or out.shape != q.shape:
+        raise ValueError("q/out must be [B][Hq][head_dim]")
+    if tuple(k_new.shape) != (B, lay.num_kv_heads, d) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [B][Hkv][head_dim]")
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("block_tables [B][max_pages], seq_lens [B]")
+    ptrs = pool.ptrs()
+    _check(lib.jf_decode_step_q4_static(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(k_new),
+                                        _ptr(v_new), _ptr(q), B, Hq, _ptr(block_tables),
+                                        block_tables.shape[1], _ptr(seq_lens),
+                                        float(softmax_scale), int(max_splits), _ptr(out),
+                                        _stream(stream)))
 
 
 def _check_prefill_args(pool: KVPool, q, k_chunk, v_chunk, block_table, out):
