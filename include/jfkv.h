@@ -346,7 +346,9 @@ jf_status jf_tq4_pool_bytes(const jf_kv_layout* layout, size_t* words_bytes,
  *                position start_pos[b] + i; rows whose position falls outside
  *                the table or whose page ID is outside [0, num_pages) are
  *                not written)
- * Norm: the float32 Euclidean norm, rounded to fp16.  Index of a coordinate:
+ * Norm: the float32 Euclidean norm, rounded to fp16 (+inf when the norm
+ * exceeds the fp16 range, i.e. |x| >= 65520; such vectors are out of range
+ * for decode).  Index of a coordinate:
  * the number of thresholds (c_j + c_{j+1}) / 2 (float32) it strictly exceeds.
  * A zero vector gets norm 0 and the indices of coordinate 0.
  * Errors: NULL or misaligned pointers, B or max_pages <= 0, total_tok < 0,
@@ -360,6 +362,43 @@ jf_status jf_tq4_encode_append(const jf_kv_layout* layout, void* words,
                                const int32_t* block_tables, int32_t B,
                                int32_t max_pages, int32_t total_tok,
                                hipStream_t stream);
+
+/* Single-query decode attention over TQ4 pages (Sec. 3.1, eq. codec: the
+ * page-native decode reads the packed indices and norms where they are
+ * stored).  Query head h reads KV head h / (num_q_heads / Hkv); request b
+ * attends to its logical positions 0..seq_lens[b]-1 through its page table.
+ * Computed without reconstructing any vector: the query is rotated once
+ * (q' = H S_k q / 16), each position's logit is softmax_scale * norm_k *
+ * (q' . c[z_k]), the weighted sum u = sum_t p_t norm_v c[z_v] is kept in the
+ * rotated space, and the output is S_v H u / (16 sum_t p_t).
+ *   k_words, v_words  u32 [NP][Hkv][P][32] (TQ4 pool layout above), 16-byte
+ *                     aligned; k_norms, v_norms fp16 [NP][Hkv][P], 16-byte
+ *                     aligned
+ *   k_signs, v_signs  fp32 [256] (device): the sign diagonals the vectors
+ *                     were encoded with; centroids fp32 [16] (device)
+ *   q, out            fp16 [B][num_q_heads][256] (device)
+ *   block_tables, max_pages, seq_lens, softmax_scale, max_splits,
+ *   workspace         as in jf_decode_attn_q4, the workspace sized by
+ *                     jf_decode_workspace_bytes(B, num_q_heads, 256,
+ *                     max_splits) (same zero-counter rules)
+ * Arithmetic: centroids rounded to fp16 once, q' as an fp16 high plus low
+ * part, products on fp16 matrix cores with fp32 accumulation.  A norm that
+ * overflowed fp16 at encode time (|x| above 65504) is +inf and makes the
+ * outputs of every query reading that position non-finite.
+ * Errors: head_dim != 256, page_size not a multiple of 32 or more than 16
+ * query heads per KV head -> JF_ERR_UNSUPPORTED; NULL or misaligned
+ * pointers, bad sizes, a short workspace or a non-finite scale ->
+ * JF_ERR_INVALID; no launch on error. */
+jf_status jf_tq4_decode_attn(const jf_kv_layout* layout, const void* k_words,
+                             const void* k_norms, const void* v_words,
+                             const void* v_norms, const float* k_signs,
+                             const float* v_signs, const float* centroids,
+                             const void* q, int32_t B, int32_t num_q_heads,
+                             const int32_t* block_tables, int32_t max_pages,
+                             const int32_t* seq_lens, float softmax_scale,
+                             int32_t max_splits, void* workspace,
+                             size_t workspace_bytes, void* out,
+                             hipStream_t stream);
 
 #ifdef __cplusplus
 }

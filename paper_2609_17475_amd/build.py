@@ -19,7 +19,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libjfkv.so")
 ARCH = os.environ.get("JFKV_ARCH", "gfx950")
 
-SOURCES = ["jfkv_host.cpp", "quantize.hip", "decode.hip", "prefill.hip", "tq4.hip"]
+SOURCES = ["jfkv_host.cpp", "quantize.hip", "decode.hip", "prefill.hip", "tq4.hip",
+           "tq4_decode.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]

@@ -569,4 +569,46 @@ jf_status jf_tq4_encode_append(const jf_kv_layout* layout, void* words, void* no
                        "tq4_encode launch");
 }
 
+jf_status jf_tq4_decode_attn(const jf_kv_layout* layout, const void* k_words,
+                             const void* k_norms, const void* v_words, const void* v_norms,
+                             const float* k_signs, const float* v_signs, const float* centroids,
+                             const void* q, int32_t B, int32_t num_q_heads,
+                             const int32_t* block_tables, int32_t max_pages,
+                             const int32_t* seq_lens, float softmax_scale, int32_t max_splits,
+                             void* workspace, size_t workspace_bytes, void* out,
+                             hipStream_t stream) {
+  jf_status st = check_tq4_layout(layout);
+  if (st) return st;
+  if (layout->page_size % 32)
+    return fail(JF_ERR_UNSUPPORTED, "TQ4 decode needs page_size a multiple of 32, got %d",
+                layout->page_size);
+  if (!k_words || !k_norms || !v_words || !v_norms || !k_signs || !v_signs || !centroids || !q ||
+      !block_tables || !seq_lens || !workspace || !out)
+    return fail(JF_ERR_INVALID, "NULL device pointer");
+  if (B <= 0 || num_q_heads <= 0 || max_pages <= 0)
+    return fail(JF_ERR_INVALID, "B, num_q_heads and max_pages must be positive");
+  if (num_q_heads % layout->num_kv_heads)
+    return fail(JF_ERR_INVALID, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                num_q_heads, layout->num_kv_heads);
+  if (num_q_heads / layout->num_kv_heads > 16)
+    return fail(JF_ERR_UNSUPPORTED, "TQ4 decode takes at most 16 query heads per KV head");
+  if ((int64_t)max_pages * layout->page_size > INT32_MAX)
+    return fail(JF_ERR_INVALID, "max_pages * page_size overflows int32");
+  if (((uintptr_t)k_words | (uintptr_t)v_words | (uintptr_t)k_norms | (uintptr_t)v_norms) & 15)
+    return fail(JF_ERR_INVALID, "index words and norms must be 16-byte aligned");
+  size_t need = 0;
+  if ((st = jf_decode_workspace_bytes(B, num_q_heads, layout->head_dim, max_splits, &need)))
+    return st;
+  if (workspace_bytes < need)
+    return fail(JF_ERR_INVALID, "workspace %zu bytes < required %zu", workspace_bytes, need);
+  if (!(softmax_scale == softmax_scale) || softmax_scale == INFINITY ||
+      softmax_scale == -INFINITY)
+    return fail(JF_ERR_INVALID, "softmax_scale must be finite");
+  return device_status(jfkv::launch_tq4_decode(*layout, k_words, k_norms, v_words, v_norms,
+                                               k_signs, v_signs, centroids, q, B, num_q_heads,
+                                               block_tables, max_pages, seq_lens, softmax_scale,
+                                               max_splits, workspace, out, stream),
+                       "tq4_decode launch");
+}
+
 }  // extern "C"

@@ -74,4 +74,11 @@ hipError_t launch_tq4_encode(const jf_kv_layout& L, void* words, void* norms, co
                              const int32_t* start_pos, const int32_t* block_tables, int32_t B,
                              int32_t max_pages, int32_t total_tok, hipStream_t stream);
 
+hipError_t launch_tq4_decode(const jf_kv_layout& L, const void* k_words, const void* k_norms,
+                             const void* v_words, const void* v_norms, const float* k_signs,
+                             const float* v_signs, const float* centroids, const void* q,
+                             int32_t B, int32_t Hq, const int32_t* block_tables,
+                             int32_t max_pages, const int32_t* seq_lens, float softmax_scale,
+                             int32_t max_splits, void* ws, void* out, hipStream_t stream);
+
 }  // namespace jfkv

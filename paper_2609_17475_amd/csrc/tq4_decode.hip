@@ -1,0 +1,474 @@
+// Single-query decode attention over TQ4 pages (d = 256), split-K with the
+// same bounded workspace and in-kernel combine as the affine decode.
+//
+// TQ4 (Sec. 3.1, eq. codec; Appendix A, Table codec) stores a vector x as an
+// fp16 norm rho^ and 256 4-bit indices z into 16 shared centroids c, with
+// x^ = rho^ S H c[z] / 16 (H the unnormalised Hadamard matrix of order 256,
+// S the diagonal of random signs).  By linearity the rotation leaves the page
+// scan:
+//   q . x^_t = rho^_t (q' . c[z_t])          with q' = H S q / 16 (once),
+//   o = sum_t p_t x^_t / sum_t p_t = S H u / (16 sum_t p_t),
+//        u = sum_t p_t rho^_t c[z_t]           (rotated back once).
+// So the scan reads the packed indices and the norms where they are stored
+// (page-native, Sec. 3.1) and never reconstructs a vector.
+//
+// Each 4-bit index becomes its centroid as an fp16 matrix-core operand by
+// byte-permute lookups: the 16 fp16 centroids are held as two byte planes of
+// four registers each; one v_perm_b32 per plane and table half fetches the
+// low or high bytes of four entries, a byte mask from the index's top bit
+// picks the table half, and two more permutes interleave the bytes into
+// fp16 pairs (about three instructions per index, shared by every query
+// head of the KV head).  The centroids are rounded to fp16 once (relative
+// error <= 2^-11); q' enters as an fp16 high part plus an fp16 low part.
+//
+// Matrix-core layout (v_mfma_f32_16x16x32_f16; lane (m, q4) = (lane % 16,
+// lane / 16) feeds operand row m, k-slots 8 q4 .. 8 q4 + 7, and receives
+// column m, rows 4 q4 .. 4 q4 + 3 of the result):
+//   scores  S^T[pos][head] over 8 k-steps of 32 dims, two 16-position tiles
+//           per 32-position row; tile t row m is position 8 (m / 4) + 4 t +
+//           m % 4, and k-step kb of lane quarter q4 is index word 8 q4 + kb
+//           (dims in the order 0, 2, 4, 6, 1, 3, 5, 7 of the word, the order
+//           the nibble selectors produce), so each lane's K data is 32
+//           contiguous bytes of one position and its scores are positions
+//           8 q4 .. 8 q4 + 7;
+//   values  u^T[dim][head] += c[z][dim][pos] x W[pos][head], W = p rho^_V
+//           (fp16); product j (0..15) has row m = dim 16 m + j, so lane
+//           (m, q4) holds index words 2 m, 2 m + 1 of positions 8 q4 ..
+//           8 q4 + 7 (8 bytes each) and the k-slots are exactly the positions
+//           of its own scores; byte b of those words holds dims 16 m + 2 b
+//           and + 1 of one position, gathered over four positions by three
+//           permutes into one selector word.
+// Online softmax per head with a lazy running maximum (raised only when a
+// logit exceeds it by more than 2 in log2 units, so p <= 4).
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "jfkv.h"
+#include "jfkv_internal.h"
+
+namespace {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kD = 256;           // head dimension of the format
+constexpr int kWordsPerVec = kD / 8;
+constexpr int kWaves = 4;         // one wave per SIMD, one block per CU
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRowPos = 32;       // positions per row (two 16-position tiles)
+constexpr int kMaxCols = 16;      // query heads per KV head: one column block
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kTau = 2.0f;      // lazy-rescale margin, log2 units
+constexpr float kMinit = -1e30f;  // finite initial maximum (masked rows give p = 0)
+
+// Byte planes of the 16 fp16 centroids: l[k] holds the low bytes of entries
+// 4k .. 4k + 3, h[k] their high bytes.
+struct Tab {
+  uint32_t l[4], h[4];
+};
+
+__device__ __forceinline__ f32x4 mfma(h8 a, h8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// m ? a : b, bitwise
+__device__ __forceinline__ uint32_t bsel(uint32_t m, uint32_t a, uint32_t b) {
+  return (a & m) | (b & ~m);
+}
+
+// The fp16 centroids of the four indices in bytes 0..3 of s (values 0..15):
+// e01 = entries of bytes 0 and 1, e23 = of bytes 2 and 3 (low half first).
+__device__ __forceinline__ void lookup4(uint32_t s, const Tab& T, uint32_t& e01, uint32_t& e23) {
+  const uint32_t i = s & 0x07070707u;            // entry within a table half
+  const uint32_t x = (s >> 3) & 0x01010101u;     // 1 where the entry is 8..15
+  const uint32_t m = (x << 8) - x;               // 0xFF there
+  const uint32_t lo = bsel(m, __builtin_amdgcn_perm(T.l[3], T.l[2], i),
+                           __builtin_amdgcn_perm(T.l[1], T.l[0], i));
+  const uint32_t hi = bsel(m, __builtin_amdgcn_perm(T.h[3], T.h[2], i),
+                           __builtin_amdgcn_perm(T.h[1], T.h[0], i));
+  e01 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
+  e23 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
+}
+
+// Score operand of one index word (eight consecutive dims of one position):
+// k-slots hold dims 0, 2, 4, 6, 1, 3, 5, 7 of the word.
+__device__ __forceinline__ h8 k_operand(uint32_t w, const Tab& T) {
+  uint32_t r0, r1, r2, r3;
+  lookup4(w & 0x0F0F0F0Fu, T, r0, r1);
+  lookup4((w >> 4) & 0x0F0F0F0Fu, T, r2, r3);
+  const u32x4 r = {r0, r1, r2, r3};
+  return __builtin_bit_cast(h8, r);
+}
+
+// Byte b of the words a0 .. a3 (four positions) as one selector word.
+__device__ __forceinline__ uint32_t gather_byte(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3,
+                                                uint32_t sel_pair) {
+  const uint32_t x01 = __builtin_amdgcn_perm(a1, a0, sel_pair);
+  const uint32_t x23 = __builtin_amdgcn_perm(a3, a2, sel_pair);
+  return __builtin_amdgcn_perm(x23, x01, 0x05040100u);
+}
+
+// In-place Walsh-Hadamard transform (unnormalised, natural order) of n rows
+// of 256 floats in LDS, by the whole block.
+__device__ void fwht_rows(float* x, int n) {
+  for (int h = 1; h < kD; h <<= 1) {
+    for (int i = threadIdx.x; i < n * (kD / 2); i += kThreads) {
+      const int r = i / (kD / 2), k = i % (kD / 2);
+      float* row = x + r * kD;
+      const int a = (k / h) * (2 * h) + (k % h);
+      const float u = row[a], v = row[a + h];
+      row[a] = u + v;
+      row[a + h] = u - v;
+    }
+    __syncthreads();
+  }
+}
+
+// Page-aligned split s of n_pages pages into S parts (remainder first).
+__device__ __forceinline__ void split_range(int n_pages, int S, int s, int& pb, int& pe) {
+  const int base = n_pages / S, rem = n_pages % S;
+  pb = s * base + min(s, rem);
+  pe = pb + base + (s < rem ? 1 : 0);
+}
+
+// One row's data in registers.
+struct RowBuf {
+  uint4 k[2][2];    // tile t: index words 8 q4 .. 8 q4 + 7 of the tile's position
+  uint2 v[8];       // words 2 m, 2 m + 1 of positions 8 q4 + p
+  uint4 kn, vn;     // norms of positions 8 q4 .. 8 q4 + 7
+  bool ok;          // the row's page exists
+};
+
+__global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
+    const uint32_t* __restrict__ k_words, const __half* __restrict__ k_norms,
+    const uint32_t* __restrict__ v_words, const __half* __restrict__ v_norms,
+    const float* __restrict__ k_signs, const float* __restrict__ v_signs,
+    const float* __restrict__ centroids, const __half* __restrict__ q,
+    const int32_t* __restrict__ block_tables, const int32_t* __restrict__ seq_lens,
+    float* __restrict__ ws, uint32_t* __restrict__ tickets, __half* __restrict__ out, int Hq,
+    int Hkv, int P, int NP, int max_pages, int max_splits, int split_cap, float scale_log2) {
+  __shared__ float s_x[kMaxCols * kD];                   // q' rotation; final rotation
+  __shared__ float s_part[kWaves][kMaxCols * (kD + 2)];  // per-wave partials (u, m, l)
+  __shared__ uint32_t s_ticket;
+
+  const int split = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  const int gq = Hq / Hkv;
+  const int h0 = kv * gq;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l16 = lane & 15, q4 = lane >> 4;
+
+  const int L = min(seq_lens[b], max_pages * P);
+  if (L <= 0) {  // an empty request: zero output rows, written by split 0
+    if (split == 0)
+      for (int i = tid; i < gq * kD; i += kThreads)
+        out[((size_t)b * Hq + h0) * kD + i] = __float2half(0.0f);
+    return;
+  }
+  const int n_pages = (L + P - 1) / P;
+  const int S = min(split_cap, n_pages);
+  if (split >= S) return;
+  int pb, pe;
+  split_range(n_pages, S, split, pb, pe);
+  const int t_end = min(pe * P, L);
+
+  // ---- centroid byte planes (fp16, round to nearest even)
+  Tab T;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t bits = __builtin_bit_cast(uint16_t, (_Float16)centroids[4 * k + e]);
+      lo |= (bits & 0xFFu) << (8 * e);
+      hi |= (bits >> 8) << (8 * e);
+    }
+    T.l[k] = lo;
+    T.h[k] = hi;
+  }
+
+  // ---- q' = H S q / 16 per query head (a negative scale negates it)
+  const float qsign = scale_log2 < 0.0f ? -1.0f : 1.0f;
+  for (int i = tid; i < gq * kD; i += kThreads) {
+    const int h = i / kD, d = i % kD;
+    s_x[i] = qsign * k_signs[d] * __half2float(q[((size_t)b * Hq + h0 + h) * kD + d]);
+  }
+  __syncthreads();
+  fwht_rows(s_x, gq);
+  // B operands: k-step kb, lane (col, q4): word 8 q4 + kb, dims 0,2,4,6,1,3,5,7
+  h8 qhi[8], qlo[8];
+  {
+    const bool col_on = l16 < gq;
+#pragma unroll
+    for (int kb = 0; kb < 8; ++kb) {
+      const int w = 8 * q4 + kb;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int d = 8 * w + ((e < 4) ? 2 * e : 2 * (e - 4) + 1);
+        const float v = col_on ? s_x[l16 * kD + d] * 0.0625f : 0.0f;
+        const _Float16 vh = (_Float16)v;
+        qhi[kb][e] = vh;
+        qlo[kb][e] = (_Float16)(v - (float)vh);
+      }
+    }
+  }
+  __syncthreads();  // s_x is reused by the final rotation
+  const float kfold = fmaxf(fabsf(scale_log2), 1e-30f);  // |scale| in log2 units
+
+  // ---- this wave's rows: split rows wave, wave + kWaves, ...
+  const int rpp = P / kRowPos;  // rows per page
+  const int n_split_pages = pe - pb;
+  const int split_rows = n_split_pages * rpp;
+  const int my_rows = split_rows > wave ? (split_rows - wave + kWaves - 1) / kWaves : 0;
+  const size_t head_slots = (size_t)P;  // vectors per (page, KV head)
+  // page IDs of the split, 64 per register (lane k: page pb + 64 g + k)
+  int grp = -1, pg_reg = -1;
+  auto page_of = [&](int pi) {
+    const int g = pi >> 6;
+    if (g != grp) {
+      grp = g;
+      const int k = 64 * g + lane;
+      pg_reg = (k < n_split_pages) ? block_tables[(size_t)b * max_pages + pb + k] : -1;
+    }
+    return __builtin_amdgcn_readlane(pg_reg, pi & 63);
+  };
+
+  auto load_row = [&](int r, RowBuf& rb) {
+    const int R = wave + kWaves * r;
+    const int pi = R / rpp, rs = R % rpp;
+    int page = page_of(pi);
+    rb.ok = (unsigned)page < (unsigned)NP;
+    if (!rb.ok) page = 0;  // never read outside the pool; the row is masked
+    const size_t vec0 = ((size_t)page * Hkv + kv) * head_slots + (size_t)rs * kRowPos;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int pos = 8 * (l16 >> 2) + 4 * t + (l16 & 3);
+      const uint4* src = reinterpret_cast<const uint4*>(k_words + (vec0 + pos) * kWordsPerVec + 8 * q4);
+      rb.k[t][0] = src[0];
+      rb.k[t][1] = src[1];
+    }
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+      rb.v[p] = *reinterpret_cast<const uint2*>(v_words + (vec0 + 8 * q4 + p) * kWordsPerVec + 2 * l16);
+    rb.kn = *reinterpret_cast<const uint4*>(k_norms + vec0 + 8 * q4);
+    rb.vn = *reinterpret_cast<const uint4*>(v_norms + vec0 + 8 * q4);
+  };
+
+  f32x4 acc_v[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) acc_v[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  float m_run = kMinit, thr = kMinit, l_run = 0.0f;
+  const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
+
+  auto compute_row = [&](const RowBuf& rb, int r) {
+    const int R = wave + kWaves * r;
+    const int t_row = (pb + R / rpp) * P + (R % rpp) * kRowPos;  // first logical position
+    // ---- scores
+    float sc[8];  // positions 8 q4 + 4 t + i at index 4 t + i
+    const uint32_t kn[4] = {rb.kn.x, rb.kn.y, rb.kn.z, rb.kn.w};
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const uint32_t w[8] = {rb.k[t][0].x, rb.k[t][0].y, rb.k[t][0].z, rb.k[t][0].w,
+                             rb.k[t][1].x, rb.k[t][1].y, rb.k[t][1].z, rb.k[t][1].w};
+      f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) {
+        const h8 a = k_operand(w[kb], T);
+        acc = mfma(a, qhi[kb], acc);
+        acc = mfma(a, qlo[kb], acc);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k = 4 * t + i;
+        const _Float16 rho = __builtin_bit_cast(h2, kn[k >> 1])[k & 1];
+        sc[k] = acc[i] * (float)rho;
+      }
+    }
+    uint32_t vn[4] = {rb.vn.x, rb.vn.y, rb.vn.z, rb.vn.w};
+    const bool full = rb.ok && t_row + kRowPos <= t_end;  // wave-uniform
+    if (!full) {
+      asm volatile("" ::: "memory");  // keep the masking behind the branch
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const bool ok = rb.ok && t_row + 8 * q4 + k < t_end;
+        sc[k] = ok ? sc[k] : -INFINITY;
+        if (!ok) {  // a masked position contributes nothing (its norm may be anything)
+          h2 pr = __builtin_bit_cast(h2, vn[k >> 1]);
+          pr[k & 1] = (_Float16)0.0f;
+          vn[k >> 1] = __builtin_bit_cast(uint32_t, pr);
+        }
+      }
+    }
+    // ---- online softmax (one running maximum per head: lanes of one column)
+    float mx = sc[0];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) mx = fmaxf(mx, sc[k]);
+    mx *= kfold;
+    if (__builtin_amdgcn_ballot_w64(mx > thr) != 0) {
+      float M = fmaxf(mx, __shfl_xor(mx, 16));
+      M = fmaxf(M, __shfl_xor(M, 32));
+      if (M > m_run) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - M);
+        m_run = M;
+        thr = M + kTau;
+        l_run *= alpha;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc_v[j] *= alpha;
+      }
+    }
+    u32x4 Wv;  // W = p rho^_V, positions 8 q4 + 0 .. 7 in k-slot order
+#pragma unroll
+    for (int k2 = 0; k2 < 4; ++k2) {
+      const h2 p = {(_Float16)__builtin_amdgcn_exp2f(fmaf(sc[2 * k2], kfold, -m_run)),
+                    (_Float16)__builtin_amdgcn_exp2f(fmaf(sc[2 * k2 + 1], kfold, -m_run))};
+      l_run = __builtin_amdgcn_fdot2(p, ones, l_run, false);
+      Wv[k2] = __builtin_bit_cast(uint32_t, p * __builtin_bit_cast(h2, vn[k2]));
+    }
+    const h8 W = __builtin_bit_cast(h8, Wv);
+    // ---- values: product j has row m = dim 16 m + j
+#pragma unroll
+    for (int bb = 0; bb < 8; ++bb) {
+      const uint32_t selp = (uint32_t)(bb & 3) | ((uint32_t)(4 + (bb & 3)) << 8) | 0x0C0C0000u;
+      uint32_t src[8];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) src[p] = (bb < 4) ? rb.v[p].x : rb.v[p].y;
+      const uint32_t s03 = gather_byte(src[0], src[1], src[2], src[3], selp);
+      const uint32_t s47 = gather_byte(src[4], src[5], src[6], src[7], selp);
+#pragma unroll
+      for (int hn = 0; hn < 2; ++hn) {  // low nibble: dim 16 m + 2 bb; high: + 1
+        uint32_t a0, a1, a2, a3;
+        lookup4(hn ? (s03 >> 4) & 0x0F0F0F0Fu : s03 & 0x0F0F0F0Fu, T, a0, a1);
+        lookup4(hn ? (s47 >> 4) & 0x0F0F0F0Fu : s47 & 0x0F0F0F0Fu, T, a2, a3);
+        const u32x4 a = {a0, a1, a2, a3};
+        const int j = 2 * bb + hn;
+        acc_v[j] = mfma(__builtin_bit_cast(h8, a), W, acc_v[j]);
+      }
+    }
+  };
+
+  RowBuf b0, b1;
+  if (my_rows > 0) load_row(0, b0);
+  for (int r = 0; r < my_rows; r += 2) {
+    if (r + 1 < my_rows) load_row(r + 1, b1);
+    compute_row(b0, r);
+    if (r + 1 < my_rows) {
+      if (r + 2 < my_rows) load_row(r + 2, b0);
+      compute_row(b1, r + 1);
+    }
+  }
+
+  // ---- merge the waves: each writes its unnormalised u^T (lane (col, q4):
+  // dims 64 q4 + 16 i + j), its maximum and its row sum
+  {
+    float lsum = l_run + __shfl_xor(l_run, 16);
+    lsum += __shfl_xor(lsum, 32);
+    float* part = s_part[wave];
+    if (l16 < gq) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) part[l16 * (kD + 2) + 64 * q4 + 16 * i + j] = acc_v[j][i];
+      if (q4 == 0) {
+        part[l16 * (kD + 2) + kD] = m_run;
+        part[l16 * (kD + 2) + kD + 1] = lsum;
+      }
+    }
+  }
+  __syncthreads();
+  for (int o = tid; o < gq * kD; o += kThreads) {
+    const int h = o / kD, d = o % kD;
+    float mw[kWaves], M = kMinit;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      mw[w] = s_part[w][h * (kD + 2) + kD];
+      M = fmaxf(M, mw[w]);
+    }
+    float num = 0.0f, den = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float f = __builtin_amdgcn_exp2f(mw[w] - M);
+      num = fmaf(f, s_part[w][h * (kD + 2) + d], num);
+      den = fmaf(f, s_part[w][h * (kD + 2) + kD + 1], den);
+    }
+    float* rec = ws + (((size_t)b * Hq + h0 + h) * max_splits + split) * (kD + 4);
+    __hip_atomic_store(&rec[d], den > 0.0f ? num / den : 0.0f, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    if (d == 0) {
+      __hip_atomic_store(&rec[kD], M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&rec[kD + 1], den, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+
+  // ---- the last split of (request, KV head) to finish combines them all
+  // (log-sum-exp over the splits, in the rotated space), then rotates back.
+  // Ordering as in the affine decode: record stores, then the ticket
+  // increment (acq_rel, device scope); the last block takes a device-scope
+  // acquire fence before it reads the records.
+  __syncthreads();
+  uint32_t* ticket = tickets + (size_t)b * Hkv + kv;
+  if (tid == 0)
+    s_ticket = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (s_ticket != (uint32_t)(S - 1)) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (int o = tid; o < gq * kD; o += kThreads) {
+    const int h = o / kD, d = o % kD;
+    const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (kD + 4);
+    float M = kMinit;
+    for (int s = 0; s < S; ++s) {
+      const float* r = recs + (size_t)s * (kD + 4);
+      if (r[kD + 1] > 0.0f) M = fmaxf(M, r[kD]);
+    }
+    float num = 0.0f, den = 0.0f;
+    for (int s = 0; s < S; ++s) {
+      const float* r = recs + (size_t)s * (kD + 4);
+      const float l = r[kD + 1];
+      if (l > 0.0f) {
+        const float f = l * __builtin_amdgcn_exp2f(r[kD] - M);
+        num = fmaf(f, r[d], num);
+        den += f;
+      }
+    }
+    s_x[o] = den > 0.0f ? num / den : 0.0f;
+  }
+  __syncthreads();
+  fwht_rows(s_x, gq);
+  for (int o = tid; o < gq * kD; o += kThreads) {
+    const int h = o / kD, d = o % kD;
+    out[((size_t)b * Hq + h0 + h) * kD + d] = __float2half(v_signs[d] * s_x[o] * 0.0625f);
+  }
+}
+
+}  // namespace
+
+namespace jfkv {
+
+hipError_t launch_tq4_decode(const jf_kv_layout& L, const void* k_words, const void* k_norms,
+                             const void* v_words, const void* v_norms, const float* k_signs,
+                             const float* v_signs, const float* centroids, const void* q,
+                             int32_t B, int32_t Hq, const int32_t* block_tables,
+                             int32_t max_pages, const int32_t* seq_lens, float softmax_scale,
+                             int32_t max_splits, void* ws, void* out, hipStream_t stream) {
+  const int64_t per_split = L.num_kv_heads;
+  const int split_cap = (int)std::max<int64_t>(
+      1, std::min<int64_t>(max_splits, (num_cus() + per_split - 1) / per_split));
+  dim3 grid(split_cap, L.num_kv_heads, B);
+  uint32_t* tickets = static_cast<uint32_t*>(ws);
+  float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kDecodeCounterBytes);
+  hipLaunchKernelGGL(tq4_decode_kernel, grid, dim3(kThreads), 0, stream,
+                     static_cast<const uint32_t*>(k_words), static_cast<const __half*>(k_norms),
+                     static_cast<const uint32_t*>(v_words), static_cast<const __half*>(v_norms),
+                     k_signs, v_signs, centroids, static_cast<const __half*>(q), block_tables,
+                     seq_lens, records, tickets, static_cast<__half*>(out), Hq,
+                     L.num_kv_heads, L.page_size, L.num_pages, max_pages, max_splits, split_cap,
+                     softmax_scale * kLog2e);
+  return hipGetLastError();
+}
+
+}  // namespace jfkv

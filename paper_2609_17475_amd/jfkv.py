@@ -28,7 +28,7 @@ EXPORTS = [
     "jf_page_table_stats", "jf_page_table_info",
     "jf_kv_quantize_append", "jf_decode_workspace_bytes", "jf_decode_attn_q4",
     "jf_decode_step_q4", "jf_decode_step_q4_static", "jf_prefill_attn_q4",
-    "jf_tq4_pool_bytes", "jf_tq4_encode_append",
+    "jf_tq4_pool_bytes", "jf_tq4_encode_append", "jf_tq4_decode_attn",
 ]
 
 
@@ -87,6 +87,8 @@ def _load():
         "jf_prefill_attn_q4": (st, [P, P, P, P, P, i32, i32, P, i32, i32, ctypes.c_float, P, P]),
         "jf_tq4_pool_bytes": (st, [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
         "jf_tq4_encode_append": (st, [P, P, P, P, P, P, P, P, P, i32, i32, i32, P]),
+        "jf_tq4_decode_attn": (st, [P, P, P, P, P, P, P, P, P, i32, i32, P, i32, P,
+                                    ctypes.c_float, i32, P, sz, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -499,3 +501,49 @@ def bind_tq4_encode_append(pool: TQ4Pool, x, signs, centroids, cu_tok, start_pos
             start_pos.shape[0], block_tables.shape[1], x.shape[0], _stream(stream))
     return BoundCall(lib.jf_tq4_encode_append, args,
                      (lay, pool, x, signs, centroids, cu_tok, start_pos, block_tables))
+
+
+def _tq4_decode_args(k_pool: TQ4Pool, v_pool: TQ4Pool, k_signs, v_signs, centroids, q,
+                     block_tables, seq_lens, softmax_scale, max_splits, workspace, out, stream):
+    import torch
+    lay = k_pool.layout
+    for t, n, dt in ((k_signs, "k_signs", torch.float32), (v_signs, "v_signs", torch.float32),
+                     (centroids, "centroids", torch.float32), (q, "q", torch.float16),
+                     (block_tables, "block_tables", torch.int32),
+                     (seq_lens, "seq_lens", torch.int32), (out, "out", torch.float16)):
+        _dev_check(t, n, dt)
+    _dev_check(workspace, "workspace")
+    if tuple(v_pool.words.shape) != tuple(k_pool.words.shape):
+        raise ValueError("K and V pools must have the same layout")
+    B, Hq, d = q.shape
+    if d != lay.head_dim or out.shape != q.shape:
+        raise ValueError("q/out must be [B][Hq][head_dim]")
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("block_tables [B][max_pages], seq_lens [B]")
+    return (ctypes.byref(lay), _ptr(k_pool.words), _ptr(k_pool.norms), _ptr(v_pool.words),
+            _ptr(v_pool.norms), _ptr(k_signs), _ptr(v_signs), _ptr(centroids), _ptr(q), B, Hq,
+            _ptr(block_tables), block_tables.shape[1], _ptr(seq_lens), float(softmax_scale),
+            int(max_splits), _ptr(workspace), workspace.numel() * workspace.element_size(),
+            _ptr(out), _stream(stream))
+
+
+def jf_tq4_decode_attn(k_pool: TQ4Pool, v_pool: TQ4Pool, k_signs, v_signs, centroids, q,
+                       block_tables, seq_lens, softmax_scale: float, max_splits: int, workspace,
+                       out, stream=None):
+    """Decode attention of q [B][Hq][256] (fp16) over TQ4 K/V pools through the
+    page tables (see include/jfkv.h); the workspace is sized by
+    jf_decode_workspace_bytes(B, Hq, 256, max_splits) and zero-filled once."""
+    _check(lib.jf_tq4_decode_attn(*_tq4_decode_args(k_pool, v_pool, k_signs, v_signs, centroids,
+                                                    q, block_tables, seq_lens, softmax_scale,
+                                                    max_splits, workspace, out, stream)))
+
+
+def bind_tq4_decode(k_pool: TQ4Pool, v_pool: TQ4Pool, k_signs, v_signs, centroids, q,
+                    block_tables, seq_lens, softmax_scale, max_splits, workspace, out,
+                    stream=None) -> "BoundCall":
+    """jf_tq4_decode_attn with its arguments checked and marshalled once."""
+    args = _tq4_decode_args(k_pool, v_pool, k_signs, v_signs, centroids, q, block_tables,
+                            seq_lens, softmax_scale, max_splits, workspace, out, stream)
+    return BoundCall(lib.jf_tq4_decode_attn, args,
+                     (k_pool, v_pool, k_signs, v_signs, centroids, q, block_tables, seq_lens,
+                      workspace, out))
