@@ -1,19 +1,34 @@
 #!/usr/bin/env python
 """Decode attention over a 4-bit paged KV cache at a 262,144-position window.
 
-One step = one decode step of one layer for one request: host page
-reservation, quantize-append of the step's new K/V row into its page (position
-262,143), then split-K decode attention of 32 query heads (8 KV heads, d=128,
-GQA 4:1) over all 262,144 positions through a 1,024-entry shuffled page table,
-with the log-sum-exp combine.  Inputs (cache, page table, the steps' new rows
+One step (the default workload, decode_256k) = one decode step of one layer
+for one request: host page reservation, then one launch of the fused step
+(jf_decode_step_q4): quantize-append of the step's new K/V row at position
+262,143, split-K decode attention of 32 query heads (8 KV heads, d=128, GQA
+4:1) over all 262,144 positions through a 1,024-entry shuffled page table,
+and the log-sum-exp combine.  Inputs (cache, page table, the steps' new rows
 and queries) are resident in HBM before timing.  Consecutive steps use
 different layers' pools (--layers, default 8 x 302 MB), so a step never finds
 the previous step's cache lines in the 256 MB last-level cache, as in a model
 whose layers each own a pool.
 
-Prints one JSON line: KV positions/s/layer (value), HBM GB/s of the decode
-kernels against the 8 TB/s peak (roofline), and the CPU oracle timed on a
-bounded sample (cpu_baseline).
+Prints one JSON line: KV positions/s/layer (value), HBM GB/s of the step
+kernel against the 8 TB/s peak (roofline), and the CPU oracle timed on a
+bounded sample, on one core and on all of them (cpu_baseline).
+
+Other workloads (--workload) print their own line:
+  decode_4k        4 q / 1 KV head, 4,096 cached positions + 1 appended row
+                   (launch-bound, cache-resident: reported in us and GB/s)
+  decode_32k_loop  32 q / 8 KV heads, 32,768 cached positions then 6,144
+                   sequential steps of append + attend (pages reserved as the
+                   length crosses page boundaries); cache-resident
+  ragged_2req      two requests of 196,608 and 131,072 positions sharing a
+                   32,768-position prefix, one batched fused step (+1 row each)
+  prefill_chunk    2,048-row chunk over a 65,536-position prefix (MFMA roofline)
+  quantize_bulk    262,143 rows x 8 KV heads quantize-append (HBM roofline)
+  tq4_encode_bulk  TQ4 encode-append, 262,143 rows x 4 KV heads, d 256
+  tq4_decode_256k  TQ4 decode attention in the paper's geometry (24 q / 4 KV
+                   heads, d 256) over 262,144 positions
 """
 from __future__ import annotations
 
@@ -29,42 +44,11 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode-attn KV positions/s/layer + achieved HBM GB/s (% of peak) at 256K ctx"
 HBM_PEAK_GBS = 8000.0
-BYTES_PER_POSITION = 1152  # 2 * Hkv * (d/2 + 4*d/G) at Hkv=8, d=128, G=64
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 / bf16 matrix peak
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
-
-
-def cpu_baseline(k16, v16, q16, table, n_sample: int, min_seconds: float):
-    """The CPU oracle on a bounded sample of the same workload: one decode step
-    (append one row, attend) over the first n_sample positions of the window
-    (by default all of it), all 32 query heads.  Building the sample's cache
-    is untimed setup."""
-    import oracle
-    P, hkv, d, G = 256, 8, 128, 64
-    NP = int(table.max()) + 1
-    lay = oracle.layout(P, hkv, d, G, NP)
-    pool = oracle.Pool(lay)
-    n_cached = n_sample - 1
-    oracle.quantize_append(pool, k16[:n_cached], v16[:n_cached], [0, n_cached], [0], table[None])
-    steps = 0
-    t0 = time.perf_counter()
-    while True:  # repeat the step (same row, same position) until min_seconds have passed
-        oracle.quantize_append(pool, k16[n_cached:n_sample], v16[n_cached:n_sample], [0, 1],
-                               [n_cached], table[None])
-        oracle.decode(pool, q16[None], table[None], [n_sample], 1.0)
-        steps += 1
-        dt = time.perf_counter() - t0
-        if dt >= min_seconds:
-            break
-    threads = min(oracle.max_threads(), hkv)  # the decode loop has one task per KV head
-    return {"value": n_sample * steps / dt, "unit": "KV positions/s/layer", "cores": threads,
-            "kind": "oracle", "seconds": dt, "steps": steps, "host_cpus": len(os.sched_getaffinity(0)),
-            "cpu_model": _cpu_model(),
-            "sample": "decode steps (quantize-append 1 row + fp64 attention of 32 q heads) "
-                      "over the first %d positions of the 262,144-position window, repeated "
-                      "for at least %.0f s, as positions/s" % (n_sample, min_seconds)}
 
 
 def _cpu_model():
@@ -75,6 +59,10 @@ def _cpu_model():
     except OSError:
         pass
     return None
+
+
+def _host():
+    return {"host_cpus": len(os.sched_getaffinity(0)), "cpu_model": _cpu_model()}
 
 
 CSRC = os.path.join(ROOT, "paper_2609_17475_amd", "csrc")
@@ -117,9 +105,6 @@ def copy_calibration(n_bytes: int, reps: int):
           flush=True)
 
 
-MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 / bf16 matrix peak
-
-
 def _timed(calls, warmup, steps, stream):
     """Mean HIP-event duration (us) of each step's calls, and wall us/step."""
     import numpy as np
@@ -143,11 +128,374 @@ def _timed(calls, warmup, steps, stream):
     return per, wall
 
 
+def _back_to_back(step, warmup, steps, stream):
+    """Run warmup steps, then time `steps` steps back to back: one HIP event
+    pair on the kernels' stream brackets them (GPU us per step, launch gaps
+    included) and the host clock between two synchronizations (wall)."""
+    import torch
+    for s in range(warmup):
+        step(s)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for s in range(warmup, warmup + steps):
+        step(s)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e6
+    return e0.elapsed_time(e1) * 1e3 / steps, wall
+
+
+def _repeat(fn, min_seconds):
+    """Call fn until min_seconds have passed; (calls, seconds)."""
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        fn()
+        n += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            return n, dt
+
+
+# --------------------------------------------------------------- fused steps
+DECODE_STEP_WORKLOADS = ("decode_256k", "decode_4k", "ragged_2req")
+
+
+def _build_decode_case(name, args, n_steps_total):
+    """Pools (args.layers copies), page tables, the steps' rows and queries of
+    a fused-step workload.  Returns a dict."""
+    import numpy as np
+    import torch
+    from paper_2609_17475_amd import jfkv, workloads
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS[name]
+    P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
+    if name == "decode_256k":
+        window = args.positions or wl.seq_lens[0]
+        if window < P or window % P:
+            raise SystemExit("--positions must be a positive multiple of the page size (%d)" % P)
+        cached = [window - 1]  # the step's row lands in the window's last slot
+        NP = window // P + (wl.pool_pages - wl.seq_lens[0] // P)
+    else:
+        cached = list(wl.seq_lens)
+        NP = wl.pool_pages
+    B = len(cached)
+    lens = [c + 1 for c in cached]
+    pre = wl.shared_prefix
+    pp = jfkv.PagePool(NP, P, shuffle_seed=wl.seed)
+    seqs = [pp.create()]
+    if pre:
+        pp.reserve(seqs[0], pre)
+        pp.set_length(seqs[0], pre)
+        seqs += [pp.fork(seqs[0], pre) for _ in range(1, B)]
+    else:
+        seqs += [pp.create() for _ in range(1, B)]
+    for s, c in zip(seqs, cached):
+        pp.reserve(s, c + 1)
+        pp.set_length(s, c)
+    max_pages = -(-max(lens) // P)
+    table = np.array(pp.export(seqs, max_pages)[0], np.int32)
+    t_table = torch.from_numpy(table).to(dev)
+    # rows: the shared prefix once, each request's own cached rows, then one
+    # new row per request and step
+    own = [c - pre for c in cached]
+    n_rows = pre + sum(own) + B * n_steps_total
+    t0 = time.perf_counter()
+    k, v = workloads.gen_kv_device(wl.seed, n_rows, hkv, d, wl.n_outlier, dev)
+    q = workloads.gen_q_device(wl.seed + 1, n_steps_total * B, hq, d, dev)
+    lay = jfkv.layout(P, hkv, d, G, NP)
+    pools = [jfkv.KVPool(lay, device=dev) for _ in range(args.layers)]
+    i32 = lambda x: torch.tensor(x, dtype=torch.int32, device=dev)  # noqa: E731
+    if pre:
+        jfkv.jf_kv_quantize_append(pools[0], k[:pre], v[:pre], i32([0, pre]), i32([0]),
+                                   t_table[:1].contiguous())
+    cu = [0]
+    for o in own:
+        cu.append(cu[-1] + o)
+    if cu[-1]:
+        jfkv.jf_kv_quantize_append(pools[0], k[pre:pre + cu[-1]], v[pre:pre + cu[-1]], i32(cu),
+                                   i32([pre] * B), t_table)
+    torch.cuda.synchronize()
+    for p in pools[1:]:
+        for n in ("k_codes", "v_codes", "k_meta", "v_meta"):
+            getattr(p, n).copy_(getattr(pools[0], n))
+    torch.cuda.synchronize()
+    log("%s: inputs and %d layer pools built in %.1fs" % (name, args.layers,
+                                                         time.perf_counter() - t0))
+    new0 = pre + cu[-1]
+    return dict(wl=wl, P=P, hkv=hkv, hq=hq, d=d, G=G, B=B, cached=cached, lens=lens, pre=pre,
+                NP=NP, pp=pp, seqs=seqs, table=table, t_table=t_table, k=k, v=v, q=q,
+                pools=pools, new0=new0, own=own, cu=cu, dev=dev)
+
+
+def _decode_oracle_baseline(c, name, args):
+    """The oracle (C, fp64 attention) on the same step: append each request's
+    row, attend; all cores on the full step, one core on a sample of the
+    first positions of request 0."""
+    import numpy as np
+    import oracle
+    k_all, v_all = c["k"].cpu().numpy(), c["v"].cpu().numpy()
+    q0 = c["q"][:c["B"]].cpu().numpy()
+    P, hkv, d, G, B = c["P"], c["hkv"], c["d"], c["G"], c["B"]
+    pre, cu, new0 = c["pre"], c["cu"], c["new0"]
+    table = c["table"]
+
+    def build(lens_cached, b_rows):
+        pool = oracle.Pool(oracle.layout(P, hkv, d, G, c["NP"]))
+        if pre:
+            oracle.quantize_append(pool, k_all[:pre], v_all[:pre], [0, pre], [0], table[:1])
+        for b in b_rows:
+            n = lens_cached[b] - pre
+            if n > 0:
+                s = pre + cu[b]
+                oracle.quantize_append(pool, k_all[s:s + n], v_all[s:s + n], [0, n], [pre],
+                                       table[b:b + 1])
+        return pool
+
+    def step(pool, lens_cached, b_rows):
+        for b in b_rows:
+            r = new0 + b
+            oracle.quantize_append(pool, k_all[r:r + 1], v_all[r:r + 1], [0, 1],
+                                   [lens_cached[b]], table[b:b + 1])
+        oracle.decode(pool, q0[b_rows], table[b_rows], [lens_cached[b] + 1 for b in b_rows], 1.0)
+
+    rows = list(range(B))
+    all_cores = oracle.max_threads()
+    pool = build(c["cached"], rows)
+    n, dt = _repeat(lambda: step(pool, c["cached"], rows), args.cpu_seconds)
+    positions = sum(l_ + 1 for l_ in c["cached"])
+    res = {"value": positions * n / dt, "unit": "KV positions/s/layer", "cores": all_cores,
+           "kind": "oracle", "seconds": dt, "steps": n,
+           "sample": "%d full step(s) of %s (quantize-append of the step rows + fp64 "
+                     "attention of all %d query heads over all %d positions), %d threads" % (
+                         n, name, c["hq"], positions, all_cores)}
+    res.update(_host())
+    # one core, on the first positions of request 0 (the oracle's cost is
+    # linear in the positions)
+    n1 = min(args.cpu_sample_1t, c["cached"][0])
+    if n1 > 0:
+        lens1 = [n1] + c["cached"][1:]
+        pool1 = build(lens1, [0])
+        oracle.set_threads(1)
+        try:
+            m, dt1 = _repeat(lambda: step(pool1, lens1, [0]), args.cpu_seconds_1t)
+        finally:
+            oracle.set_threads(all_cores)
+        res["single_thread"] = {"value": (n1 + 1) * m / dt1, "unit": "KV positions/s/layer",
+                                "cores": 1, "seconds": dt1, "steps": m,
+                                "sample": "request 0's first %d positions + the step row, "
+                                          "all %d query heads" % (n1, c["hq"])}
+    return res
+
+
+def bench_decode_steps(name, args):
+    """A fused decode step (append one row per request, attend) repeated on
+    rotated layer pools, timed back to back."""
+    import torch
+    from paper_2609_17475_amd import jfkv
+    n_steps_total = args.warmup + args.steps
+    c = _build_decode_case(name, args, n_steps_total)
+    P, hkv, hq, d, G, B = c["P"], c["hkv"], c["hq"], c["d"], c["G"], c["B"]
+    stream = torch.cuda.current_stream()
+    lens_t = torch.tensor(c["lens"], dtype=torch.int32, device=c["dev"])
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(B, hq, d, args.max_splits),
+                     dtype=torch.uint8, device=c["dev"])
+    out = torch.empty((n_steps_total, B, hq, d), dtype=torch.float16, device=c["dev"])
+    calls = []
+    for s in range(n_steps_total):
+        pool = c["pools"][s % args.layers]
+        r = c["new0"] + B * s
+        calls.append(jfkv.bind_decode_step(pool, c["k"][r:r + B], c["v"][r:r + B],
+                                           c["q"][B * s:B * s + B], c["t_table"], lens_t, 1.0,
+                                           args.max_splits, ws, out[s], stream))
+    pp, seqs, lens = c["pp"], c["seqs"], c["lens"]
+
+    def step(s):
+        for sq, L in zip(seqs, lens):
+            pp.reserve(sq, L)  # host page reservation (satisfied: the rows' pages exist)
+        calls[s]()
+
+    gpu_us, wall_us = _back_to_back(step, args.warmup, args.steps, stream)
+    assert torch.isfinite(out.float()).all().item(), "non-finite decode output"
+    bpp = 2 * hkv * (d // 2 + 4 * d // G)            # bytes per position and layer
+    logical = sum(lens)
+    unique = logical - (B - 1) * c["pre"]            # shared prefix pages read through each table
+    nbytes = unique * bpp + B * (2 * hkv * d * 2 + bpp)  # + the rows read and written
+    achieved = nbytes / (gpu_us * 1e-6) / 1e9
+    wl = c["wl"]
+    L0 = lens[0]
+    window = name == "decode_256k" and L0 == wl.seq_lens[0]
+    label = name if (name != "decode_256k" or window) else "decode_%d" % L0
+    split_cap = min(args.max_splits,
+                    -(-torch.cuda.get_device_properties(0).multi_processor_count // hkv))
+    result = {
+        "metric": METRIC if window else "decode-attn KV positions/s/layer (%s)" % label,
+        "value": logical / (wall_us * 1e-6), "unit": "KV positions/s/layer", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall_us / 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u4 codes x f16 -> f32", "data": "synthetic",
+        "config": {"workload": label, "positions": lens, "batch": B, "num_q_heads": hq,
+                   "num_kv_heads": hkv, "head_dim": d, "page_size": P, "group_size": G,
+                   "shared_prefix": c["pre"], "max_splits": args.max_splits,
+                   "splits_used": [min(split_cap, -(-L // P)) for L in lens],
+                   "layers_rotated": args.layers,
+                   "step": "jf_decode_step_q4 (append + attend, one kernel)"},
+        "hbm_GBs": achieved, "hbm_pct_of_peak": 100.0 * achieved / HBM_PEAK_GBS,
+        "us_per_step": {"step_kernel": gpu_us, "wall": wall_us},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic() if window else None,
+                     "kernel": "decode_kernel, fused step (row append, split-K partials, "
+                               "in-kernel combine)",
+                     "algorithmic_bytes": nbytes,
+                     "bytes_per_position": bpp, "unique_positions": unique},
+    }
+    if name == "decode_4k":
+        result["roofline"]["regime"] = ("launch-bound: %.1f MB per step stays in the "
+                                        "last-level cache" % (nbytes / 1e6))
+    log("%s: gpu %.2f us/step, wall %.2f us/step, %.0f GB/s" % (label, gpu_us, wall_us,
+                                                                achieved))
+    if args.cpu_seconds > 0:
+        try:
+            result["cpu_baseline"] = _decode_oracle_baseline(c, label, args)
+        except Exception as e:  # the baseline is a report, not the product
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+def bench_decode_loop(args):
+    """decode_32k_loop: 32,768 cached positions, then 6,144 sequential steps;
+    each step reserves pages on the host (a new page every 256 steps, its
+    table entry copied to the device), then one fused step appends the row at
+    position L and attends L + 1 positions.  All steps are timed."""
+    import numpy as np
+    import torch
+    import oracle
+    from paper_2609_17475_amd import jfkv, workloads
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS["decode_32k_loop"]
+    P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
+    L0, n_steps = wl.seq_lens[0], wl.steps
+    max_pages = -(-(L0 + n_steps) // P)
+    k, v = workloads.gen_kv_device(wl.seed, L0 + n_steps, hkv, d, wl.n_outlier, dev)
+    q = workloads.gen_q_device(wl.seed + 1, n_steps, hq, d, dev)
+    lay = jfkv.layout(P, hkv, d, G, wl.pool_pages)
+    stream = torch.cuda.current_stream()
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(1, hq, d, args.max_splits),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty((n_steps, 1, hq, d), dtype=torch.float16, device=dev)
+    i32 = lambda x: torch.tensor(x, dtype=torch.int32, device=dev)  # noqa: E731
+
+    def setup():
+        pp = jfkv.PagePool(wl.pool_pages, P, shuffle_seed=wl.seed)
+        s = pp.create()
+        pp.reserve(s, L0)
+        pp.set_length(s, L0)
+        table = np.array(pp.export([s], max_pages)[0], np.int32)
+        t_table = torch.from_numpy(table).to(dev)
+        pool = jfkv.KVPool(lay, device=dev)
+        jfkv.jf_kv_quantize_append(pool, k[:L0], v[:L0], i32([0, L0]), i32([0]), t_table)
+        lens = torch.tensor([L0 + 1 + i for i in range(n_steps)], dtype=torch.int32,
+                            device=dev).view(n_steps, 1)
+        calls = [jfkv.bind_decode_step(pool, k[L0 + i:L0 + i + 1], v[L0 + i:L0 + i + 1],
+                                       q[i:i + 1].view(1, hq, d), t_table, lens[i], 1.0,
+                                       args.max_splits, ws, out[i], stream)
+                 for i in range(n_steps)]
+        torch.cuda.synchronize()
+        return pp, s, table, t_table, pool, lens, calls
+
+    def run(n, state):
+        pp, s, table, t_table, pool, lens, calls = state
+        pinned = torch.empty(max_pages, dtype=torch.int32).pin_memory()
+        n_pages = -(-L0 // P)
+        for i in range(n):
+            L = L0 + i
+            if (L + 1 + P - 1) // P > n_pages:  # the row opens a new page
+                pp.reserve(s, L + 1)
+                tab = pp.export([s], max_pages)[0][0]
+                n_pages += 1
+                pinned[n_pages - 1] = tab[n_pages - 1]
+                t_table[0, n_pages - 1:n_pages].copy_(pinned[n_pages - 1:n_pages],
+                                                      non_blocking=True)
+            calls[i]()
+            pp.set_length(s, L + 1)
+
+    warm = setup()
+    run(min(64, n_steps), warm)  # warm-up on a separate pool
+    torch.cuda.synchronize()
+    del warm
+    state = setup()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    run(n_steps, state)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / n_steps * 1e6
+    gpu = e0.elapsed_time(e1) * 1e3 / n_steps
+    assert torch.isfinite(out.float()).all().item(), "non-finite decode output"
+    bpp = 2 * hkv * (d // 2 + 4 * d // G)
+    positions = sum(L0 + 1 + i for i in range(n_steps))
+    nbytes = positions * bpp + n_steps * (2 * hkv * d * 2 + bpp)
+    eff = nbytes / (gpu * 1e-6 * n_steps) / 1e9
+    result = {
+        "metric": "decode-attn KV positions/s/layer (decode_32k_loop: 6,144 sequential steps)",
+        "value": positions / (wall * 1e-6 * n_steps), "unit": "KV positions/s/layer",
+        "n_gpus": 1, "steps": n_steps, "warmup": 64, "ms_per_step": wall / 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u4 codes x f16 -> f32", "data": "synthetic",
+        "config": {"workload": "decode_32k_loop", "positions": [L0 + 1, L0 + n_steps],
+                   "num_q_heads": hq, "num_kv_heads": hkv, "head_dim": d, "page_size": P,
+                   "group_size": G, "max_splits": args.max_splits,
+                   "step": "host reserve (+ page-table entry copy every 256 steps) + "
+                           "jf_decode_step_q4"},
+        "us_per_step": {"gpu": gpu, "wall": wall},
+        "roofline": {"bound": "hbm", "achieved": eff, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": eff / HBM_PEAK_GBS, "traffic": None, "kernel": "decode_kernel",
+                     "algorithmic_bytes": nbytes,
+                     "regime": "effective GB/s: the 38-45 MB working set stays in the "
+                               "256 MB last-level cache across steps"},
+    }
+    log("decode_32k_loop: gpu %.2f us/step, wall %.2f us/step" % (gpu, wall))
+    if args.cpu_seconds > 0:
+        try:  # the oracle over the first 64 steps, extrapolated linearly in positions
+            kh, vh, qh = k.cpu().numpy(), v.cpu().numpy(), q.cpu().numpy()
+            pp = jfkv.PagePool(wl.pool_pages, P, shuffle_seed=wl.seed)
+            s = pp.create()
+            pp.reserve(s, L0 + 64)
+            table = np.array(pp.export([s], max_pages)[0], np.int32)
+            opool = oracle.Pool(oracle.layout(P, hkv, d, G, wl.pool_pages))
+            oracle.quantize_append(opool, kh[:L0], vh[:L0], [0, L0], [0], table)
+            t0 = time.perf_counter()
+            pos = 0
+            for i in range(64):
+                L = L0 + i
+                oracle.quantize_append(opool, kh[L:L + 1], vh[L:L + 1], [0, 1], [L], table)
+                oracle.decode(opool, qh[i:i + 1], table, [L + 1], 1.0)
+                pos += L + 1
+            dt = time.perf_counter() - t0
+            result["cpu_baseline"] = dict(
+                value=pos / dt, unit="KV positions/s/layer", cores=oracle.max_threads(),
+                kind="oracle", seconds=dt, steps=64,
+                sample="the first 64 of the 6,144 steps (append + fp64 attention of 32 heads "
+                       "over 32,769..32,832 positions); the full loop extrapolates to %.1f s"
+                       % (dt * positions / pos), **_host())
+        except Exception as e:
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+# --------------------------------------------------------------- prefill
 def bench_prefill(args):
     """Chunked prefill: a 2,048-row chunk (32 q / 8 KV heads, d 128) attends
     to a 65,536-position 4-bit prefix in 256 shuffled pages plus itself
     (causal), then the chunk is appended as 8 pages.  MFMA roofline over the
     attention kernel: FLOP = 4 d Hq sum_i (p0 + i + 1)."""
+    import numpy as np
     import torch
     from paper_2609_17475_amd import jfkv, workloads
     dev = torch.device("cuda:0")
@@ -158,7 +506,8 @@ def bench_prefill(args):
     pp = jfkv.PagePool(wl.pool_pages, P, shuffle_seed=wl.seed)
     s = pp.create()
     pp.reserve(s, p0 + T)
-    table = torch.tensor(pp.export([s], (p0 + T) // P)[0], dtype=torch.int32, device=dev)
+    table_np = np.array(pp.export([s], (p0 + T) // P)[0], np.int32)
+    table = torch.from_numpy(table_np).to(dev)
     k, v = workloads.gen_kv_device(wl.seed, p0 + T, hkv, d, wl.n_outlier, dev)
     q = workloads.gen_q_device(wl.seed + 1, T, hq, d, dev)
     pool = jfkv.KVPool(lay, device=dev)
@@ -178,7 +527,7 @@ def bench_prefill(args):
     flop = 4.0 * d * hq * sum(p0 + i + 1 for i in range(T))
     achieved = flop / (t_attn * 1e-6) / 1e12
     assert torch.isfinite(out.float()).all().item(), "non-finite prefill output"
-    print(json.dumps({
+    result = {
         "metric": "chunked-prefill attention TFLOP/s over a 4-bit paged prefix",
         "value": flop / (wall * 1e-6) / 1e12, "unit": "TFLOP/s", "n_gpus": 1, "steps": steps,
         "warmup": args.warmup, "ms_per_step": wall / 1e3, "higher_is_better": True,
@@ -189,14 +538,36 @@ def bench_prefill(args):
         "us_per_step": {"attention": t_attn, "append": t_app, "wall": wall},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / MFMA_F16_PEAK_TFLOPS, "traffic": None,
-                     "kernel": "prefill_kernel", "algorithmic_flop": flop},
-        "cpu_baseline": None}), flush=True)
+                     "kernel": "prefill_kernel", "algorithmic_flop": flop}}
+    if args.cpu_seconds > 0:
+        try:  # the oracle on 64 evenly spaced query rows, scaled to the chunk
+            import oracle
+            opool = oracle.Pool(oracle.layout(P, hkv, d, G, wl.pool_pages))
+            kh, vh = k.cpu().numpy(), v.cpu().numpy()
+            oracle.quantize_append(opool, kh[:p0], vh[:p0], [0, p0], [0], table_np)
+            rows = np.linspace(0, T - 1, 64).astype(np.int32)
+            t0 = time.perf_counter()
+            oracle.prefill(opool, q.cpu().numpy(), kh[p0:], vh[p0:], table_np[0], p0, 1.0,
+                           rows=rows)
+            dt = time.perf_counter() - t0
+            f_rows = 4.0 * d * hq * float(sum(p0 + int(i) + 1 for i in rows))
+            result["cpu_baseline"] = dict(
+                value=f_rows / dt / 1e12, unit="TFLOP/s", cores=oracle.max_threads(),
+                kind="oracle", seconds=dt,
+                sample="64 evenly spaced query rows of the chunk (all 32 heads, fp64), "
+                       "FLOP counted as in the roofline", **_host())
+        except Exception as e:
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
 
 
+# --------------------------------------------------------------- bulk encodes
 def bench_quantize_bulk(args):
     """Bulk quantize-append of 262,143 rows x 8 KV heads (the cache of the
     256K decode workload) into 1,024 shuffled pages; HBM roofline over the
     kernel: 2 x 256 B read and 2 x (64 + 8) B written per (row, KV head)."""
+    import numpy as np
     import torch
     from paper_2609_17475_amd import jfkv, workloads
     dev = torch.device("cuda:0")
@@ -207,7 +578,8 @@ def bench_quantize_bulk(args):
     pp = jfkv.PagePool(wl.pool_pages, P, shuffle_seed=wl.seed)
     s = pp.create()
     pp.reserve(s, L + 1)
-    table = torch.tensor(pp.export([s], (L + 1) // P)[0], dtype=torch.int32, device=dev)
+    table_np = np.array(pp.export([s], (L + 1) // P)[0], np.int32)
+    table = torch.from_numpy(table_np).to(dev)
     k, v = workloads.gen_kv_device(wl.seed, L, hkv, d, wl.n_outlier, dev)
     pools = [jfkv.KVPool(lay, device=dev) for _ in range(4)]
     cu = torch.tensor([0, L], dtype=torch.int32, device=dev)
@@ -218,7 +590,7 @@ def bench_quantize_bulk(args):
     (t_q,), wall = _timed(calls, args.warmup, steps, stream)
     nbytes = L * hkv * 2 * (2 * d + d // 2 + 4 * d // G)
     achieved = nbytes / (t_q * 1e-6) / 1e9
-    print(json.dumps({
+    result = {
         "metric": "bulk quantize-append GB/s (262,143 rows x 8 KV heads)",
         "value": nbytes / (wall * 1e-6) / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": steps,
         "warmup": args.warmup, "ms_per_step": wall / 1e3, "higher_is_better": True,
@@ -229,8 +601,33 @@ def bench_quantize_bulk(args):
         "us_per_step": {"quantize": t_q, "wall": wall},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("quantize"),
-                     "kernel": "quantize_rows_kernel", "algorithmic_bytes": nbytes},
-        "cpu_baseline": None}), flush=True)
+                     "kernel": "quantize_rows_kernel", "algorithmic_bytes": nbytes}}
+    if args.cpu_seconds > 0:
+        try:  # the whole bulk append in the oracle
+            import oracle
+            opool = oracle.Pool(oracle.layout(P, hkv, d, G, wl.pool_pages))
+            kh, vh = k.cpu().numpy(), v.cpu().numpy()
+            t0 = time.perf_counter()
+            oracle.quantize_append(opool, kh, vh, [0, L], [0], table_np)
+            dt = time.perf_counter() - t0
+            result["cpu_baseline"] = dict(value=nbytes / dt / 1e9, unit="GB/s", cores=1,
+                                          kind="oracle", seconds=dt,
+                                          sample="the full append (262,143 rows x 8 KV heads, "
+                                                 "single-threaded loop), same bytes", **_host())
+        except Exception as e:
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+def _tq4_inputs(P, hkv, L, NP, seed, dev):
+    import numpy as np
+    import torch
+    rng = np.random.default_rng(seed)
+    table = rng.permutation(NP)[:-(-L // P)][None].astype(np.int32)
+    signs = [torch.tensor(np.where(rng.random(256) < 0.5, -1.0, 1.0), dtype=torch.float32,
+                          device=dev) for _ in range(2)]
+    return table, signs
 
 
 def bench_tq4_encode(args):
@@ -243,14 +640,12 @@ def bench_tq4_encode(args):
     dev = torch.device("cuda:0")
     P, hkv, d, L = 256, 4, 256, 262143
     NP = L // P + 1 + 8
-    rng = np.random.default_rng(4)
-    table = torch.tensor(rng.permutation(NP)[:L // P + 1][None].astype(np.int32), device=dev)
+    table_np, (signs, _) = _tq4_inputs(P, hkv, L + 1, NP, 4, dev)
+    table = torch.from_numpy(table_np).to(dev)
     g = torch.Generator(device=dev).manual_seed(4)
     x = torch.randn((L, hkv, d), generator=g, device=dev, dtype=torch.float32).half()
     # signs and centroids are inputs of the kernel: any +-1 vector and any
     # ascending 16 values time the same; these are fixed stand-ins
-    signs = torch.tensor(np.where(rng.random(d) < 0.5, -1.0, 1.0), dtype=torch.float32,
-                         device=dev)
     cents = torch.linspace(-0.17, 0.17, 16, dtype=torch.float32, device=dev)
     lay = jfkv.layout(P, hkv, d, 64, NP)
     pools = [jfkv.TQ4Pool(lay, device=dev) for _ in range(4)]
@@ -263,7 +658,7 @@ def bench_tq4_encode(args):
     (t_e,), wall = _timed(calls, args.warmup, steps, stream)
     nbytes = L * hkv * (2 * d + d // 2 + 2)
     achieved = nbytes / (t_e * 1e-6) / 1e9
-    print(json.dumps({
+    result = {
         "metric": "TQ4 bulk encode-append GB/s (262,143 rows x 4 KV heads, d 256)",
         "value": nbytes / (wall * 1e-6) / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": steps,
         "warmup": args.warmup, "ms_per_step": wall / 1e3, "higher_is_better": True,
@@ -274,8 +669,125 @@ def bench_tq4_encode(args):
         "us_per_step": {"tq4_encode": t_e, "wall": wall},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "tq4_encode_kernel", "algorithmic_bytes": nbytes},
-        "cpu_baseline": None}), flush=True)
+                     "kernel": "tq4_encode_kernel", "algorithmic_bytes": nbytes}}
+    if args.cpu_seconds > 0:
+        try:  # the numpy TQ4 oracle's encode on 32,768 rows x 4 heads, scaled
+            from oracle import tq4
+            c = tq4.codebook(d)[0]
+            s_np = signs.cpu().numpy().astype(np.float64)
+            xs = x[:32768].cpu().numpy()
+            t0 = time.perf_counter()
+            for h in range(hkv):
+                idx, nrm, _ = tq4.encode(xs[:, h], s_np, c)
+                tq4.pack(idx)
+            dt = time.perf_counter() - t0
+            nb = 32768 * hkv * (2 * d + d // 2 + 2)
+            result["cpu_baseline"] = dict(value=nb / dt / 1e9, unit="GB/s", cores=_blas_threads(),
+                                          kind="oracle", seconds=dt,
+                                          sample="encode + pack of the first 32,768 rows x 4 "
+                                                 "heads (numpy, float64), same bytes per vector",
+                                          **_host())
+        except Exception as e:
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        return None
+
+
+def bench_tq4_decode(args):
+    """TQ4 decode attention in the paper's geometry: 24 query heads over 4 KV
+    heads, d 256, 262,144 positions in 1,024 shuffled pages (rotated layer
+    pools); HBM roofline over the kernel: 2 x 4 x (128 + 2) B per position."""
+    import numpy as np
+    import torch
+    from paper_2609_17475_amd import jfkv, workloads
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS["tq4_decode_256k"]
+    P, hkv, hq, d = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim
+    L, NP = wl.seq_lens[0], wl.pool_pages
+    table_np, (sk, sv) = _tq4_inputs(P, hkv, L, NP, wl.seed, dev)
+    table = torch.from_numpy(table_np).to(dev)
+    # signs and centroids are inputs of the kernel: any +-1 vectors and any
+    # ascending 16 values time the same; these are fixed stand-ins
+    cents = torch.linspace(-0.17, 0.17, 16, dtype=torch.float32, device=dev)
+    k, v = workloads.gen_kv_device(wl.seed, L, hkv, d, wl.n_outlier, dev)
+    lay = jfkv.layout(P, hkv, d, 64, NP)
+    cu = torch.tensor([0, L], dtype=torch.int32, device=dev)
+    st = torch.tensor([0], dtype=torch.int32, device=dev)
+    kp, vp = jfkv.TQ4Pool(lay, device=dev), jfkv.TQ4Pool(lay, device=dev)
+    jfkv.jf_tq4_encode_append(kp, k, sk, cents, cu, st, table)
+    jfkv.jf_tq4_encode_append(vp, v, sv, cents, cu, st, table)
+    pools = [(kp, vp)]
+    for _ in range(args.layers - 1):
+        a, b = jfkv.TQ4Pool(lay, device=dev), jfkv.TQ4Pool(lay, device=dev)
+        for dst, src in ((a, kp), (b, vp)):
+            dst.words.copy_(src.words)
+            dst.norms.copy_(src.norms)
+        pools.append((a, b))
+    torch.cuda.synchronize()
+    n_total = args.warmup + args.steps
+    q = workloads.gen_q_device(wl.seed + 1, n_total, hq, d, dev)
+    lens = torch.tensor([L], dtype=torch.int32, device=dev)
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(1, hq, d, args.max_splits),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty((n_total, 1, hq, d), dtype=torch.float16, device=dev)
+    stream = torch.cuda.current_stream()
+    calls = [jfkv.bind_tq4_decode(*pools[s % args.layers], sk, sv, cents, q[s:s + 1], table,
+                                  lens, 1.0, args.max_splits, ws, out[s], stream)
+             for s in range(n_total)]
+    gpu_us, wall_us = _back_to_back(lambda s: calls[s](), args.warmup, args.steps, stream)
+    assert torch.isfinite(out.float()).all().item(), "non-finite TQ4 decode output"
+    bpp = 2 * hkv * (d // 2 + 2)
+    nbytes = L * bpp
+    achieved = nbytes / (gpu_us * 1e-6) / 1e9
+    result = {
+        "metric": "TQ4 decode-attn KV positions/s/layer (24 q / 4 KV heads, d 256, 256K ctx)",
+        "value": L / (wall_us * 1e-6), "unit": "KV positions/s/layer", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall_us / 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u4 indices -> f16 centroids x f16 -> f32", "data": "synthetic",
+        "config": {"workload": "tq4_decode_256k", "positions": L, "num_q_heads": hq,
+                   "num_kv_heads": hkv, "head_dim": d, "page_size": P,
+                   "max_splits": args.max_splits, "layers_rotated": args.layers},
+        "us_per_step": {"kernel": gpu_us, "wall": wall_us},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "tq4_decode_kernel", "algorithmic_bytes": nbytes,
+                     "bytes_per_position": bpp}}
+    log("tq4_decode_256k: gpu %.2f us/step, %.0f GB/s" % (gpu_us, achieved))
+    if args.cpu_seconds > 0:
+        try:  # the numpy TQ4 oracle's decode on the first 32,768 positions
+            from oracle import tq4
+            n = 32768
+            c = cents.cpu().numpy()
+            s_k, s_v = sk.cpu().numpy().astype(np.float64), sv.cpu().numpy().astype(np.float64)
+            kw, kn = tq4.gather(kp.words.cpu().numpy().view(np.uint32), kp.norms.cpu().numpy(),
+                                table_np[0], n)
+            vw, vn = tq4.gather(vp.words.cpu().numpy().view(np.uint32), vp.norms.cpu().numpy(),
+                                table_np[0], n)
+            qh = q[0].cpu().numpy()
+            t0 = time.perf_counter()
+            tq4.decode_attention(qh, kw, kn, vw, vn, s_k, s_v, c, 1.0)
+            dt = time.perf_counter() - t0
+            result["cpu_baseline"] = dict(value=n / dt, unit="KV positions/s/layer",
+                                          cores=_blas_threads(), kind="oracle", seconds=dt,
+                                          sample="fp64 decode of all 24 heads over the first "
+                                                 "32,768 positions (numpy)", **_host())
+        except Exception as e:
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+WORKLOADS = ("decode_256k", "decode_4k", "decode_32k_loop", "ragged_2req", "prefill_chunk",
+             "quantize_bulk", "tq4_encode_bulk", "tq4_decode_256k")
 
 
 def main():
@@ -285,217 +797,46 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--layers", type=int, default=8, help="pools rotated across steps")
     ap.add_argument("--max-splits", type=int, default=64)
-    ap.add_argument("--two-calls", action="store_true",
-                    help="decode_256k: append and attend as two launches "
-                         "(jf_kv_quantize_append + jf_decode_attn_q4) instead of jf_decode_step_q4")
-    ap.add_argument("--cpu-sample", type=int, default=262144,
-                    help="positions in the CPU oracle sample (0 = skip)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="repeat the CPU oracle step for at least this long")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="repeat the all-core CPU oracle step for at least this long "
+                         "(0 = no cpu_baseline)")
+    ap.add_argument("--cpu-seconds-1t", type=float, default=4.0,
+                    help="repeat the one-core CPU oracle step for at least this long")
+    ap.add_argument("--cpu-sample-1t", type=int, default=32768,
+                    help="positions of the one-core CPU oracle sample (0 = skip)")
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="0 skips the CPU baseline (same as --cpu-seconds 0)")
     ap.add_argument("--positions", type=int, default=0,
-                    help="decode: context length in positions, a multiple of the page size "
-                         "(0 = the 262,144-position window of decode_256k); other lengths "
-                         "print a decode_<positions> line without the counter traffic")
+                    help="decode_256k: context length in positions, a multiple of the page size "
+                         "(0 = the 262,144-position window); other lengths print a "
+                         "decode_<positions> line without the counter traffic")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
-    ap.add_argument("--workload", default="decode_256k",
-                    choices=["decode_256k", "prefill_chunk", "quantize_bulk", "tq4_encode_bulk"],
-                    help="decode_256k (the headline line); prefill_chunk and quantize_bulk "
-                         "print their own lines")
+    ap.add_argument("--workload", default="decode_256k", choices=WORKLOADS)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+    if args.cpu_sample == 0:
+        args.cpu_seconds = 0.0
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, max(1, args.steps))
         return
-    if args.workload == "prefill_chunk":
-        bench_prefill(args)
-        return
-    if args.workload == "quantize_bulk":
-        bench_quantize_bulk(args)
-        return
-    if args.workload == "tq4_encode_bulk":
-        bench_tq4_encode(args)
-        return
-
-    import numpy as np
     import torch
-
-    from paper_2609_17475_amd import jfkv, workloads
-
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    wl = workloads.WORKLOADS["decode_256k"]
-    P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
-    L = args.positions or wl.seq_lens[0]
-    if L < P or L % P:
-        print("--positions must be a positive multiple of the page size (%d)" % P, file=sys.stderr)
-        sys.exit(2)
-    window = L == wl.seq_lens[0]
-    n_cached = L - 1
-    n_steps_total = args.warmup + args.steps
-    NP = L // P + (wl.pool_pages - wl.seq_lens[0] // P)  # the window's pages + spare pages
-    lay = jfkv.layout(P, hkv, d, G, NP)
-
-    # ---- page table: one request holding the full window (shuffled pages)
-    pp = jfkv.PagePool(NP, P, shuffle_seed=wl.seed)
-    seq = pp.create()
-    pp.reserve(seq, L)
-    pp.set_length(seq, n_cached)
-    table_rows, _ = pp.export([seq], L // P)
-    table = np.array(table_rows, np.int32)
-    t_table = torch.from_numpy(table).to(dev)
-
-    # ---- inputs (seeded, drawn on the device)
-    t0 = time.perf_counter()
-    k, v = workloads.gen_kv_device(wl.seed, n_cached + n_steps_total, hkv, d, wl.n_outlier, dev)
-    q = workloads.gen_q_device(wl.seed + 1, n_steps_total, hq, d, dev)
-    log("inputs drawn in %.1fs" % (time.perf_counter() - t0))
-
-    # ---- layer 0 cache built by the library's quantize-append, copied to the others
-    pools = [jfkv.KVPool(lay, device=dev) for _ in range(args.layers)]
-    t0 = time.perf_counter()
-    jfkv.jf_kv_quantize_append(pools[0], k[:n_cached], v[:n_cached],
-                               torch.tensor([0, n_cached], dtype=torch.int32, device=dev),
-                               torch.tensor([0], dtype=torch.int32, device=dev), t_table)
-    torch.cuda.synchronize()
-    log("bulk quantize of %d rows: %.1f ms (incl. launch)" % (n_cached, 1e3 * (time.perf_counter() - t0)))
-    for p in pools[1:]:
-        for n in ("k_codes", "v_codes", "k_meta", "v_meta"):
-            getattr(p, n).copy_(getattr(pools[0], n))
-    torch.cuda.synchronize()
-
-    # ---- per-step bound calls: append row n_cached + s at position n_cached, attend L
-    cu = torch.tensor([0, 1], dtype=torch.int32, device=dev)
-    start = torch.tensor([n_cached], dtype=torch.int32, device=dev)
-    lens = torch.tensor([L], dtype=torch.int32, device=dev)
-    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(1, hq, d, args.max_splits), dtype=torch.uint8,
-                     device=dev)
-    out = torch.empty((n_steps_total, 1, hq, d), dtype=torch.float16, device=dev)
-    stream = torch.cuda.current_stream()
-    appends, decodes = [], []
-    for s in range(n_steps_total):
-        pool = pools[s % args.layers]
-        row = slice(n_cached + s, n_cached + s + 1)
-        qs = q[s:s + 1].view(1, hq, d)
-        if args.two_calls:
-            appends.append(jfkv.bind_quantize_append(pool, k[row], v[row], cu, start, t_table,
-                                                     stream))
-            decodes.append(jfkv.bind_decode(pool, qs, t_table, lens, 1.0, args.max_splits, ws,
-                                            out[s], stream))
-        else:  # one launch: the row is appended at position L - 1, then attended to
-            appends.append(lambda: None)
-            decodes.append(jfkv.bind_decode_step(pool, k[row], v[row], qs, t_table, lens, 1.0,
-                                                 args.max_splits, ws, out[s], stream))
-
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(n_steps_total)]
-
-    def step(s, timed_events=False):
-        pp.reserve(seq, L)  # host page reservation (already satisfied at the window)
-        if timed_events:
-            if args.two_calls:
-                ev[s][0].record(stream)
-                appends[s]()
-            ev[s][1].record(stream)
-            decodes[s]()
-            ev[s][2].record(stream)
-        else:
-            appends[s]()
-            decodes[s]()
-
-    for s in range(args.warmup):
-        step(s)
-    torch.cuda.synchronize()
-    # the timed steps, back to back between two synchronizations; one HIP
-    # event pair on the kernels' stream brackets them (the kernel's average
-    # duration for the roofline: the GPU time per step, launch gaps included)
-    ev_all = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-    t0 = time.perf_counter()
-    ev_all[0].record(stream)
-    for s in range(args.warmup, n_steps_total):
-        step(s)
-    ev_all[1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_ms_per_step = ev_all[0].elapsed_time(ev_all[1]) / args.steps
-    if args.two_calls:
-        # the same steps again with events around each kernel, to split the
-        # step between the append and the decode kernels
-        for s in range(args.warmup, n_steps_total):
-            step(s, timed_events=True)
-        torch.cuda.synchronize()
-
-    timed = range(args.warmup, n_steps_total)
-    if args.two_calls:
-        t_app = [ev[s][0].elapsed_time(ev[s][1]) for s in timed]
-        t_dec = [ev[s][1].elapsed_time(ev[s][2]) for s in timed]
-    else:  # one kernel per step: its average is the bracketed GPU time per step
-        t_app = [0.0]
-        t_dec = [gpu_ms_per_step]
-    ms_per_step = 1e3 * wall / args.steps
-    dec_ms = float(np.mean(t_dec))
-    # the step kernel's algorithmic bytes: the window's codes and (scale,
-    # bias) words, plus, when fused, the new row's fp16 K/V read and its
-    # codes and meta written
-    dec_bytes = L * BYTES_PER_POSITION + (0 if args.two_calls else 2 * hkv * d * 2 + BYTES_PER_POSITION)
-    achieved = dec_bytes / (dec_ms * 1e-3) / 1e9
-    log("append %.2f us  decode %.2f us  gpu/step %.2f us  wall/step %.2f us" % (
-        1e3 * np.mean(t_app), 1e3 * dec_ms, 1e3 * gpu_ms_per_step, 1e3 * ms_per_step))
-
-    # sanity: the timed steps produced finite outputs
-    assert torch.isfinite(out.float()).all().item(), "non-finite decode output"
-
-    result = {
-        "metric": METRIC,
-        "value": L / (ms_per_step * 1e-3),
-        "unit": "KV positions/s/layer",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "u4 codes x f16 -> f32",
-        "data": "synthetic",
-        "config": {"workload": "decode_256k" if window else "decode_%d" % L, "positions": L, "batch": 1, "num_q_heads": hq,
-                   "num_kv_heads": hkv, "head_dim": d, "page_size": P, "group_size": G,
-                   "pages": L // P, "max_splits": args.max_splits,
-                   "splits_used": min(args.max_splits, L // P, -(-torch.cuda.get_device_properties(
-                       0).multi_processor_count // hkv)),
-                   "layers_rotated": args.layers,
-                   "step": ("jf_kv_quantize_append + jf_decode_attn_q4" if args.two_calls
-                            else "jf_decode_step_q4 (append + attend, one kernel)")},
-        "hbm_GBs": achieved,
-        "hbm_pct_of_peak": 100.0 * achieved / HBM_PEAK_GBS,
-        "us_per_step": {"append": (1e3 * float(np.mean(t_app)) if args.two_calls else None),
-                        "decode" if args.two_calls else "step_kernel": 1e3 * dec_ms,
-                        "gpu": 1e3 * gpu_ms_per_step,
-                        "wall": 1e3 * ms_per_step},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": measured_traffic() if window else None,
-                     "kernel": ("decode_kernel (split-K partials and the in-kernel combine)"
-                                if args.two_calls else
-                                "decode_kernel, fused step (row append, split-K partials, "
-                                "in-kernel combine)"),
-                     "algorithmic_bytes": dec_bytes},
-    }
-    if args.cpu_sample > 0:
-        try:
-            n_s = min(args.cpu_sample, L)
-            rows = n_s
-            kh = k[:rows].cpu().numpy()
-            vh = v[:rows].cpu().numpy()
-            qh = q[args.warmup].cpu().numpy()
-            result["cpu_baseline"] = cpu_baseline(kh, vh, qh, table[0], n_s, args.cpu_seconds)
-        except Exception as e:  # the baseline is a report, not the product
-            log("cpu baseline failed: %r" % (e,))
-            result["cpu_baseline"] = None
-    print(json.dumps(result), flush=True)
+    torch.cuda.set_device(torch.device("cuda:0"))
+    if args.workload in DECODE_STEP_WORKLOADS:
+        bench_decode_steps(args.workload, args)
+    elif args.workload == "decode_32k_loop":
+        bench_decode_loop(args)
+    elif args.workload == "prefill_chunk":
+        bench_prefill(args)
+    elif args.workload == "quantize_bulk":
+        bench_quantize_bulk(args)
+    elif args.workload == "tq4_encode_bulk":
+        bench_tq4_encode(args)
+    else:
+        bench_tq4_decode(args)
 
 
 if __name__ == "__main__":

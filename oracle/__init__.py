@@ -83,6 +83,8 @@ def lib():
             L.jfo_prefill.restype = ctypes.c_int
             L.jfo_max_threads.argtypes = []
             L.jfo_max_threads.restype = ctypes.c_int
+            L.jfo_set_threads.argtypes = [ctypes.c_int]
+            L.jfo_set_threads.restype = None
             _lib = L
     return _lib
 
@@ -222,3 +224,8 @@ def prefill(pool: Pool, q, k_chunk, v_chunk, block_table, prefix_len: int, alpha
 
 def max_threads() -> int:
     return lib().jfo_max_threads()
+
+
+def set_threads(n: int):
+    """Threads of the oracle's OpenMP loops (for timing it on 1 or all cores)."""
+    lib().jfo_set_threads(int(n))

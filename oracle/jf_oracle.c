@@ -26,6 +26,14 @@ int jfo_max_threads(void) {
 #endif
 }
 
+void jfo_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------
  * binary16 from its definition: sign, 5-bit biased exponent, 10-bit
  * fraction; exponent 0 holds subnormals (fraction * 2^-24).
@@ -314,35 +322,56 @@ int jfo_decode(const jfo_layout* L, const uint8_t* k_codes,
                int32_t Hq, const int32_t* block_tables, int32_t max_pages,
                const int32_t* seq_lens, double alpha, double* out) {
   int32_t H = L->num_kv_heads, d = L->head_dim;
-  if (H <= 0 || Hq % H) return -1;
+  if (H <= 0 || Hq % H || d > 512) return -1;
   int32_t gq = Hq / H; /* query heads per KV head; head h reads kv = h / gq */
   for (int32_t b = 0; b < B; ++b)
     if (seq_lens[b] <= 0) return -1;
+  int64_t n_kv = (int64_t)B * H;
+  double** Ks = calloc((size_t)n_kv, sizeof(double*));
+  double** Vs = calloc((size_t)n_kv, sizeof(double*));
+  if (!Ks || !Vs) {
+    free(Ks);
+    free(Vs);
+    return -1;
+  }
   int err = 0;
-  /* one (request, KV head) per iteration: gather once, serve its gq heads */
+  /* gather each (request, KV head) once, in logical order */
 #pragma omp parallel for schedule(dynamic) reduction(| : err)
-  for (int64_t task = 0; task < (int64_t)B * H; ++task) {
+  for (int64_t task = 0; task < n_kv; ++task) {
     int32_t b = (int32_t)(task / H), kv = (int32_t)(task % H);
     int64_t n = seq_lens[b];
-    double* K = malloc(sizeof(double) * n * d);
-    double* V = malloc(sizeof(double) * n * d);
-    double* s = malloc(sizeof(double) * n);
-    double qv[512];
-    if (!K || !V || !s ||
+    Ks[task] = malloc(sizeof(double) * n * d);
+    Vs[task] = malloc(sizeof(double) * n * d);
+    if (!Ks[task] || !Vs[task] ||
         gather(L, k_codes, k_meta, v_codes, v_meta,
-               block_tables + (size_t)b * max_pages, max_pages, kv, n, K, V)) {
+               block_tables + (size_t)b * max_pages, max_pages, kv, n, Ks[task], Vs[task]))
       err |= 1;
-    } else {
-      for (int32_t h = kv * gq; h < (kv + 1) * gq; ++h) {
-        const uint16_t* qh = q + ((size_t)b * Hq + h) * d;
-        for (int32_t i = 0; i < d; ++i) qv[i] = jfo_half_to_double(qh[i]);
-        attend(qv, K, V, n, d, alpha, s, out + ((size_t)b * Hq + h) * d);
-      }
-    }
-    free(K);
-    free(V);
-    free(s);
   }
+  /* then one task per (request, query head) */
+  if (!err) {
+#pragma omp parallel for schedule(dynamic) reduction(| : err)
+    for (int64_t task = 0; task < (int64_t)B * Hq; ++task) {
+      int32_t b = (int32_t)(task / Hq), h = (int32_t)(task % Hq);
+      int64_t n = seq_lens[b];
+      int64_t kvt = (int64_t)b * H + h / gq;
+      double* s = malloc(sizeof(double) * n);
+      double qv[512];
+      if (!s) {
+        err |= 1;
+        continue;
+      }
+      const uint16_t* qh = q + ((size_t)b * Hq + h) * d;
+      for (int32_t i = 0; i < d; ++i) qv[i] = jfo_half_to_double(qh[i]);
+      attend(qv, Ks[kvt], Vs[kvt], n, d, alpha, s, out + ((size_t)b * Hq + h) * d);
+      free(s);
+    }
+  }
+  for (int64_t t = 0; t < n_kv; ++t) {
+    free(Ks[t]);
+    free(Vs[t]);
+  }
+  free(Ks);
+  free(Vs);
   return err ? -1 : 0;
 }
 

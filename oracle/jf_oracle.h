@@ -110,8 +110,10 @@ int jfo_prefill(const jfo_layout* L, const uint8_t* k_codes,
                 int32_t prefix_len, double alpha, int chunk_quantized,
                 const int32_t* rows, int32_t n_rows, double* out);
 
-/* Threads the OpenMP loops use (1 when built without OpenMP). */
+/* Threads the OpenMP loops use (1 when built without OpenMP), and a way to
+ * set it (for timing the oracle on one core and on all of them). */
 int jfo_max_threads(void);
+void jfo_set_threads(int n);
 
 #ifdef __cplusplus
 }

@@ -65,6 +65,7 @@ constexpr int kMaxCols = 16;      // query heads per KV head: one column block
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kTau = 2.0f;      // lazy-rescale margin, log2 units
 constexpr float kMinit = -1e30f;  // finite initial maximum (masked rows give p = 0)
+constexpr int kMaxSplits = 256;   // split cap of the launch (the combine's LDS bound)
 
 // Byte planes of the 16 fp16 centroids: l[k] holds the low bytes of entries
 // 4k .. 4k + 3, h[k] their high bytes.
@@ -81,12 +82,18 @@ __device__ __forceinline__ uint32_t bsel(uint32_t m, uint32_t a, uint32_t b) {
   return (a & m) | (b & ~m);
 }
 
-// The fp16 centroids of the four indices in bytes 0..3 of s (values 0..15):
+// 0xFF in each byte of the result whose byte of x has its top bit set (byte
+// permute selectors 8..11 replicate the top bit of bytes 1, 3, 5, 7 of the
+// pair {x, x << 8}, i.e. of bytes 0, 2, 1, 3 of x).
+__device__ __forceinline__ uint32_t top_bit_mask(uint32_t x) {
+  return __builtin_amdgcn_perm(x, x << 8, 0x0B090A08u);
+}
+
+// The fp16 centroids of four indices given as entry bytes i (0..7 within a
+// table half) and half masks m (0xFF where the index is 8..15):
 // e01 = entries of bytes 0 and 1, e23 = of bytes 2 and 3 (low half first).
-__device__ __forceinline__ void lookup4(uint32_t s, const Tab& T, uint32_t& e01, uint32_t& e23) {
-  const uint32_t i = s & 0x07070707u;            // entry within a table half
-  const uint32_t x = (s >> 3) & 0x01010101u;     // 1 where the entry is 8..15
-  const uint32_t m = (x << 8) - x;               // 0xFF there
+__device__ __forceinline__ void lookup4(uint32_t i, uint32_t m, const Tab& T, uint32_t& e01,
+                                        uint32_t& e23) {
   const uint32_t lo = bsel(m, __builtin_amdgcn_perm(T.l[3], T.l[2], i),
                            __builtin_amdgcn_perm(T.l[1], T.l[0], i));
   const uint32_t hi = bsel(m, __builtin_amdgcn_perm(T.h[3], T.h[2], i),
@@ -95,12 +102,22 @@ __device__ __forceinline__ void lookup4(uint32_t s, const Tab& T, uint32_t& e01,
   e23 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
 }
 
+// The centroids of the four low nibbles (n = 0) or high nibbles (n = 1) of
+// the bytes of w: bit 3 of a low nibble is bit 7 of w << 4.
+__device__ __forceinline__ void lookup_nibbles(uint32_t w, int n, const Tab& T, uint32_t& e01,
+                                               uint32_t& e23) {
+  if (n == 0)
+    lookup4(w & 0x07070707u, top_bit_mask(w << 4), T, e01, e23);
+  else
+    lookup4((w >> 4) & 0x07070707u, top_bit_mask(w), T, e01, e23);
+}
+
 // Score operand of one index word (eight consecutive dims of one position):
 // k-slots hold dims 0, 2, 4, 6, 1, 3, 5, 7 of the word.
 __device__ __forceinline__ h8 k_operand(uint32_t w, const Tab& T) {
   uint32_t r0, r1, r2, r3;
-  lookup4(w & 0x0F0F0F0Fu, T, r0, r1);
-  lookup4((w >> 4) & 0x0F0F0F0Fu, T, r2, r3);
+  lookup_nibbles(w, 0, T, r0, r1);
+  lookup_nibbles(w, 1, T, r2, r3);
   const u32x4 r = {r0, r1, r2, r3};
   return __builtin_bit_cast(h8, r);
 }
@@ -154,6 +171,7 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     int Hkv, int P, int NP, int max_pages, int max_splits, int split_cap, float scale_log2) {
   __shared__ float s_x[kMaxCols * kD];                   // q' rotation; final rotation
   __shared__ float s_part[kWaves][kMaxCols * (kD + 2)];  // per-wave partials (u, m, l)
+  __shared__ h8 s_qop[8][2][64];                         // score B operands (q' high, low)
   __shared__ uint32_t s_ticket;
 
   const int split = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
@@ -200,22 +218,25 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   }
   __syncthreads();
   fwht_rows(s_x, gq);
-  // B operands: k-step kb, lane (col, q4): word 8 q4 + kb, dims 0,2,4,6,1,3,5,7
-  h8 qhi[8], qlo[8];
-  {
+  // B operands in LDS (one 16-byte entry per lane, read back conflict-free):
+  // k-step kb, lane (col, q4): word 8 q4 + kb, dims 0,2,4,6,1,3,5,7, as an
+  // fp16 high part and an fp16 low part; waves fill two k-steps each
+#pragma unroll
+  for (int k2 = 0; k2 < 8 / kWaves; ++k2) {
+    const int kb = (8 / kWaves) * wave + k2;
+    const int w = 8 * q4 + kb;
     const bool col_on = l16 < gq;
+    h8 hi, lo;
 #pragma unroll
-    for (int kb = 0; kb < 8; ++kb) {
-      const int w = 8 * q4 + kb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int d = 8 * w + ((e < 4) ? 2 * e : 2 * (e - 4) + 1);
-        const float v = col_on ? s_x[l16 * kD + d] * 0.0625f : 0.0f;
-        const _Float16 vh = (_Float16)v;
-        qhi[kb][e] = vh;
-        qlo[kb][e] = (_Float16)(v - (float)vh);
-      }
+    for (int e = 0; e < 8; ++e) {
+      const int d = 8 * w + ((e < 4) ? 2 * e : 2 * (e - 4) + 1);
+      const float v = s_x[min(l16, gq - 1) * kD + d] * 0.0625f;
+      const _Float16 vh = col_on ? (_Float16)v : (_Float16)0.0f;
+      hi[e] = vh;
+      lo[e] = col_on ? (_Float16)(v - (float)vh) : (_Float16)0.0f;
     }
+    s_qop[kb][0][lane] = hi;
+    s_qop[kb][1][lane] = lo;
   }
   __syncthreads();  // s_x is reused by the final rotation
   const float kfold = fmaxf(fabsf(scale_log2), 1e-30f);  // |scale| in log2 units
@@ -271,24 +292,29 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     // ---- scores
     float sc[8];  // positions 8 q4 + 4 t + i at index 4 t + i
     const uint32_t kn[4] = {rb.kn.x, rb.kn.y, rb.kn.z, rb.kn.w};
+    const uint32_t w[2][8] = {{rb.k[0][0].x, rb.k[0][0].y, rb.k[0][0].z, rb.k[0][0].w,
+                               rb.k[0][1].x, rb.k[0][1].y, rb.k[0][1].z, rb.k[0][1].w},
+                              {rb.k[1][0].x, rb.k[1][0].y, rb.k[1][0].z, rb.k[1][0].w,
+                               rb.k[1][1].x, rb.k[1][1].y, rb.k[1][1].z, rb.k[1][1].w}};
+    f32x4 acc[2] = {{0.0f, 0.0f, 0.0f, 0.0f}, {0.0f, 0.0f, 0.0f, 0.0f}};
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const uint32_t w[8] = {rb.k[t][0].x, rb.k[t][0].y, rb.k[t][0].z, rb.k[t][0].w,
-                             rb.k[t][1].x, rb.k[t][1].y, rb.k[t][1].z, rb.k[t][1].w};
-      f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int kb = 0; kb < 8; ++kb) {
+      const h8 qh = s_qop[kb][0][lane], ql = s_qop[kb][1][lane];
 #pragma unroll
-      for (int kb = 0; kb < 8; ++kb) {
-        const h8 a = k_operand(w[kb], T);
-        acc = mfma(a, qhi[kb], acc);
-        acc = mfma(a, qlo[kb], acc);
+      for (int t = 0; t < 2; ++t) {
+        const h8 a = k_operand(w[t][kb], T);
+        acc[t] = mfma(a, qh, acc[t]);
+        acc[t] = mfma(a, ql, acc[t]);
       }
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int k = 4 * t + i;
         const _Float16 rho = __builtin_bit_cast(h2, kn[k >> 1])[k & 1];
-        sc[k] = acc[i] * (float)rho;
+        sc[k] = acc[t][i] * (float)rho;
       }
-    }
     uint32_t vn[4] = {rb.vn.x, rb.vn.y, rb.vn.z, rb.vn.w};
     const bool full = rb.ok && t_row + kRowPos <= t_end;  // wave-uniform
     if (!full) {
@@ -342,8 +368,8 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
 #pragma unroll
       for (int hn = 0; hn < 2; ++hn) {  // low nibble: dim 16 m + 2 bb; high: + 1
         uint32_t a0, a1, a2, a3;
-        lookup4(hn ? (s03 >> 4) & 0x0F0F0F0Fu : s03 & 0x0F0F0F0Fu, T, a0, a1);
-        lookup4(hn ? (s47 >> 4) & 0x0F0F0F0Fu : s47 & 0x0F0F0F0Fu, T, a2, a3);
+        lookup_nibbles(s03, hn, T, a0, a1);
+        lookup_nibbles(s47, hn, T, a2, a3);
         const u32x4 a = {a0, a1, a2, a3};
         const int j = 2 * bb + hn;
         acc_v[j] = mfma(__builtin_bit_cast(h8, a), W, acc_v[j]);
@@ -417,25 +443,79 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   if (s_ticket != (uint32_t)(S - 1)) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  for (int o = tid; o < gq * kD; o += kThreads) {
-    const int h = o / kD, d = o % kD;
+  // split weights w_s = l_s 2^(m_s - M) (M the largest m_s of a non-empty
+  // split) and their sum, one wave per head, lanes over the splits; kept in
+  // LDS (s_part reused: gq * S <= 16 * kMaxSplits = 4,096 weights, then the
+  // gq sums)
+  float* s_w = s_part[0];                   // [gq][S]
+  float* s_den = s_part[0] + kMaxCols * kMaxSplits;  // [gq]
+  static_assert(kMaxCols * kMaxSplits + kMaxCols <= kMaxCols * (kD + 2), "weights fit");
+  for (int h = wave; h < gq; h += kWaves) {
     const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (kD + 4);
-    float M = kMinit;
-    for (int s = 0; s < S; ++s) {
-      const float* r = recs + (size_t)s * (kD + 4);
-      if (r[kD + 1] > 0.0f) M = fmaxf(M, r[kD]);
+    float mv[kMaxSplits / 64], lv[kMaxSplits / 64];
+    float M = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kMaxSplits / 64; ++j) {
+      const int s = lane + 64 * j;
+      const float2 ml = s < S ? *reinterpret_cast<const float2*>(recs + (size_t)s * (kD + 4) + kD)
+                              : make_float2(0.0f, 0.0f);
+      mv[j] = ml.y > 0.0f ? ml.x : -INFINITY;
+      lv[j] = ml.y;
+      M = fmaxf(M, mv[j]);
     }
-    float num = 0.0f, den = 0.0f;
-    for (int s = 0; s < S; ++s) {
-      const float* r = recs + (size_t)s * (kD + 4);
-      const float l = r[kD + 1];
-      if (l > 0.0f) {
-        const float f = l * __builtin_amdgcn_exp2f(r[kD] - M);
-        num = fmaf(f, r[d], num);
-        den += f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
+    float den = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kMaxSplits / 64; ++j) {
+      const int s = lane + 64 * j;
+      const float w = mv[j] == -INFINITY ? 0.0f : lv[j] * __builtin_amdgcn_exp2f(mv[j] - M);
+      if (s < S) s_w[h * S + s] = w;
+      den += w;
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) den += __shfl_xor(den, off);
+    if (lane == 0) s_den[h] = den;
+  }
+  __syncthreads();
+  // o = sum_s w_s o_s / sum_s w_s.  A wave task is (head, half of the dims);
+  // lane (c, k) = (lane % 32, lane / 32) sums dims 128 half + 4 c .. + 3 over
+  // the splits k, k + 2, ..., kCh independent 16-byte record loads at a time
+  constexpr int kCh = 32;
+  for (int task = wave; task < 2 * gq; task += kWaves) {
+    const int h = task >> 1, k = lane >> 5;
+    const int d0 = (kD / 2) * (task & 1) + 4 * (lane & 31);
+    const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (kD + 4) + d0;
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int s0 = k; s0 < S; s0 += 2 * kCh) {
+      float4 o[kCh];
+#pragma unroll
+      for (int i = 0; i < kCh; ++i) {  // past the end: a valid record, weight 0
+        const int s = min(s0 + 2 * i, S - 1);
+        o[i] = *reinterpret_cast<const float4*>(recs + (size_t)s * (kD + 4));
+      }
+#pragma unroll
+      for (int i = 0; i < kCh; ++i) {
+        const int s = s0 + 2 * i;
+        const float w = s < S ? s_w[h * S + s] : 0.0f;
+        acc.x = fmaf(w, o[i].x, acc.x);
+        acc.y = fmaf(w, o[i].y, acc.y);
+        acc.z = fmaf(w, o[i].z, acc.z);
+        acc.w = fmaf(w, o[i].w, acc.w);
       }
     }
-    s_x[o] = den > 0.0f ? num / den : 0.0f;
+    acc.x += __shfl_xor(acc.x, 32);
+    acc.y += __shfl_xor(acc.y, 32);
+    acc.z += __shfl_xor(acc.z, 32);
+    acc.w += __shfl_xor(acc.w, 32);
+    if (k == 0) {
+      const float den = s_den[h];
+      const float inv = den > 0.0f ? 1.0f / den : 0.0f;
+      s_x[h * kD + d0 + 0] = acc.x * inv;
+      s_x[h * kD + d0 + 1] = acc.y * inv;
+      s_x[h * kD + d0 + 2] = acc.z * inv;
+      s_x[h * kD + d0 + 3] = acc.w * inv;
+    }
   }
   __syncthreads();
   fwht_rows(s_x, gq);
@@ -457,7 +537,8 @@ hipError_t launch_tq4_decode(const jf_kv_layout& L, const void* k_words, const v
                              int32_t max_splits, void* ws, void* out, hipStream_t stream) {
   const int64_t per_split = L.num_kv_heads;
   const int split_cap = (int)std::max<int64_t>(
-      1, std::min<int64_t>(max_splits, (num_cus() + per_split - 1) / per_split));
+      1, std::min<int64_t>(std::min<int64_t>(max_splits, kMaxSplits),
+                           (num_cus() + per_split - 1) / per_split));
   dim3 grid(split_cap, L.num_kv_heads, B);
   uint32_t* tickets = static_cast<uint32_t*>(ws);
   float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kDecodeCounterBytes);

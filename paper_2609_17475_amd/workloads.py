@@ -22,6 +22,8 @@ for them.  Shapes follow the paper's page geometry (256-token pages, Background
                    first 32,768 positions share physical pages.
   prefill_chunk    2,048-row chunk over a 65,536-position prefix (256 shuffled
                    pages), 32/8 heads, then appended as 8 new pages.
+  tq4_decode_256k  the paper's geometry and codec: 24/4 heads, d=256, 262,144
+                   positions in 1,024 shuffled pages of TQ4 vectors.
 
 Recipe (fixed draw order, numpy PCG64 ``default_rng(seed)``):
   1. K then V: float32 N(0,1), shape [n_rows][Hkv][d];
@@ -70,6 +72,9 @@ WORKLOADS = {
                             seed=4, shared_prefix=32768),
     "prefill_chunk": Workload("prefill_chunk", 32, 8, 128, (65536,), 256 + 16, 3, seed=5,
                               chunk=2048),
+    # the paper's own geometry and format (24 query heads over 4 KV heads,
+    # d = 256, TQ4 pages) at its full native window
+    "tq4_decode_256k": Workload("tq4_decode_256k", 24, 4, 256, (262144,), 1024 + 8, 5, seed=6),
 }
 
 
