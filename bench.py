@@ -29,6 +29,8 @@ Other workloads (--workload) print their own line:
   tq4_encode_bulk  TQ4 encode-append, 262,143 rows x 4 KV heads, d 256
   tq4_decode_256k  TQ4 decode attention in the paper's geometry (24 q / 4 KV
                    heads, d 256) over 262,144 positions
+  verify_256k      the short packed verifier: 3 causal query tokens over
+                   decode_256k's 262,144-position cache
 """
 from __future__ import annotations
 
@@ -786,8 +788,90 @@ def bench_tq4_decode(args):
     print(json.dumps(result), flush=True)
 
 
+def bench_verify(args):
+    """verify_256k: the short packed verifier over decode_256k's cache, three
+    causal query tokens per request (32 q / 8 KV heads, d 128), rotated layer
+    pools.  HBM roofline over the kernel with the cache counted once
+    (1,152 B per position): the bytes a verifier that scans the pages once
+    per step must move."""
+    import numpy as np
+    import torch
+    import oracle
+    from paper_2609_17475_amd import jfkv, workloads
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS["verify_256k"]
+    P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
+    L, sq, NP = wl.seq_lens[0], wl.queries, wl.pool_pages
+    pp = jfkv.PagePool(NP, P, shuffle_seed=wl.seed)
+    s0 = pp.create()
+    pp.reserve(s0, L)
+    pp.set_length(s0, L)
+    table = np.array(pp.export([s0], L // P)[0], np.int32)
+    t_table = torch.from_numpy(table).to(dev)
+    k, v = workloads.gen_kv_device(wl.seed, L, hkv, d, wl.n_outlier, dev)
+    n_total = args.warmup + args.steps
+    q = workloads.gen_q_device(wl.seed + 1, n_total * sq, hq, d, dev).view(n_total, 1, sq, hq, d)
+    lay = jfkv.layout(P, hkv, d, G, NP)
+    pools = [jfkv.KVPool(lay, device=dev) for _ in range(args.layers)]
+    i32 = lambda x: torch.tensor(x, dtype=torch.int32, device=dev)  # noqa: E731
+    jfkv.jf_kv_quantize_append(pools[0], k, v, i32([0, L]), i32([0]), t_table)
+    torch.cuda.synchronize()
+    for p in pools[1:]:
+        for n in ("k_codes", "v_codes", "k_meta", "v_meta"):
+            getattr(p, n).copy_(getattr(pools[0], n))
+    lens = i32([L])
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(1, hq * sq, d, args.max_splits),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty((n_total, 1, sq, hq, d), dtype=torch.float16, device=dev)
+    stream = torch.cuda.current_stream()
+    calls = [jfkv.bind_verify(pools[s % args.layers], q[s], t_table, lens, 1.0, args.max_splits,
+                              ws, out[s], stream) for s in range(n_total)]
+    torch.cuda.synchronize()
+    gpu_us, wall_us = _back_to_back(lambda s: calls[s](), args.warmup, args.steps, stream)
+    assert torch.isfinite(out.float()).all().item(), "non-finite verify output"
+    bpp = 2 * hkv * (d // 2 + 4 * d // G)
+    nbytes = L * bpp + 2 * sq * hq * d * 2
+    achieved = nbytes / (gpu_us * 1e-6) / 1e9
+    gqv = hq // hkv * sq
+    n_hchunks = -(-gqv // 4)
+    result = {
+        "metric": "verify-attn KV positions/s/layer (3 causal query tokens, 32 q / 8 KV heads, "
+                  "256K ctx)",
+        "value": L / (wall_us * 1e-6), "unit": "KV positions/s/layer", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall_us / 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u4 codes x f16 -> f32", "data": "synthetic",
+        "config": {"workload": "verify_256k", "positions": L, "query_tokens": sq,
+                   "num_q_heads": hq, "num_kv_heads": hkv, "head_dim": d, "page_size": P,
+                   "group_size": G, "max_splits": args.max_splits,
+                   "head_chunks_per_kv_head": n_hchunks, "layers_rotated": args.layers},
+        "us_per_step": {"kernel": gpu_us, "wall": wall_us},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "decode_kernel (verifier: per-token causal limits)",
+                     "algorithmic_bytes": nbytes, "bytes_per_position": bpp}}
+    log("verify_256k: gpu %.2f us/step, %.0f GB/s (cache counted once)" % (gpu_us, achieved))
+    if args.cpu_seconds > 0:
+        try:  # the C oracle's verify (fp64) on the first positions of the cache
+            n = min(args.cpu_sample or 32768, L)
+            pool = oracle.Pool(oracle.layout(P, hkv, d, G, NP))
+            kh, vh = k[:n].cpu().numpy(), v[:n].cpu().numpy()
+            oracle.quantize_append(pool, kh, vh, [0, n], [0], table)
+            qh = q[0].cpu().numpy()
+            m, dt = _repeat(lambda: oracle.verify(pool, qh, table, [n], 1.0), args.cpu_seconds)
+            result["cpu_baseline"] = dict(
+                value=n * m / dt, unit="KV positions/s/layer", cores=oracle.max_threads(),
+                kind="oracle", seconds=dt, steps=m,
+                sample="fp64 verification of 3 tokens x 32 heads over the first %d positions "
+                       "(one decode per token), %d step(s)" % (n, m), **_host())
+        except Exception as e:
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
 WORKLOADS = ("decode_256k", "decode_4k", "decode_32k_loop", "ragged_2req", "prefill_chunk",
-             "quantize_bulk", "tq4_encode_bulk", "tq4_decode_256k")
+             "quantize_bulk", "tq4_encode_bulk", "tq4_decode_256k", "verify_256k")
 
 
 def main():
@@ -835,6 +919,8 @@ def main():
         bench_quantize_bulk(args)
     elif args.workload == "tq4_encode_bulk":
         bench_tq4_encode(args)
+    elif args.workload == "verify_256k":
+        bench_verify(args)
     else:
         bench_tq4_decode(args)
 

@@ -252,6 +252,30 @@ jf_status jf_decode_attn_q4(const jf_kv_layout* layout,
                             size_t workspace_bytes, void* out,
                             hipStream_t stream);
 
+/* Short packed verification (Sec. 3.1, the speculative-verification
+ * paragraph after eq. groupattention; Appendix A, "Codec and Attention
+ * Dispatch": causal string masks, 2 to 4 queries).  The last num_queries
+ * positions of request b (already appended: positions seq_lens[b] -
+ * num_queries .. seq_lens[b] - 1) are its query tokens; token k sees the
+ * positions 0 .. seq_lens[b] - num_queries + k (a causal mask aligned to the
+ * end of the cache).  One page scan serves every token and query head of a
+ * KV head chunk, as in jf_decode_attn_q4.
+ *   q            fp16 [B][num_queries][num_q_heads][d] (device)
+ *   num_queries  1..4 (1 is jf_decode_attn_q4); larger: JF_ERR_UNSUPPORTED
+ *   workspace    at least jf_decode_workspace_bytes(B, num_q_heads *
+ *                num_queries, d, max_splits); same zeroing rule as decode
+ *   out          fp16 [B][num_queries][num_q_heads][d] (device)
+ * Other arguments as jf_decode_attn_q4; a token whose visible length is
+ * <= 0 gets an all-zero output row. */
+jf_status jf_verify_attn_q4(const jf_kv_layout* layout,
+                            const jf_kv_pool_ptrs* pool, const void* q,
+                            int32_t B, int32_t num_queries, int32_t num_q_heads,
+                            const int32_t* block_tables, int32_t max_pages,
+                            const int32_t* seq_lens, float softmax_scale,
+                            int32_t max_splits, void* workspace,
+                            size_t workspace_bytes, void* out,
+                            hipStream_t stream);
+
 /* One decode step, append then attend, in one kernel: request b's new row
  * (k_new, v_new: fp16 [B][Hkv][d], device) is quantized into the pool at
  * logical position seq_lens[b] - 1 exactly as jf_kv_quantize_append would

@@ -199,6 +199,26 @@ def decode(pool: Pool, q, block_tables, seq_lens, alpha: float) -> np.ndarray:
     return out
 
 
+def verify(pool: Pool, q, block_tables, seq_lens, alpha: float) -> np.ndarray:
+    """Short packed verification (Sec. 3.1, speculative verification; Appendix
+    A, causal string masks over 2 to 4 queries).  q fp16 [B][Sq][Hq][d] ->
+    fp64 [B][Sq][Hq][d].  The last Sq cached positions of request b are its
+    query tokens; token k attends to positions 0 .. L_b - Sq + k, i.e. the
+    plain decode definition over the first L_b - Sq + k + 1 positions (an
+    all-zero row when that count is <= 0)."""
+    q = np.asarray(q)
+    B, Sq = q.shape[:2]
+    lens = [int(x) for x in np.asarray(seq_lens).reshape(-1)]
+    bt = _i32(block_tables)
+    out = np.zeros(q.shape, np.float64)
+    for k in range(Sq):
+        vis = [L - Sq + 1 + k for L in lens]
+        live = [b for b in range(B) if vis[b] > 0]
+        if live:
+            out[live, k] = decode(pool, q[live, k], bt[live], [vis[b] for b in live], alpha)
+    return out
+
+
 def prefill(pool: Pool, q, k_chunk, v_chunk, block_table, prefix_len: int, alpha: float,
             chunk_quantized: bool = False, rows=None) -> np.ndarray:
     """q fp16 [T][Hq][d], k/v fp16 [T][Hkv][d] -> fp64 [len(rows) or T][Hq][d]."""

@@ -340,6 +340,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t records_rsrc(const float* base
                                            0x00020000);
 }
 
+// Row of (request b, head slot vh) in q and out.  With sq query tokens per
+// request (the short verifier) the kernel's Hq heads are Hq / sq query heads
+// times sq tokens: vh = head * sq + token, stored token-major
+// ([B][sq][Hq / sq][D]); sq = 1 is single-query decode ([B][Hq][D]).
+__device__ __forceinline__ size_t qrow(int b, int vh, int Hq, int sq) {
+  return ((size_t)b * sq + vh % sq) * (Hq / sq) + vh / sq;
+}
+
 // Log-sum-exp combine of the split records of heads h0 .. h0+nh-1 (nh <= 4)
 // of request b: M = max m_s, w_s = l_s 2^(m_s - M), o = sum w_s o_s / sum w_s.
 // WPH waves per head: wave w combines dims [D/WPH (w % WPH), +D/WPH) of head
@@ -349,8 +357,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t records_rsrc(const float* base
 // shuffles.  Records: [max_splits][D + 4] fp32 per head (o/l in 0..D-1, m at
 // D, l at D+1).
 template <int D, int WPH>
-__device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int h0, int nh,
-                               int max_splits, int S) {
+__device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int sq, int h0,
+                               int nh, int max_splits, int S) {
   constexpr int DW = D / WPH;     // dims per wave
   constexpr int CPL = DW / 4;     // float4 chunks per wave
   constexpr int KP = 64 / CPL;    // lanes per chunk (split parts)
@@ -412,7 +420,7 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
   }
   if (k == 0) {
     const float r = den > 0.0f ? 1.0f / den : 0.0f;
-    __half2* dst = reinterpret_cast<__half2*>(out + ((size_t)b * Hq + h0 + h) * D + d0 + 4 * c);
+    __half2* dst = reinterpret_cast<__half2*>(out + qrow(b, h0 + h, Hq, sq) * D + d0 + 4 * c);
     dst[0] = __floats2half2_rn(num[0] * r, num[1] * r);
     dst[1] = __floats2half2_rn(num[2] * r, num[3] * r);
   }
@@ -448,8 +456,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     const uint4* __restrict__ k_new, const uint4* __restrict__ v_new,
     const __half* __restrict__ q, const int32_t* __restrict__ block_tables,
     const int32_t* __restrict__ seq_lens, float* __restrict__ ws, uint32_t* __restrict__ tickets,
-    __half* __restrict__ out, int Hq, int Hkv, int P, int NP, int max_pages, int max_splits,
-    int split_cap, int n_hchunks, float scale_log2) {
+    __half* __restrict__ out, int Hq, int sq, int Hkv, int P, int NP, int max_pages,
+    int max_splits, int split_cap, int n_hchunks, float scale_log2) {
   constexpr int kWaves = waves_for<D>();
   constexpr int kThreads = 64 * kWaves;
   constexpr int NG = D / G;                // scale groups per head
@@ -500,7 +508,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   uint4 qraw[NHALF][WQ];
   {
     const uint4* src = reinterpret_cast<const uint4*>(
-        q + ((size_t)b * Hq + h0 + min(hs, nh - 1)) * D + DQ * q4);
+        q + qrow(b, h0 + min(hs, nh - 1), Hq, sq) * D + DQ * q4);
 #pragma unroll
     for (int e = 0; e < NHALF; ++e)
 #pragma unroll
@@ -525,7 +533,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   if (L <= 0) {  // an empty request: all-zero output rows, written by split 0
     if (split == 0)
       for (int i = tid; i < nh * D; i += kThreads)
-        out[((size_t)b * Hq + h0) * D + i] = __float2half(0.0f);
+        out[qrow(b, h0 + i / D, Hq, sq) * D + i % D] = __float2half(0.0f);
     return;
   }
   const int n_pages = (L + P - 1) / P;
@@ -534,6 +542,10 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   int pb, pe;
   split_range(n_pages, S, split, pb, pe);
   const int t_end = min(pe * P, L);
+  // causal limits of the verifier: token k of sq sees positions < L - sq + 1
+  // + k (its own and those before it); rows below t_full need no mask
+  const int t_full = min(t_end, L - sq + 1);
+  const int t_lim = min(t_end, L - sq + 1 + (h0 + min(hs, nh - 1)) % sq);
   const int rows_per_page = P / kRowPos;
 
   // this wave's rows: the split's rows in page order, wave, wave + kWaves, ...
@@ -804,7 +816,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
       }
     }
     const bool pg_ok = stage_ok[ST];
-    const bool full = pg_ok && t_row + kRowPos <= t_end;  // wave-uniform
+    const bool full = pg_ok && t_row + kRowPos <= t_full;  // wave-uniform
 
     uint32_t kw[NHALF][2][WQ];   // K code words [half][tile][step]
     uint32_t kmw[NHALF][2][4];   // K (scale, bias) of positions 8 q4 + 4 t + i
@@ -891,7 +903,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const bool ok = pg_ok && t_row + 8 * q4 + 4 * t + i < t_end;
+          const bool ok = pg_ok && t_row + 8 * q4 + 4 * t + i < t_lim;
           sc[t][i] = ok ? sc[t][i] : -INFINITY;
 #pragma unroll
           for (int e = 0; e < NHALF; ++e) vmw[e][t][i] = ok ? vmw[e][t][i] : 0u;
@@ -1059,7 +1071,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   if (s_ticket != (uint32_t)(S - 1)) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  combine_splits<D, kWaves / kHeadSlots>(ws, out, b, Hq, h0, nh, max_splits, S);
+  combine_splits<D, kWaves / kHeadSlots>(ws, out, b, Hq, sq, h0, nh, max_splits, S);
 }
 
 template <int D, int G, bool APPEND>
@@ -1067,7 +1079,7 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
                     const void* v_new, const void* q,
                     int32_t B, int32_t Hq, const int32_t* bt, int32_t max_pages,
                     const int32_t* lens, float scale, int32_t max_splits, uint32_t* tickets,
-                    float* records, void* out, hipStream_t stream) {
+                    float* records, void* out, int32_t sq, hipStream_t stream) {
   const int gq = Hq / L.num_kv_heads;
   const int n_hchunks = (gq + kHeadSlots - 1) / kHeadSlots;
   // Splits per request: enough blocks for one per CU when one request runs
@@ -1083,7 +1095,7 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
                      static_cast<uint8_t*>(pool.v_codes), static_cast<uint32_t*>(pool.v_meta),
                      static_cast<const uint4*>(k_new), static_cast<const uint4*>(v_new),
                      static_cast<const __half*>(q),
-                     bt, lens, records, tickets, static_cast<__half*>(out), Hq,
+                     bt, lens, records, tickets, static_cast<__half*>(out), Hq, (int)sq,
                      L.num_kv_heads, L.page_size, L.num_pages, max_pages, max_splits, split_cap,
                      n_hchunks,
                      scale * kLog2e);
@@ -1112,9 +1124,10 @@ namespace {
 hipError_t dispatch(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
                     const void* v_new, const void* q, int32_t B, int32_t Hq, const int32_t* bt,
                     int32_t max_pages, const int32_t* lens, float scale, int32_t max_splits,
-                    uint32_t* tickets, float* records, void* out, hipStream_t stream) {
+                    uint32_t* tickets, float* records, void* out, int32_t sq,
+                    hipStream_t stream) {
 #define JF_ARGS L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale, max_splits, tickets, \
-                records, out, stream
+                records, out, sq, stream
 #define JF_CASE(D_, G_)                                              \
   if (L.head_dim == D_ && L.group_size == G_)                        \
     return k_new ? launch_t<D_, G_, true>(JF_ARGS) : launch_t<D_, G_, false>(JF_ARGS);
@@ -1135,12 +1148,13 @@ hipError_t dispatch(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
 hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
                          const void* v_new, const void* q, int32_t B, int32_t Hq,
                          const int32_t* bt, int32_t max_pages, const int32_t* lens, float scale,
-                         int32_t max_splits, void* ws, void* out, hipStream_t stream) {
+                         int32_t max_splits, void* ws, void* out, hipStream_t stream,
+                         int32_t sq) {
   // completion counters first, then the split records
   uint32_t* tickets = static_cast<uint32_t*>(ws);
   float* records = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kDecodeCounterBytes);
   return dispatch(L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale, max_splits,
-                  tickets, records, out, stream);
+                  tickets, records, out, sq, stream);
 }
 
 // ---- the decode step without a caller workspace: its completion counters
@@ -1192,7 +1206,7 @@ hipError_t launch_decode_static(const jf_kv_layout& L, const jf_kv_pool_ptrs& po
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return dispatch(L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale, max_splits,
-                  tickets, records, out, stream);
+                  tickets, records, out, 1, stream);
 }
 
 }  // namespace jfkv

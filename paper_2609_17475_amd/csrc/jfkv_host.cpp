@@ -445,6 +445,31 @@ jf_status jf_decode_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* p
                        workspace_bytes, out, stream);
 }
 
+jf_status jf_verify_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                            const void* q, int32_t B, int32_t num_queries, int32_t num_q_heads,
+                            const int32_t* block_tables, int32_t max_pages,
+                            const int32_t* seq_lens, float softmax_scale, int32_t max_splits,
+                            void* workspace, size_t workspace_bytes, void* out,
+                            hipStream_t stream) {
+  jf_status st = check_decode_args(layout, pool, q, B, num_q_heads, block_tables, max_pages,
+                                   seq_lens, softmax_scale, max_splits, out);
+  if (st) return st;
+  if (!workspace) return fail(JF_ERR_INVALID, "NULL device pointer");
+  if (num_queries < 1 || num_queries > 4)
+    return fail(JF_ERR_UNSUPPORTED, "num_queries %d outside 1..4", num_queries);
+  const int64_t heads = (int64_t)num_q_heads * num_queries;
+  if (heads > INT32_MAX) return fail(JF_ERR_INVALID, "num_q_heads * num_queries overflows");
+  size_t need = 0;
+  if ((st = jf_decode_workspace_bytes(B, (int32_t)heads, layout->head_dim, max_splits, &need)))
+    return st;
+  if (workspace_bytes < need)
+    return fail(JF_ERR_INVALID, "workspace %zu bytes < required %zu", workspace_bytes, need);
+  return device_status(jfkv::launch_decode(*layout, *pool, nullptr, nullptr, q, B, (int32_t)heads,
+                                           block_tables, max_pages, seq_lens, softmax_scale,
+                                           max_splits, workspace, out, stream, num_queries),
+                       "verify launch");
+}
+
 jf_status jf_decode_step_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
                             const void* k_new, const void* v_new, const void* q, int32_t B,
                             int32_t num_q_heads, const int32_t* block_tables,

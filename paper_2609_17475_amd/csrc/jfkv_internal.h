@@ -45,14 +45,15 @@ hipError_t launch_quantize_append(const jf_kv_layout& L, const jf_kv_pool_ptrs& 
                                   hipStream_t stream);
 
 // k_new/v_new non-null: the fused decode step (append one row per request
-// at position seq_lens[b] - 1, then attend).
+// at position seq_lens[b] - 1, then attend).  sq > 1 (k_new null): the
+// short verifier, num_q_heads = query heads * sq (q and out token-major).
 hipError_t launch_decode(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
                          const void* k_new, const void* v_new,
                          const void* q, int32_t B, int32_t num_q_heads,
                          const int32_t* block_tables, int32_t max_pages,
                          const int32_t* seq_lens, float softmax_scale,
                          int32_t max_splits, void* workspace, void* out,
-                         hipStream_t stream);
+                         hipStream_t stream, int32_t sq = 1);
 
 // The same step with its counters and records in the library's static
 // device array (the caller passes no workspace).

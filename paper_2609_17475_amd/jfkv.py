@@ -27,7 +27,7 @@ EXPORTS = [
     "jf_page_table_set_length", "jf_page_table_release", "jf_page_table_export",
     "jf_page_table_stats", "jf_page_table_info",
     "jf_kv_quantize_append", "jf_decode_workspace_bytes", "jf_decode_attn_q4",
-    "jf_decode_step_q4", "jf_decode_step_q4_static", "jf_prefill_attn_q4",
+    "jf_verify_attn_q4", "jf_decode_step_q4", "jf_decode_step_q4_static", "jf_prefill_attn_q4",
     "jf_tq4_pool_bytes", "jf_tq4_encode_append", "jf_tq4_decode_attn",
 ]
 
@@ -80,6 +80,8 @@ def _load():
         "jf_decode_workspace_bytes": (st, [i32, i32, i32, i32, ctypes.POINTER(sz)]),
         "jf_decode_attn_q4": (st, [P, P, P, i32, i32, P, i32, P, ctypes.c_float, i32, P, sz, P,
                                    P]),
+        "jf_verify_attn_q4": (st, [P, P, P, i32, i32, i32, P, i32, P, ctypes.c_float, i32, P, sz,
+                                   P, P]),
         "jf_decode_step_q4": (st, [P, P, P, P, P, i32, i32, P, i32, P, ctypes.c_float, i32, P, sz,
                                    P, P]),
         "jf_decode_step_q4_static": (st, [P, P, P, P, P, i32, i32, P, i32, P, ctypes.c_float,
@@ -304,6 +306,30 @@ def jf_decode_attn_q4(pool: KVPool, q, block_tables, seq_lens, softmax_scale: fl
                                  _stream(stream)))
 
 
+def jf_verify_attn_q4(pool: KVPool, q, block_tables, seq_lens, softmax_scale: float,
+                      max_splits: int, workspace, out, stream=None):
+    """Short packed verification: q, out fp16 [B][Sq][Hq][d] (Sq = 1..4); token
+    k of request b sees positions 0 .. seq_lens[b] - Sq + k."""
+    import torch
+    _dev_check(q, "q", torch.float16)
+    _dev_check(block_tables, "block_tables", torch.int32)
+    _dev_check(seq_lens, "seq_lens", torch.int32)
+    _dev_check(workspace, "workspace")
+    _dev_check(out, "out", torch.float16)
+    if q.dim() != 4 or q.shape[3] != pool.layout.head_dim or out.shape != q.shape:
+        raise ValueError("q/out must be [B][Sq][Hq][head_dim]")
+    B, Sq, Hq, _ = q.shape
+    if block_tables.dim() != 2 or block_tables.shape[0] != B or seq_lens.shape[0] != B:
+        raise ValueError("block_tables [B][max_pages], seq_lens [B]")
+    lay = pool.layout
+    ptrs = pool.ptrs()
+    _check(lib.jf_verify_attn_q4(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), B, Sq, Hq,
+                                 _ptr(block_tables), block_tables.shape[1], _ptr(seq_lens),
+                                 float(softmax_scale), int(max_splits), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _ptr(out),
+                                 _stream(stream)))
+
+
 def jf_decode_step_q4(pool: KVPool, k_new, v_new, q, block_tables, seq_lens,
                       softmax_scale: float, max_splits: int, workspace, out, stream=None):
     """Append request b's row (k_new/v_new fp16 [B][Hkv][d]) at position
@@ -423,6 +449,21 @@ def bind_decode_step(pool: KVPool, k_new, v_new, q, block_tables, seq_lens, soft
             _ptr(out), _stream(stream))
     return BoundCall(lib.jf_decode_step_q4, args,
                      (lay, ptrs, pool, k_new, v_new, q, block_tables, seq_lens, workspace, out))
+
+
+def bind_verify(pool: KVPool, q, block_tables, seq_lens, softmax_scale, max_splits, workspace,
+                out, stream=None) -> BoundCall:
+    """jf_verify_attn_q4 with its arguments marshalled once (q, out [B][Sq][Hq][d])."""
+    lay, ptrs = pool.layout, pool.ptrs()
+    if q.dim() != 4 or out.shape != q.shape or q.shape[3] != lay.head_dim:
+        raise ValueError("q/out must be [B][Sq][Hq][head_dim]")
+    B, Sq, Hq, _ = q.shape
+    args = (ctypes.byref(lay), ctypes.byref(ptrs), _ptr(q), B, Sq, Hq, _ptr(block_tables),
+            block_tables.shape[1], _ptr(seq_lens), float(softmax_scale), int(max_splits),
+            _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(out),
+            _stream(stream))
+    return BoundCall(lib.jf_verify_attn_q4, args,
+                     (lay, ptrs, pool, q, block_tables, seq_lens, workspace, out))
 
 
 def bind_prefill(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len, softmax_scale, out,

@@ -24,6 +24,9 @@ for them.  Shapes follow the paper's page geometry (256-token pages, Background
                    pages), 32/8 heads, then appended as 8 new pages.
   tq4_decode_256k  the paper's geometry and codec: 24/4 heads, d=256, 262,144
                    positions in 1,024 shuffled pages of TQ4 vectors.
+  verify_256k      decode_256k's cache with 3 query tokens per request (the
+                   paper's verification width: two proposed tokens and a
+                   bonus position), causal among them.
 
 Recipe (fixed draw order, numpy PCG64 ``default_rng(seed)``):
   1. K then V: float32 N(0,1), shape [n_rows][Hkv][d];
@@ -59,6 +62,7 @@ class Workload:
     chunk: int = 0           # prefill chunk rows (prefill workloads)
     steps: int = 0           # sequential decode steps (loop workloads)
     max_splits: int = 64
+    queries: int = 1         # query tokens per request (the short verifier: 2..4)
     page_size: int = PAGE_SIZE
     group_size: int = GROUP_SIZE
 
@@ -75,6 +79,7 @@ WORKLOADS = {
     # the paper's own geometry and format (24 query heads over 4 KV heads,
     # d = 256, TQ4 pages) at its full native window
     "tq4_decode_256k": Workload("tq4_decode_256k", 24, 4, 256, (262144,), 1024 + 8, 5, seed=6),
+    "verify_256k": Workload("verify_256k", 32, 8, 128, (262144,), 1024 + 8, 3, seed=7, queries=3),
 }
 
 

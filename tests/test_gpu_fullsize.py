@@ -137,6 +137,41 @@ def test_decode_256k_full():
     log("  max err %.2e rel L2 %.2e" % (err, rel))
 
 
+def test_verify_256k_full():
+    """The short verifier in the bench's configuration: 32 q / 8 KV heads,
+    262,144 positions in 1,024 shuffled pages whose last three positions are
+    the three query tokens (appended with the cache); pools byte-equal to the
+    oracle's; tokens 0 and 2 (the shortest and the longest causal window)
+    against the oracle's decode of all 32 heads over L - 2 and L positions."""
+    wl = workloads.WORKLOADS["verify_256k"]
+    log("fullsize verify_256k")
+    P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
+    L, sq = wl.seq_lens[0], wl.queries
+    pools = Pools(P, hkv, d, G, wl.pool_pages)
+    pp = jfkv.PagePool(wl.pool_pages, P, shuffle_seed=wl.seed)
+    s = pp.create()
+    pp.reserve(s, L)
+    table = np.array(pp.export([s], L // P)[0], np.int32)
+    k, v = workloads.gen_kv_device(wl.seed, L, hkv, d, wl.n_outlier, DEV)
+    q = workloads.gen_q_device(wl.seed + 1, sq, hq, d, DEV)[None]  # [1][sq][hq][d]
+    pools.append(k, v, [0, L], [0], table)
+    pools.assert_equal("verify_256k")
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(1, hq * sq, d, wl.max_splits),
+                     dtype=torch.uint8, device=DEV)
+    out = torch.empty_like(q)
+    jfkv.jf_verify_attn_q4(pools.gpu, q, torch.from_numpy(table).to(DEV), _i32([L]), 1.0,
+                           wl.max_splits, ws, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    qh = q.cpu().numpy()
+    for t in (0, sq - 1):
+        log("  oracle token %d" % t)
+        ref = oracle.decode(pools.host, np.ascontiguousarray(qh[:, t]), table,
+                            [L - sq + 1 + t], 1.0)
+        err, rel = check_tol(got[:, t], ref, rel_elem=2.0 ** -11, what="verify_256k token %d" % t)
+        log("  token %d max err %.2e rel L2 %.2e" % (t, err, rel))
+
+
 def test_ragged_shared_prefix_full():
     """Two requests of 196,608 and 131,072 cached positions whose first
     32,768 positions are one physical copy (forked pages, reference count 2),
