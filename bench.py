@@ -331,7 +331,8 @@ def bench_decode_steps(name, args):
     window = name == "decode_256k" and L0 == wl.seq_lens[0]
     label = name if (name != "decode_256k" or window) else "decode_%d" % L0
     split_cap = min(args.max_splits,
-                    -(-torch.cuda.get_device_properties(0).multi_processor_count // hkv))
+                    max(1, torch.cuda.get_device_properties(0).multi_processor_count
+                        // (hkv * -(-(hq // hkv) // 4))))
     result = {
         "metric": METRIC if window else "decode-attn KV positions/s/layer (%s)" % label,
         "value": logical / (wall_us * 1e-6), "unit": "KV positions/s/layer", "n_gpus": 1,

@@ -77,6 +77,7 @@ constexpr float kMinit = -1e30f;
 constexpr int kMaxThreads = 512;    // a block: one split, one block per CU
 constexpr int kRowPos = 32;         // positions per row: two 16-position MFMA tiles
 constexpr int kHeadSlots = 4;       // query heads per block
+constexpr int kXcds = 8;            // XCDs of the chip (block placement only)
 constexpr int kRingBudget = 162816; // LDS bytes of a block's rings (a CU's LDS less 1 KiB)
 // Waves per block: two per SIMD where the LDS rings fit (d <= 128), so one
 // wave computes while the other waits on its page loads; the waves meet at a
@@ -484,8 +485,26 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t smem[kWaves][kStages][kStageBytes];
   __shared__ uint32_t s_ticket;
 
-  const int kv = blockIdx.y / n_hchunks;
-  const int hc = blockIdx.y % n_hchunks;
+  // Block -> (split, KV head, head chunk).  One head chunk: x = split,
+  // y = KV head.  Several chunks read the same pages, so their blocks are
+  // placed on one XCD (blocks are dealt to the XCDs in turn by linear ID):
+  // x = group * (kXcds * n_hchunks) + hc * kXcds + lane, where slot
+  // group * kXcds + lane is (split, KV head); the chunks of a slot then share
+  // that XCD's L2 while they stream the same rows.
+  int split, kv, hc;
+  if (n_hchunks == 1) {
+    split = blockIdx.x;
+    kv = blockIdx.y;
+    hc = 0;
+  } else {
+    const int per = kXcds * n_hchunks;
+    const int g = blockIdx.x / per, r = blockIdx.x % per;
+    const int slot = g * kXcds + r % kXcds;
+    hc = r / kXcds;
+    split = slot % split_cap;
+    kv = slot / split_cap;
+    if (kv >= Hkv) return;  // padding of the last group
+  }
   const int b = blockIdx.z;
   const int gq = Hq / Hkv;
   const int h0 = kv * gq + hc * kHeadSlots;
@@ -493,7 +512,6 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
-  const int split = blockIdx.x;
 
   const int l16 = lane & 15, q4 = lane >> 4;
   const int hs = l16 & 3, gs = l16 >> 2;  // accumulator column: head slot, column slot
@@ -1088,8 +1106,13 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
   // (they are on the device).
   const int64_t per_split = (int64_t)L.num_kv_heads * n_hchunks;
   const int split_cap =
-      (int)std::max<int64_t>(1, std::min<int64_t>(max_splits, (jfkv::num_cus() + per_split - 1) / per_split));
-  dim3 grid(split_cap, L.num_kv_heads * n_hchunks, B);
+      (int)std::max<int64_t>(1, std::min<int64_t>(max_splits, jfkv::num_cus() / per_split));
+  // several head chunks: one x index per (split, KV head, chunk), grouped by
+  // XCD (the kernel decodes it)
+  const int64_t slots = (int64_t)split_cap * L.num_kv_heads;
+  dim3 grid = n_hchunks == 1
+                  ? dim3(split_cap, L.num_kv_heads, B)
+                  : dim3((uint32_t)(((slots + kXcds - 1) / kXcds) * kXcds * n_hchunks), 1, B);
   hipLaunchKernelGGL((decode_kernel<D, G, APPEND>), grid, dim3(64 * waves_for<D>()), 0, stream,
                      static_cast<uint8_t*>(pool.k_codes), static_cast<uint32_t*>(pool.k_meta),
                      static_cast<uint8_t*>(pool.v_codes), static_cast<uint32_t*>(pool.v_meta),
