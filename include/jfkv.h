@@ -343,6 +343,28 @@ jf_status jf_prefill_attn_q4(const jf_kv_layout* layout,
                              int32_t prefix_len, float softmax_scale,
                              void* out, hipStream_t stream);
 
+/* Page -> operand reconstruction of one head group for an SDPA-style
+ * consumer (Background, "Stored format is not execution format", eq.
+ * layerbytes; Sec. 3.1, "Finish one head group before starting the next",
+ * eq. groupattention): the dequantized K and V vectors of KV heads
+ * kv0 .. kv0 + num_heads - 1 at logical positions 0 .. n_pos - 1 of one
+ * request, read through block_table, written as contiguous operands.  A
+ * grouped prefill reconstructs one group (the paper's: two KV heads),
+ * attends with that group's query heads, and reuses the same
+ * 2 * num_heads * n_pos * d * 2 bytes for the next group.
+ *   block_table  int32 [max_pages] (device); n_pos <= max_pages * page_size
+ *   k_out, v_out fp16 [num_heads][n_pos][d] (device, 16-byte aligned,
+ *                caller-owned); element = scale * code + bias rounded once to
+ *                fp16 (nearest, ties to even: the exact value's rounding,
+ *                not a rounding of an fp32 intermediate)
+ * A page ID outside [0, num_pages) gives zero vectors.  n_pos = 0 launches
+ * nothing. */
+jf_status jf_reconstruct_q4(const jf_kv_layout* layout,
+                            const jf_kv_pool_ptrs* pool,
+                            const int32_t* block_table, int32_t max_pages,
+                            int32_t n_pos, int32_t kv0, int32_t num_heads,
+                            void* k_out, void* v_out, hipStream_t stream);
+
 /* ---------------------------------------------------------------- TQ4
  * The paper's own 4-bit format (Sec. 3.1, eq. codec; Appendix A, Table
  * codec): a 256-element vector x is stored as the fp16 norm of x and 256
@@ -424,6 +446,24 @@ jf_status jf_tq4_decode_attn(const jf_kv_layout* layout, const void* k_words,
                              int32_t max_splits, void* workspace,
                              size_t workspace_bytes, void* out,
                              hipStream_t stream);
+
+/* TQ4 page -> operand reconstruction (Appendix A, Table codec: page lookup,
+ * index unpacking, centroid lookup, inverse rotation and norm restoration
+ * in one kernel; Sec. 3.1, eq. groupattention): x_hat = norm * S H_256
+ * c[z] / 16 for KV heads kv0 .. kv0 + num_heads - 1 at logical positions
+ * 0 .. n_pos - 1 of one request, as contiguous fp16 k_out, v_out
+ * [num_heads][n_pos][256] (device, 8-byte aligned).  Arithmetic in fp32
+ * (centroids as given, the transform's sums, then signs and norm / 16),
+ * rounded once to fp16.  Pool, signs and centroids as in
+ * jf_tq4_decode_attn; block_table int32 [max_pages] (device).  A page ID
+ * outside [0, num_pages) gives zero vectors. */
+jf_status jf_tq4_reconstruct(const jf_kv_layout* layout, const void* k_words,
+                             const void* k_norms, const void* v_words,
+                             const void* v_norms, const float* k_signs,
+                             const float* v_signs, const float* centroids,
+                             const int32_t* block_table, int32_t max_pages,
+                             int32_t n_pos, int32_t kv0, int32_t num_heads,
+                             void* k_out, void* v_out, hipStream_t stream);
 
 #ifdef __cplusplus
 }

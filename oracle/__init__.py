@@ -63,6 +63,10 @@ def lib():
             L.jfo_half_to_double.restype = ctypes.c_double
             L.jfo_float_to_half.argtypes = [ctypes.c_float, ctypes.c_int]
             L.jfo_float_to_half.restype = ctypes.c_uint16
+            L.jfo_double_to_half.argtypes = [ctypes.c_double, ctypes.c_int]
+            L.jfo_double_to_half.restype = ctypes.c_uint16
+            L.jfo_reconstruct.argtypes = [P, P, P, ctypes.c_int, P, i32, i32, i32, i32, P]
+            L.jfo_reconstruct.restype = ctypes.c_int
             L.jfo_quantize_group.argtypes = [P, i32, P, P, P]
             L.jfo_quantize_group.restype = None
             L.jfo_quantize_groups.argtypes = [P, ctypes.c_int64, i32, P, P, P]
@@ -116,6 +120,11 @@ def half_to_double(bits: int) -> float:
 def float_to_half(f: float, mode: int) -> int:
     """mode 0 = nearest-even, 1 = toward -inf, 2 = toward +inf; returns bits."""
     return lib().jfo_float_to_half(float(np.float32(f)), int(mode))
+
+
+def double_to_half(x: float, mode: int = 0) -> int:
+    """The same rounding of a binary64 value; returns bits."""
+    return lib().jfo_double_to_half(float(x), int(mode))
 
 
 # ---------------------------------------------------------------- quantizer
@@ -197,6 +206,28 @@ def decode(pool: Pool, q, block_tables, seq_lens, alpha: float) -> np.ndarray:
     if rc != 0:
         raise ValueError("oracle decode: invalid arguments")
     return out
+
+
+def reconstruct(pool: Pool, block_table, n_pos: int, kv0: int, g: int):
+    """Page -> operand reconstruction of one head group (Background, eq.
+    layerbytes; Sec. 3.1, eq. groupattention): (K, V) fp16 [g][n_pos][d], the
+    dequantized vectors of KV heads kv0 .. kv0+g-1 at logical positions
+    0 .. n_pos-1 of one request (block_table [max_pages]), each element the
+    exact value rounded once to fp16 (nearest even); pages outside the pool
+    give zeros."""
+    bt = _i32(block_table).reshape(-1)
+    d = pool.layout.head_dim
+    res = []
+    for is_v, (codes, meta) in enumerate(((pool.k_codes, pool.k_meta),
+                                          (pool.v_codes, pool.v_meta))):
+        out = np.zeros((g, n_pos, d), np.uint16)
+        rc = lib().jfo_reconstruct(ctypes.byref(pool.layout), _ptr(codes), _ptr(meta), is_v,
+                                   _ptr(bt), bt.shape[0], int(n_pos), int(kv0), int(g),
+                                   _ptr(out))
+        if rc != 0:
+            raise ValueError("oracle reconstruct: invalid arguments")
+        res.append(out.view(np.float16))
+    return res[0], res[1]
 
 
 def verify(pool: Pool, q, block_tables, seq_lens, alpha: float) -> np.ndarray:

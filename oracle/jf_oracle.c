@@ -68,13 +68,13 @@ static uint16_t half_floor_pattern(double a) {
   return lo;
 }
 
-/* Round the (exactly representable in binary64) binary32 value f to
- * binary16.  Candidates are the two neighbours of |f|; "away" is the larger
- * magnitude.  Beyond the largest finite value the upper neighbour is
- * infinity, which round-to-nearest reaches from 65520 up (the halfway point
- * to 2^16, where the next binade would start). */
-uint16_t jfo_float_to_half(float f, int mode) {
-  double x = (double)f;
+/* Round the binary64 value x to binary16.  Candidates are the two
+ * neighbours of |x|; "away" is the larger magnitude.  Beyond the largest
+ * finite value the upper neighbour is infinity, which round-to-nearest
+ * reaches from 65520 up (the halfway point to 2^16, where the next binade
+ * would start).  The distances to the neighbours are exact: the neighbours
+ * and every binary64 value in their range are dyadic with few enough bits. */
+uint16_t jfo_double_to_half(double x, int mode) {
   if (isnan(x)) return 0x7e00;
   uint16_t sign = signbit(x) ? 0x8000 : 0;
   double a = fabs(x);
@@ -104,6 +104,9 @@ uint16_t jfo_float_to_half(float f, int mode) {
   }
   return (uint16_t)(sign | mag);
 }
+
+/* binary32 input: exact in binary64, so the same rounding. */
+uint16_t jfo_float_to_half(float f, int mode) { return jfo_double_to_half((double)f, mode); }
 
 static float half_to_float(uint16_t h) { return (float)jfo_half_to_double(h); }
 
@@ -270,6 +273,37 @@ void jfo_dequant_vector(const jfo_layout* L, const uint8_t* codes,
     double b = jfo_half_to_double(meta[mi + 1]);
     out[i] = s * (double)get_code(L, codes, is_v, page, kv, slot, i) + b;
   }
+}
+
+/* ------------------------------------------------------------------------
+ * Page -> operand reconstruction of one head group (Background, "Stored
+ * format is not execution format", eq. layerbytes; Sec. 3.1, eq.
+ * groupattention): the dequantized vectors of KV heads kv0 .. kv0 + g - 1 at
+ * logical positions 0 .. n - 1 (page table[t / P], slot t % P), each element
+ * the exact value s * q + b rounded once to binary16 (nearest, ties to even),
+ * written as out[(kv - kv0) * n + t][d].  A page ID outside [0, num_pages)
+ * gives zeros.
+ * ---------------------------------------------------------------------- */
+int jfo_reconstruct(const jfo_layout* L, const uint8_t* codes, const uint16_t* meta, int is_v,
+                    const int32_t* table, int32_t max_pages, int32_t n, int32_t kv0, int32_t g,
+                    uint16_t* out) {
+  int32_t d = L->head_dim, P = L->page_size;
+  if (d <= 0 || d > 512 || n < 0 || kv0 < 0 || g <= 0 || kv0 + g > L->num_kv_heads ||
+      (int64_t)n > (int64_t)max_pages * P)
+    return -1;
+  double x[512];
+  for (int32_t j = 0; j < g; ++j)
+    for (int32_t t = 0; t < n; ++t) {
+      uint16_t* o = out + ((size_t)j * n + t) * d;
+      int32_t page = table[t / P];
+      if (page < 0 || page >= L->num_pages) {
+        for (int32_t i = 0; i < d; ++i) o[i] = 0;
+        continue;
+      }
+      jfo_dequant_vector(L, codes, meta, is_v, page, kv0 + j, t % P, x);
+      for (int32_t i = 0; i < d; ++i) o[i] = jfo_double_to_half(x[i], 0);
+    }
+  return 0;
 }
 
 /* ------------------------------------------------------------------------

@@ -46,6 +46,8 @@ typedef struct {
 double   jfo_half_to_double(uint16_t h);
 /* mode: 0 = round to nearest even, 1 = toward -inf, 2 = toward +inf */
 uint16_t jfo_float_to_half(float f, int mode);
+/* The same rounding of a binary64 value. */
+uint16_t jfo_double_to_half(double x, int mode);
 
 /* ---- one group ----------------------------------------------------------
  * x: G fp16 values.  Writes G unpacked codes (0..15), scale and bias bits. */
@@ -85,6 +87,15 @@ int jfo_quantize_append(const jfo_layout* L, uint8_t* k_codes, uint16_t* k_meta,
 void jfo_dequant_vector(const jfo_layout* L, const uint8_t* codes,
                         const uint16_t* meta, int is_v, int32_t page,
                         int32_t kv, int32_t slot, double* out);
+
+/* Page -> operand reconstruction of KV heads kv0 .. kv0+g-1 over logical
+ * positions 0..n-1 of one request (table: [max_pages]): binary16 bits
+ * out[g][n][d], each element the exact dequantized value rounded to nearest
+ * (ties to even); pages outside [0, num_pages) give zeros.  Returns 0, or
+ * -1 for invalid arguments. */
+int jfo_reconstruct(const jfo_layout* L, const uint8_t* codes, const uint16_t* meta, int is_v,
+                    const int32_t* table, int32_t max_pages, int32_t n, int32_t kv0, int32_t g,
+                    uint16_t* out);
 
 /* Single-query decode for B requests.  q: fp16 [B][Hq][d].  Request b
  * attends to its logical positions 0..seq_lens[b]-1.  out: fp64 [B][Hq][d].

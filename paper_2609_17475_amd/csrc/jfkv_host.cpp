@@ -541,6 +541,50 @@ jf_status jf_prefill_attn_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* 
                        "prefill launch");
 }
 
+namespace {
+
+// Arguments of the page -> operand reconstructions (both formats).
+jf_status check_reconstruct_args(const jf_kv_layout* layout, const int32_t* block_table,
+                                 int32_t max_pages, int32_t n_pos, int32_t kv0,
+                                 int32_t num_heads, void* k_out, void* v_out, uintptr_t align) {
+  if (max_pages <= 0 || n_pos < 0)
+    return fail(JF_ERR_INVALID, "max_pages must be positive and n_pos >= 0");
+  if ((int64_t)n_pos > (int64_t)max_pages * layout->page_size)
+    return fail(JF_ERR_INVALID, "n_pos %d exceeds max_pages %d * page_size %d", n_pos, max_pages,
+                layout->page_size);
+  if (kv0 < 0 || num_heads <= 0 || (int64_t)kv0 + num_heads > layout->num_kv_heads)
+    return fail(JF_ERR_INVALID, "KV heads %d .. %d outside 0 .. %d", kv0, kv0 + num_heads - 1,
+                layout->num_kv_heads - 1);
+  if ((int64_t)num_heads * n_pos > INT32_MAX)
+    return fail(JF_ERR_UNSUPPORTED, "num_heads * n_pos above INT32_MAX vectors");
+  if (n_pos > 0 && (!block_table || !k_out || !v_out))
+    return fail(JF_ERR_INVALID, "NULL device pointer");
+  if (((uintptr_t)k_out | (uintptr_t)v_out) & (align - 1))
+    return fail(JF_ERR_INVALID, "k_out and v_out must be %d-byte aligned", (int)align);
+  return ok();
+}
+
+}  // namespace
+
+jf_status jf_reconstruct_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                            const int32_t* block_table, int32_t max_pages, int32_t n_pos,
+                            int32_t kv0, int32_t num_heads, void* k_out, void* v_out,
+                            hipStream_t stream) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if ((st = check_pool(pool))) return st;
+  if ((st = check_reconstruct_args(layout, block_table, max_pages, n_pos, kv0, num_heads, k_out,
+                                   v_out, 16)))
+    return st;
+  if ((((uintptr_t)pool->k_codes | (uintptr_t)pool->v_codes) & 7) ||
+      (((uintptr_t)pool->k_meta | (uintptr_t)pool->v_meta) & 3))
+    return fail(JF_ERR_INVALID, "pool codes must be 8-byte and meta 4-byte aligned");
+  if (n_pos == 0) return ok();
+  return device_status(jfkv::launch_reconstruct(*layout, *pool, block_table, max_pages, n_pos,
+                                                kv0, num_heads, k_out, v_out, stream),
+                       "reconstruct launch");
+}
+
 // ------------------------------------------------------------------ TQ4
 namespace {
 
@@ -634,6 +678,30 @@ jf_status jf_tq4_decode_attn(const jf_kv_layout* layout, const void* k_words,
                                                block_tables, max_pages, seq_lens, softmax_scale,
                                                max_splits, workspace, out, stream),
                        "tq4_decode launch");
+}
+
+jf_status jf_tq4_reconstruct(const jf_kv_layout* layout, const void* k_words,
+                             const void* k_norms, const void* v_words, const void* v_norms,
+                             const float* k_signs, const float* v_signs, const float* centroids,
+                             const int32_t* block_table, int32_t max_pages, int32_t n_pos,
+                             int32_t kv0, int32_t num_heads, void* k_out, void* v_out,
+                             hipStream_t stream) {
+  jf_status st = check_tq4_layout(layout);
+  if (st) return st;
+  if ((st = check_reconstruct_args(layout, block_table, max_pages, n_pos, kv0, num_heads, k_out,
+                                   v_out, 8)))
+    return st;
+  if (n_pos == 0) return ok();
+  if (!k_words || !k_norms || !v_words || !v_norms || !k_signs || !v_signs || !centroids)
+    return fail(JF_ERR_INVALID, "NULL device pointer");
+  if ((((uintptr_t)k_words | (uintptr_t)v_words) & 3) ||
+      (((uintptr_t)k_norms | (uintptr_t)v_norms) & 1) ||
+      (((uintptr_t)k_signs | (uintptr_t)v_signs) & 15))
+    return fail(JF_ERR_INVALID, "index words 4-byte, norms 2-byte, signs 16-byte aligned");
+  return device_status(jfkv::launch_tq4_reconstruct(*layout, k_words, k_norms, v_words, v_norms,
+                                                    k_signs, v_signs, centroids, block_table,
+                                                    n_pos, kv0, num_heads, k_out, v_out, stream),
+                       "tq4_reconstruct launch");
 }
 
 }  // extern "C"

@@ -63,6 +63,19 @@ hipError_t launch_decode_static(const jf_kv_layout& L, const jf_kv_pool_ptrs& po
                                 int32_t max_pages, const int32_t* seq_lens, float softmax_scale,
                                 int32_t max_splits, void* out, hipStream_t stream);
 
+// Page -> operand reconstruction of KV heads kv0 .. kv0 + num_heads - 1 at
+// positions 0 .. n_pos - 1 of one request: fp16 [num_heads][n_pos][d] K and V.
+hipError_t launch_reconstruct(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
+                              const int32_t* block_table, int32_t max_pages, int32_t n_pos,
+                              int32_t kv0, int32_t num_heads, void* k_out, void* v_out,
+                              hipStream_t stream);
+hipError_t launch_tq4_reconstruct(const jf_kv_layout& L, const void* k_words, const void* k_norms,
+                                  const void* v_words, const void* v_norms, const float* k_signs,
+                                  const float* v_signs, const float* centroids,
+                                  const int32_t* block_table, int32_t n_pos, int32_t kv0,
+                                  int32_t num_heads, void* k_out, void* v_out,
+                                  hipStream_t stream);
+
 hipError_t launch_prefill(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
                           const void* q, const void* k_chunk, const void* v_chunk,
                           int32_t T, int32_t num_q_heads,

@@ -166,9 +166,105 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
   }
 }
 
+// Page -> operand reconstruction of TQ4 vectors (Appendix A, Table codec:
+// page lookup, index unpacking, centroid lookup, inverse rotation, norm
+// restoration in one kernel): x_hat = rho_hat S H_256 c[z] / 16 for KV heads
+// kv0 .. kv0 + g - 1 at logical positions 0 .. n - 1 of one request, written
+// as contiguous fp16 [g][n][256] K (blockIdx.z = 0) or V operands.  One wave
+// per vector, kVecPerWave vectors per wave with their loads issued together;
+// lane l holds elements 4l .. 4l + 3 (its half of index word l / 2), looks
+// their centroids up in LDS and runs the same eight butterfly stages as the
+// encoder (H_256 is symmetric), then multiplies by its signs and rho_hat / 16
+// (fp32) and writes 8 bytes, so a vector's 512 bytes leave in one coalesced
+// store.  A page ID outside the pool gives zeros.
+__global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_reconstruct_kernel(
+    const uint32_t* __restrict__ k_words, const __half* __restrict__ k_norms,
+    const uint32_t* __restrict__ v_words, const __half* __restrict__ v_norms,
+    const float* __restrict__ k_signs, const float* __restrict__ v_signs,
+    const float* __restrict__ centroids, const int32_t* __restrict__ table, int n, int kv0,
+    int Hkv, int P, int NP, uint2* __restrict__ k_out, uint2* __restrict__ v_out) {
+  __shared__ float cent[kLevels];
+  if (threadIdx.x < kLevels) cent[threadIdx.x] = centroids[threadIdx.x];
+  __syncthreads();
+  const bool is_v = blockIdx.z != 0;
+  const uint32_t* words = is_v ? v_words : k_words;
+  const __half* norms = is_v ? v_norms : k_norms;
+  uint2* out = is_v ? v_out : k_out;
+  const int j = blockIdx.y;
+  const int kv = kv0 + j;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int t0 = ((int)blockIdx.x * kWavesPerBlock + wave) * kVecPerWave;
+  if (t0 >= n) return;  // the whole wave
+  const int nv = min(kVecPerWave, n - t0);
+  const float4 sg = reinterpret_cast<const float4*>(is_v ? v_signs : k_signs)[lane];
+
+  uint32_t wd[kVecPerWave];
+  float rho[kVecPerWave];
+  bool ok[kVecPerWave];
+#pragma unroll
+  for (int v = 0; v < kVecPerWave; ++v) {
+    wd[v] = 0u;
+    rho[v] = 0.0f;
+    ok[v] = false;  // outside the pool: zeros
+    if (v < nv) {
+      const int t = t0 + v;
+      const int page = table[t / P];  // wave-uniform
+      ok[v] = (unsigned)page < (unsigned)NP;
+      if (ok[v]) {
+        const int64_t vec = ((int64_t)page * Hkv + kv) * P + (t % P);
+        wd[v] = words[vec * (kD / 8) + (lane >> 1)];
+        rho[v] = __half2float(norms[vec]);
+      }
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < kVecPerWave; ++v) {
+    if (v >= nv) break;
+    const uint32_t q = wd[v] >> (16 * (lane & 1));  // element 4 lane + i at bits 4 i
+    float e0 = cent[q & 15u], e1 = cent[(q >> 4) & 15u];
+    float e2 = cent[(q >> 8) & 15u], e3 = cent[(q >> 12) & 15u];
+    {
+      const float a0 = e0 + e1, a1 = e0 - e1, a2 = e2 + e3, a3 = e2 - e3;
+      e0 = a0 + a2; e1 = a1 + a3; e2 = a0 - a2; e3 = a1 - a3;
+    }
+    stage<1>(e0, e1, e2, e3, lane);
+    stage<2>(e0, e1, e2, e3, lane);
+    stage<4>(e0, e1, e2, e3, lane);
+    stage<8>(e0, e1, e2, e3, lane);
+    stage<16>(e0, e1, e2, e3, lane);
+    stage<32>(e0, e1, e2, e3, lane);
+    const float f = rho[v] * 0.0625f;
+    uint2 o = make_uint2(0u, 0u);
+    if (ok[v]) {
+      o.x = __builtin_bit_cast(uint32_t, __floats2half2_rn(sg.x * e0 * f, sg.y * e1 * f));
+      o.y = __builtin_bit_cast(uint32_t, __floats2half2_rn(sg.z * e2 * f, sg.w * e3 * f));
+    }
+    out[((int64_t)j * n + t0 + v) * (kD / 4) + lane] = o;
+  }
+}
+
 }  // namespace
 
 namespace jfkv {
+
+hipError_t launch_tq4_reconstruct(const jf_kv_layout& L, const void* k_words, const void* k_norms,
+                                  const void* v_words, const void* v_norms, const float* k_signs,
+                                  const float* v_signs, const float* centroids,
+                                  const int32_t* block_table, int32_t n_pos, int32_t kv0,
+                                  int32_t num_heads, void* k_out, void* v_out,
+                                  hipStream_t stream) {
+  if (n_pos == 0) return hipSuccess;
+  constexpr int kPerBlock = kWavesPerBlock * kVecPerWave;
+  dim3 grid((unsigned)((n_pos + kPerBlock - 1) / kPerBlock), (unsigned)num_heads, 2);
+  hipLaunchKernelGGL(tq4_reconstruct_kernel, grid, dim3(64 * kWavesPerBlock), 0, stream,
+                     static_cast<const uint32_t*>(k_words), static_cast<const __half*>(k_norms),
+                     static_cast<const uint32_t*>(v_words), static_cast<const __half*>(v_norms),
+                     k_signs, v_signs, centroids, block_table, n_pos, kv0, L.num_kv_heads,
+                     L.page_size, L.num_pages, static_cast<uint2*>(k_out),
+                     static_cast<uint2*>(v_out));
+  return hipGetLastError();
+}
 
 hipError_t launch_tq4_encode(const jf_kv_layout& L, void* words, void* norms, const void* x,
                              const float* signs, const float* centroids, const int32_t* cu_tok,

@@ -28,7 +28,8 @@ EXPORTS = [
     "jf_page_table_stats", "jf_page_table_info",
     "jf_kv_quantize_append", "jf_decode_workspace_bytes", "jf_decode_attn_q4",
     "jf_verify_attn_q4", "jf_decode_step_q4", "jf_decode_step_q4_static", "jf_prefill_attn_q4",
-    "jf_tq4_pool_bytes", "jf_tq4_encode_append", "jf_tq4_decode_attn",
+    "jf_reconstruct_q4", "jf_tq4_pool_bytes", "jf_tq4_encode_append", "jf_tq4_decode_attn",
+    "jf_tq4_reconstruct",
 ]
 
 
@@ -87,6 +88,8 @@ def _load():
         "jf_decode_step_q4_static": (st, [P, P, P, P, P, i32, i32, P, i32, P, ctypes.c_float,
                                           i32, P, P]),
         "jf_prefill_attn_q4": (st, [P, P, P, P, P, i32, i32, P, i32, i32, ctypes.c_float, P, P]),
+        "jf_reconstruct_q4": (st, [P, P, P, i32, i32, i32, i32, P, P, P]),
+        "jf_tq4_reconstruct": (st, [P, P, P, P, P, P, P, P, P, i32, i32, i32, i32, P, P, P]),
         "jf_tq4_pool_bytes": (st, [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
         "jf_tq4_encode_append": (st, [P, P, P, P, P, P, P, P, P, i32, i32, i32, P]),
         "jf_tq4_decode_attn": (st, [P, P, P, P, P, P, P, P, P, i32, i32, P, i32, P,
@@ -478,6 +481,24 @@ def bind_prefill(pool: KVPool, q, k_chunk, v_chunk, block_table, prefix_len, sof
                      (lay, ptrs, pool, q, k_chunk, v_chunk, block_table, out))
 
 
+def jf_reconstruct_q4(pool: KVPool, block_table, n_pos: int, kv0: int, num_heads: int, k_out,
+                      v_out, stream=None):
+    """K, V of KV heads kv0 .. kv0+num_heads-1 at positions 0..n_pos-1 as fp16
+    k_out, v_out [num_heads][n_pos][d] (block_table int32 [max_pages])."""
+    import torch
+    _dev_check(block_table, "block_table", torch.int32)
+    _dev_check(k_out, "k_out", torch.float16)
+    _dev_check(v_out, "v_out", torch.float16)
+    lay = pool.layout
+    shape = (num_heads, n_pos, lay.head_dim)
+    if tuple(k_out.shape) != shape or tuple(v_out.shape) != shape:
+        raise ValueError("k_out/v_out must be [num_heads][n_pos][head_dim]")
+    ptrs = pool.ptrs()
+    _check(lib.jf_reconstruct_q4(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(block_table),
+                                 block_table.shape[-1], int(n_pos), int(kv0), int(num_heads),
+                                 _ptr(k_out), _ptr(v_out), _stream(stream)))
+
+
 # ---------------------------------------------------------------- TQ4 format
 def tq4_pool_bytes(lay: Layout):
     w, n = ctypes.c_size_t(), ctypes.c_size_t()
@@ -588,3 +609,27 @@ def bind_tq4_decode(k_pool: TQ4Pool, v_pool: TQ4Pool, k_signs, v_signs, centroid
     return BoundCall(lib.jf_tq4_decode_attn, args,
                      (k_pool, v_pool, k_signs, v_signs, centroids, q, block_tables, seq_lens,
                       workspace, out))
+
+
+def jf_tq4_reconstruct(k_pool: TQ4Pool, v_pool: TQ4Pool, k_signs, v_signs, centroids,
+                       block_table, n_pos: int, kv0: int, num_heads: int, k_out, v_out,
+                       stream=None):
+    """x_hat = norm * S H c[z] / 16 of KV heads kv0 .. kv0+num_heads-1 at
+    positions 0..n_pos-1 as fp16 k_out, v_out [num_heads][n_pos][256]."""
+    import torch
+    for t, n, dt in ((k_signs, "k_signs", torch.float32), (v_signs, "v_signs", torch.float32),
+                     (centroids, "centroids", torch.float32),
+                     (block_table, "block_table", torch.int32), (k_out, "k_out", torch.float16),
+                     (v_out, "v_out", torch.float16)):
+        _dev_check(t, n, dt)
+    lay = k_pool.layout
+    if tuple(v_pool.words.shape) != tuple(k_pool.words.shape):
+        raise ValueError("K and V pools must have the same layout")
+    shape = (num_heads, n_pos, lay.head_dim)
+    if tuple(k_out.shape) != shape or tuple(v_out.shape) != shape:
+        raise ValueError("k_out/v_out must be [num_heads][n_pos][head_dim]")
+    _check(lib.jf_tq4_reconstruct(ctypes.byref(lay), _ptr(k_pool.words), _ptr(k_pool.norms),
+                                  _ptr(v_pool.words), _ptr(v_pool.norms), _ptr(k_signs),
+                                  _ptr(v_signs), _ptr(centroids), _ptr(block_table),
+                                  block_table.shape[-1], int(n_pos), int(kv0), int(num_heads),
+                                  _ptr(k_out), _ptr(v_out), _stream(stream)))
