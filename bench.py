@@ -31,6 +31,10 @@ Other workloads (--workload) print their own line:
                    heads, d 256) over 262,144 positions
   verify_256k      the short packed verifier: 3 causal query tokens over
                    decode_256k's 262,144-position cache
+  reconstruct_grouped  page -> operand reconstruction of a 2-KV-head group
+                   over prefill_chunk's prefix (HBM roofline), the grouped
+                   reconstruct + SDPA prefill against the fused prefill, and
+                   TQ4 reconstruction at 196,608 positions
 """
 from __future__ import annotations
 
@@ -871,8 +875,172 @@ def bench_verify(args):
     print(json.dumps(result), flush=True)
 
 
+def bench_reconstruct(args):
+    """reconstruct_grouped: page -> operand reconstruction of one two-KV-head
+    group (the paper's grouping) over prefill_chunk's 65,536-position prefix
+    (8 KV heads, d 128, group 64), HBM roofline over the kernel (per position
+    and head: 2 x (64 + 8) B read, 2 x 256 B written).  Beside it, the
+    grouped prefill the paper runs (reconstruct a group, append the chunk's
+    fp16 rows, SDPA for the group's query heads, next group) against the fused
+    matrix-core prefill on the same chunk: time and incremental peak device
+    memory.  And TQ4 reconstruction at the paper's head-group probe geometry
+    (4 KV heads, d 256, 196,608 positions, groups of two)."""
+    import numpy as np
+    import torch
+    from paper_2609_17475_amd import jfkv, workloads
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS["prefill_chunk"]
+    P, hkv, hq, d, G = wl.page_size, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.group_size
+    p0, T, grp = wl.seq_lens[0], wl.chunk, 2
+    gq = hq // hkv
+    lay = jfkv.layout(P, hkv, d, G, wl.pool_pages)
+    pp = jfkv.PagePool(wl.pool_pages, P, shuffle_seed=wl.seed)
+    s0 = pp.create()
+    pp.reserve(s0, p0 + T)
+    table_np = np.array(pp.export([s0], (p0 + T) // P)[0], np.int32)
+    table = torch.from_numpy(table_np).to(dev)
+    k, v = workloads.gen_kv_device(wl.seed, p0 + T, hkv, d, wl.n_outlier, dev)
+    q = workloads.gen_q_device(wl.seed + 1, T, hq, d, dev)
+    pool = jfkv.KVPool(lay, device=dev)
+    i32 = lambda x: torch.tensor(x, dtype=torch.int32, device=dev)  # noqa: E731
+    jfkv.jf_kv_quantize_append(pool, k[:p0], v[:p0], i32([0, p0]), i32([0]), table)
+    kc, vc = k[p0:].contiguous(), v[p0:].contiguous()
+    t1 = table[0].contiguous()
+    kr = torch.empty((grp, p0, d), dtype=torch.float16, device=dev)
+    vr = torch.empty_like(kr)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def recon(j):
+        jfkv.jf_reconstruct_q4(pool, t1, p0, grp * j, grp, kr, vr, stream)
+
+    n_groups = hkv // grp
+    steps = max(4, args.steps // 4) * n_groups
+    # one group per call, the groups in turn, back to back
+    t_rec, wall = _back_to_back(lambda s: recon(s % n_groups), args.warmup, steps, stream)
+    per_pos_head = 2 * (d // 2 + 4 * d // G) + 2 * 2 * d
+    nbytes = grp * p0 * per_pos_head
+    achieved = nbytes / (t_rec * 1e-6) / 1e9
+    vectors = 2 * grp * p0
+    result = {
+        "metric": "page->operand reconstruction, K+V vectors/s (2-KV-head group, 65,536 "
+                  "positions, d 128, group 64)",
+        "value": vectors / (t_rec * 1e-6), "unit": "vectors/s", "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": wall / 1e3, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u4 codes -> f16 (exact rounding)",
+        "data": "synthetic",
+        "config": {"workload": "reconstruct_grouped", "positions": p0, "group_kv_heads": grp,
+                   "num_kv_heads": hkv, "head_dim": d, "page_size": P, "group_size": G,
+                   "operand_bytes": 2 * grp * p0 * d * 2},
+        "us_per_step": {"reconstruct_group": t_rec, "wall": wall},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "reconstruct_kernel (K and V in one launch)",
+                     "algorithmic_bytes": nbytes, "bytes_per_position_and_head": per_pos_head}}
+    log("reconstruct group: %.2f us, %.0f GB/s" % (t_rec, achieved))
+
+    # grouped prefill (reconstruct + SDPA per group) against the fused prefill
+    mask = torch.ones((T, p0 + T), dtype=torch.bool, device=dev)
+    mask[:, p0:] = torch.tril(torch.ones((T, T), dtype=torch.bool, device=dev))
+    mask4 = mask[None, None]
+    out_g = torch.empty((T, hq, d), dtype=torch.float16, device=dev)
+    out_f = torch.empty_like(out_g)
+
+    def grouped():
+        from torch.nn.attention import SDPBackend, sdpa_kernel
+        for j in range(n_groups):
+            recon(j)
+            # the group's K/V rows for each of its query heads (the backend
+            # takes no grouped heads)
+            K = torch.cat([kr, kc[:, grp * j:grp * (j + 1)].transpose(0, 1)], 1)
+            V = torch.cat([vr, vc[:, grp * j:grp * (j + 1)].transpose(0, 1)], 1)
+            K = K.repeat_interleave(gq, 0)[None]
+            V = V.repeat_interleave(gq, 0)[None]
+            Q = q[:, grp * j * gq:grp * (j + 1) * gq].transpose(0, 1)[None].contiguous()
+            with sdpa_kernel([SDPBackend.EFFICIENT_ATTENTION]):
+                O = torch.nn.functional.scaled_dot_product_attention(
+                    Q, K, V, attn_mask=mask4, scale=1.0)
+            out_g[:, grp * j * gq:grp * (j + 1) * gq] = O[0].transpose(0, 1)
+
+    fused = jfkv.bind_prefill(pool, q, kc, vc, t1, p0, 1.0, out_f, stream)
+    cmp = {}
+    try:
+        for name, fn in (("grouped_reconstruct_sdpa", grouped), ("fused_prefill", fused)):
+            fn()
+            torch.cuda.synchronize()
+            base = torch.cuda.memory_allocated()
+            torch.cuda.reset_peak_memory_stats()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            reps = 3
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            cmp[name] = {"ms_per_chunk": e0.elapsed_time(e1) / reps,
+                         "incremental_peak_MiB": (torch.cuda.max_memory_allocated() - base) / 2**20}
+        diff = (out_g.float() - out_f.float()).abs().max().item()
+        cmp["max_abs_diff_between_paths"] = diff
+        cmp["sdpa_backend"] = ("torch efficient attention (fp16, [1,1,T,L] boolean mask, K/V "
+                                "rows repeated per query head)")
+        cmp["chunk"] = T
+        cmp["prefix"] = p0
+    except Exception as e:  # the consumer is torch's; the comparison is a report
+        log("grouped SDPA comparison unavailable: %r" % (e,))
+        cmp = {"error": repr(e)[:200]}
+    result["grouped_prefill_vs_fused"] = cmp
+
+    # TQ4 reconstruction at the paper's probe geometry
+    try:
+        L4, P4, h4 = 196608, 256, 4
+        NP4 = L4 // P4 + 4
+        tnp, (sk, sv) = _tq4_inputs(P4, h4, L4, NP4, 8, dev)
+        t4 = torch.from_numpy(tnp[0]).to(dev)
+        lay4 = jfkv.layout(P4, h4, 256, 64, NP4)
+        cents = torch.linspace(-0.17, 0.17, 16, dtype=torch.float32, device=dev)
+        kp, vp = jfkv.TQ4Pool(lay4, device=dev), jfkv.TQ4Pool(lay4, device=dev)
+        g4 = torch.Generator(device=dev).manual_seed(8)
+        for pl, sg in ((kp, sk), (vp, sv)):
+            x = torch.randn((L4, h4, 256), generator=g4, device=dev, dtype=torch.float32).half()
+            jfkv.jf_tq4_encode_append(pl, x, sg, cents, i32([0, L4]), i32([0]), t4[None])
+            del x
+        k4 = torch.empty((2, L4, 256), dtype=torch.float16, device=dev)
+        v4 = torch.empty_like(k4)
+        t_tq4, _ = _back_to_back(
+            lambda s: jfkv.jf_tq4_reconstruct(kp, vp, sk, sv, cents, t4, L4, 2 * (s % 2), 2, k4,
+                                              v4, stream), args.warmup, steps, stream)
+        b4 = 2 * L4 * 2 * (128 + 2 + 512)
+        result["tq4_reconstruct_group"] = {
+            "positions": L4, "group_kv_heads": 2, "head_dim": 256, "us": t_tq4,
+            "GBs": b4 / (t_tq4 * 1e-6) / 1e9, "frac_of_hbm_peak": b4 / (t_tq4 * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            "operand_MiB_group_of_2": 2 * 2 * L4 * 256 * 2 / 2**20,
+            "operand_MiB_all_4_heads": 2 * 4 * L4 * 256 * 2 / 2**20}
+    except Exception as e:
+        log("tq4 reconstruct timing failed: %r" % (e,))
+        result["tq4_reconstruct_group"] = None
+
+    if args.cpu_seconds > 0:
+        try:  # the oracle's reconstruction of the group over the first positions
+            import oracle
+            n = min(args.cpu_sample or 8192, p0)
+            opool = oracle.Pool(oracle.layout(P, hkv, d, G, wl.pool_pages))
+            oracle.quantize_append(opool, k[:n].cpu().numpy(), v[:n].cpu().numpy(), [0, n], [0],
+                                   table_np)
+            m, dt = _repeat(lambda: oracle.reconstruct(opool, table_np[0], n, 0, grp),
+                            args.cpu_seconds)
+            result["cpu_baseline"] = dict(value=2 * grp * n * m / dt, unit="vectors/s", cores=1,
+                                          kind="oracle", seconds=dt, steps=m,
+                                          sample="K and V of a 2-head group over the first %d "
+                                                 "positions, %d time(s)" % (n, m), **_host())
+        except Exception as e:
+            log("cpu baseline failed: %r" % (e,))
+            result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
 WORKLOADS = ("decode_256k", "decode_4k", "decode_32k_loop", "ragged_2req", "prefill_chunk",
-             "quantize_bulk", "tq4_encode_bulk", "tq4_decode_256k", "verify_256k")
+             "quantize_bulk", "tq4_encode_bulk", "tq4_decode_256k", "verify_256k",
+             "reconstruct_grouped")
 
 
 def main():
@@ -922,6 +1090,8 @@ def main():
         bench_tq4_encode(args)
     elif args.workload == "verify_256k":
         bench_verify(args)
+    elif args.workload == "reconstruct_grouped":
+        bench_reconstruct(args)
     else:
         bench_tq4_decode(args)
 

@@ -576,9 +576,9 @@ jf_status jf_reconstruct_q4(const jf_kv_layout* layout, const jf_kv_pool_ptrs* p
   if ((st = check_reconstruct_args(layout, block_table, max_pages, n_pos, kv0, num_heads, k_out,
                                    v_out, 16)))
     return st;
-  if ((((uintptr_t)pool->k_codes | (uintptr_t)pool->v_codes) & 7) ||
+  if ((((uintptr_t)pool->k_codes | (uintptr_t)pool->v_codes) & 15) ||
       (((uintptr_t)pool->k_meta | (uintptr_t)pool->v_meta) & 3))
-    return fail(JF_ERR_INVALID, "pool codes must be 8-byte and meta 4-byte aligned");
+    return fail(JF_ERR_INVALID, "pool codes must be 16-byte and meta 4-byte aligned");
   if (n_pos == 0) return ok();
   return device_status(jfkv::launch_reconstruct(*layout, *pool, block_table, max_pages, n_pos,
                                                 kv0, num_heads, k_out, v_out, stream),

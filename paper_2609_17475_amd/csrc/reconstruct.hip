@@ -8,20 +8,22 @@
 //
 // Each element is the exact value s * q + b rounded once to fp16.  One fp32
 // FMA gives s * q + b rounded to fp32 (s * q is exact: an 11-bit scale times
-// a 4-bit code); converting that to fp16 rounds a second time, which can
-// differ from rounding the exact value only when the fp32 result lies exactly
-// on an fp16 rounding midpoint (or in fp16's subnormal range, where the
-// midpoint pattern differs).  Those results are detected with two integer
-// tests and recomputed exactly: the fp32 sum's error by TwoSum (exact), the
-// sum rounded to odd in fp32 (toward zero, last bit set when inexact), then
-// to fp16 (rounding to odd with 13 spare bits makes the second rounding
-// exact).
+// a 4-bit code); converting that to fp16 rounds a second time, which differs
+// from rounding the exact value only if the fp32 result was inexact.  It is
+// exact whenever every sum of the group fits fp32's 24 bits: its lowest
+// possible bit is that of s or of b (fp16: 10 bits below the leading one, and
+// not below 2^-24; q is an integer), its highest below 2^e with 2^e above
+// 15 |s| + |b|.  A group failing that test (a tiny bias under a large scale,
+// or the reverse) takes the exact path: the fp32 sum's error by TwoSum
+// (exact), the sum rounded to odd in fp32 (toward zero, last bit set when
+// inexact), then to fp16 (rounding to odd with 13 spare bits makes the second
+// rounding exact).
 //
-// Work: a lane reads 8 elements' codes of a position (K) or of a pair of
-// positions (V, stored position-paired) and their groups' (scale, bias)
-// words, and writes 8 fp16 values (16 bytes) per position, so a wave reads
-// consecutive positions' codes as one contiguous run and writes their
-// operands contiguously.  Each lane keeps kIters loads in flight.
+// Work: a lane reads 16 bytes of codes (32 elements) of one position (K) or
+// of a pair of positions (V, stored position-paired) and their groups'
+// (scale, bias) words, and writes the fp16 values as 16-byte stores, so a
+// wave reads consecutive positions' codes as one contiguous run and writes
+// their operands contiguously.  Each lane keeps kIters loads in flight.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -32,7 +34,7 @@
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kIters = 4;  // loads in flight per lane
+constexpr int kIters = 4;  // 16-byte code loads in flight per lane
 
 // fp16 of s * q + b rounded once, via fp32 rounded to odd (see above).
 __device__ __forceinline__ float to_odd(float s, float q, float b) {
@@ -48,18 +50,22 @@ __device__ __forceinline__ float to_odd(float s, float q, float b) {
   return __builtin_bit_cast(float, u);
 }
 
-// fp32 values whose conversion to fp16 may differ from rounding the exact
-// value they approximate: an fp16 rounding midpoint of the normal range (the
-// 13 bits below fp16's precision are 1000000000000), or magnitudes below
-// 2^-14 (fp16 subnormals).
-__device__ __forceinline__ bool near_midpoint(float x) {
-  const uint32_t u = __builtin_bit_cast(uint32_t, x);
-  return (u & 0x1FFFu) == 0x1000u || (u & 0x7FFFFFFFu) < 0x38800000u;
+// Every s * q + b (q = 0 .. 15) of a group is exact in fp32 (see above).
+__device__ __forceinline__ bool group_exact(float s, float b) {
+  if (s == 0.0f || b == 0.0f) return true;  // one term: s * q or b, exact
+  // frexp exponent e: |x| in [2^(e-1), 2^e); an fp16 value's lowest bit is
+  // at 2^(e-11) or 2^-24
+  const int es = __builtin_amdgcn_frexp_expf(s), eb = __builtin_amdgcn_frexp_expf(b);
+  const int low = max(min(es, eb) - 11, -24);
+  // one more than the bound's exponent: the rounded bound may fall below a
+  // power of two the exact bound reaches
+  const int high = __builtin_amdgcn_frexp_expf(fmaf(fabsf(s), 15.0f, fabsf(b))) + 1;
+  return high - low <= 24;
 }
 
 // fp16 of the eight elements of one code word (element k at bits 4k) with
 // the group's (scale, bias) word; the exact path for the whole wave when any
-// lane's fp32 result may round differently from the exact value.
+// lane's group may have inexact fp32 sums.
 __device__ __forceinline__ uint4 emit8(uint32_t cw, uint32_t mw) {
   const float s = __half2float(__ushort_as_half((unsigned short)(mw & 0xFFFFu)));
   const float b = __half2float(__ushort_as_half((unsigned short)(mw >> 16)));
@@ -71,13 +77,9 @@ __device__ __forceinline__ uint4 emit8(uint32_t cw, uint32_t mw) {
     q[2 * k + 1] = (float)((hi4 >> (8 * k)) & 0xFFu);  // element 2 k + 1
   }
   float x[8];
-  bool risky = false;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    x[k] = fmaf(s, q[k], b);
-    risky |= near_midpoint(x[k]);
-  }
-  if (__builtin_amdgcn_ballot_w64(risky) != 0) {
+  for (int k = 0; k < 8; ++k) x[k] = fmaf(s, q[k], b);
+  if (__builtin_amdgcn_ballot_w64(!group_exact(s, b)) != 0) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) x[k] = to_odd(s, q[k], b);
   }
@@ -89,78 +91,106 @@ __device__ __forceinline__ uint4 emit8(uint32_t cw, uint32_t mw) {
   return o;
 }
 
-// K: lane (position, word w) handles elements 8 w .. 8 w + 7 of one
-// position.  V (codes stored in position pairs: 32-bit word u of a pair
-// holds dims 4u .. 4u + 3 of the even slot in its low half and of the odd
-// slot in its high half): lane (pair, v) reads words 2v, 2v + 1 of a pair (8
-// bytes) and handles elements 8 v .. 8 v + 7 of both positions.
+// Lane work per load: 16 bytes of codes = 32 elements.  K: lane (position,
+// c) reads code words 4c .. 4c + 3 of one position (elements 32 c .. 32 c +
+// 31).  V (codes stored in position pairs: 32-bit word u of a pair holds dims
+// 4u .. 4u + 3 of the even slot in its low half and of the odd slot in its
+// high half): lane (pair, c) reads words 4c .. 4c + 3 of a pair, elements
+// 16 c .. 16 c + 15 of both positions.  Either way the lane's elements of a
+// position lie in one scale group (G >= 32) and leave as 16-byte stores.
 template <int D, int G, bool V>
-__global__ __launch_bounds__(64 * kWaves) void reconstruct_kernel(
-    const uint32_t* __restrict__ codes, const uint32_t* __restrict__ meta,
+__device__ __forceinline__ void reconstruct_body(
+    const uint4* __restrict__ codes, const uint32_t* __restrict__ meta,
     const int32_t* __restrict__ table, int n, int kv0, int Hkv, int P, int NP,
     uint4* __restrict__ out) {
-  constexpr int WPP = D / 8;         // 16-byte output chunks per position
-  constexpr int LPU = 64 / WPP;      // units (positions or pairs) per wave and load
-  constexpr int NG = D / G;          // groups per position
-  constexpr int PER = V ? 2 : 1;     // positions per unit
+  constexpr int LPU = V ? D / 16 : D / 32;  // lanes per unit (a position, or a pair)
+  constexpr int UPW = 64 / LPU;             // units per wave and load
+  constexpr int PER = V ? 2 : 1;            // positions per unit
+  constexpr int EPL = 32 / PER;             // elements per lane and position
+  constexpr int NG = D / G;                 // groups per position
+  constexpr int CPP = D / 8;                // 16-byte output chunks per position
+  static_assert(G >= EPL, "a lane's elements lie in one group");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int j = blockIdx.y;          // head within the group
+  const int j = blockIdx.y;  // head within the group
   const int kv = kv0 + j;
-  const int w = lane % WPP;
-  const int g = (8 * w) / G;
-  const int u0 = (blockIdx.x * kWaves + wave) * kIters * LPU + lane / WPP;
+  const int c = lane % LPU;
+  const int g = (EPL * c) / G;
+  const int u0 = (blockIdx.x * kWaves + wave) * kIters * UPW + lane / LPU;
 
-  uint32_t cw[kIters][PER], mw[kIters][PER];
+  uint4 cw[kIters];
+  uint32_t mw[kIters][PER];
 #pragma unroll
   for (int i = 0; i < kIters; ++i) {
-    const int t = PER * (u0 + i * LPU);  // first position of the unit
+    const int t = PER * (u0 + i * UPW);  // first position of the unit
+    cw[i] = make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
-    for (int e = 0; e < PER; ++e) cw[i][e] = mw[i][e] = 0u;  // outside the pool: zeros
+    for (int e = 0; e < PER; ++e) mw[i][e] = 0u;  // outside the pool: zeros
     const int page = t < n ? table[t / P] : -1;
     if ((unsigned)page < (unsigned)NP) {
       const size_t vec = ((size_t)page * Hkv + kv) * P + (t % P);
-      if constexpr (V) {
-        const uint2 c2 = *reinterpret_cast<const uint2*>(codes + vec * (D / 8) + 2 * w);
-        cw[i][0] = (c2.x & 0xFFFFu) | (c2.y << 16);
-        cw[i][1] = (c2.x >> 16) | (c2.y & 0xFFFF0000u);
-        mw[i][0] = meta[vec * NG + g];
-        mw[i][1] = meta[(vec + 1) * NG + g];
-      } else {
-        cw[i][0] = codes[vec * WPP + w];
-        mw[i][0] = meta[vec * NG + g];
-      }
+      // (a pair's first vector: the pair's words start at its byte offset)
+      cw[i] = codes[vec * (D / 32) + c];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) mw[i][e] = meta[(vec + e) * NG + g];
     }
   }
 #pragma unroll
   for (int i = 0; i < kIters; ++i) {
-    const int t = PER * (u0 + i * LPU);
+    const int t = PER * (u0 + i * UPW);
+    uint32_t w[PER][EPL / 8];  // K-order code words per position
+    if constexpr (V) {
+      const uint32_t a[4] = {cw[i].x, cw[i].y, cw[i].z, cw[i].w};
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        w[0][h] = (a[2 * h] & 0xFFFFu) | (a[2 * h + 1] << 16);
+        w[1][h] = (a[2 * h] >> 16) | (a[2 * h + 1] & 0xFFFF0000u);
+      }
+    } else {
+      w[0][0] = cw[i].x; w[0][1] = cw[i].y; w[0][2] = cw[i].z; w[0][3] = cw[i].w;
+    }
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
-      const uint4 o = emit8(cw[i][e], mw[i][e]);
-      if (t + e < n) out[((size_t)j * n + t + e) * WPP + w] = o;
+      uint4 o[EPL / 8];
+#pragma unroll
+      for (int h = 0; h < EPL / 8; ++h) o[h] = emit8(w[e][h], mw[i][e]);
+      if (t + e < n) {
+        uint4* dst = out + ((size_t)j * n + t + e) * CPP + (EPL / 8) * c;
+#pragma unroll
+        for (int h = 0; h < EPL / 8; ++h) dst[h] = o[h];
+      }
     }
   }
+}
+
+// K (blockIdx.z = 0) and V (1) in one launch.
+template <int D, int G>
+__global__ __launch_bounds__(64 * kWaves) void reconstruct_kernel(
+    const uint4* __restrict__ k_codes, const uint32_t* __restrict__ k_meta,
+    const uint4* __restrict__ v_codes, const uint32_t* __restrict__ v_meta,
+    const int32_t* __restrict__ table, int n, int kv0, int Hkv, int P, int NP,
+    uint4* __restrict__ k_out, uint4* __restrict__ v_out) {
+  if (blockIdx.z == 0)
+    reconstruct_body<D, G, false>(k_codes, k_meta, table, n, kv0, Hkv, P, NP, k_out);
+  else
+    reconstruct_body<D, G, true>(v_codes, v_meta, table, n, kv0, Hkv, P, NP, v_out);
 }
 
 template <int D, int G>
 hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const int32_t* table,
                     int32_t n, int32_t kv0, int32_t g, void* k_out, void* v_out,
                     hipStream_t stream) {
-  constexpr int LPU = 64 / (D / 8);
-  constexpr int kUnits = kWaves * kIters * LPU;  // units per block
-  const unsigned kb = (unsigned)((n + kUnits - 1) / kUnits);
-  const unsigned vb = (unsigned)((n + 2 * kUnits - 1) / (2 * kUnits));
-  hipLaunchKernelGGL((reconstruct_kernel<D, G, false>), dim3(kb, (unsigned)g), dim3(64 * kWaves),
-                     0, stream, static_cast<const uint32_t*>(pool.k_codes),
-                     static_cast<const uint32_t*>(pool.k_meta), table, n, kv0, L.num_kv_heads,
-                     L.page_size, L.num_pages, static_cast<uint4*>(k_out));
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((reconstruct_kernel<D, G, true>), dim3(vb, (unsigned)g), dim3(64 * kWaves),
-                     0, stream, static_cast<const uint32_t*>(pool.v_codes),
+  // positions per block: kWaves waves x kIters loads x (64 / lanes per
+  // unit) units x positions per unit; the same for K and V
+  constexpr int kPos = kWaves * kIters * 64 / (D / 32);
+  const unsigned blocks = (unsigned)((n + kPos - 1) / kPos);
+  hipLaunchKernelGGL((reconstruct_kernel<D, G>), dim3(blocks, (unsigned)g, 2), dim3(64 * kWaves),
+                     0, stream, static_cast<const uint4*>(pool.k_codes),
+                     static_cast<const uint32_t*>(pool.k_meta),
+                     static_cast<const uint4*>(pool.v_codes),
                      static_cast<const uint32_t*>(pool.v_meta), table, n, kv0, L.num_kv_heads,
-                     L.page_size, L.num_pages, static_cast<uint4*>(v_out));
+                     L.page_size, L.num_pages, static_cast<uint4*>(k_out),
+                     static_cast<uint4*>(v_out));
   return hipGetLastError();
 }
 
