@@ -82,7 +82,8 @@ typedef enum {
   JF_ERR_NO_PAGES = 2,    /* page reservation could not be satisfied         */
   JF_ERR_DEVICE = 3,      /* HIP launch or runtime error                     */
   JF_ERR_UNSUPPORTED = 4, /* valid but not implemented geometry              */
-  JF_ERR_STATE = 5        /* operation not allowed in the object's state     */
+  JF_ERR_STATE = 5,       /* operation not allowed in the object's state     */
+  JF_ERR_IO = 6           /* host file I/O failed (snapshots)                */
 } jf_status;
 
 /* Message for the last failing jf_* call on this thread ("" if none). */
@@ -364,6 +365,74 @@ jf_status jf_reconstruct_q4(const jf_kv_layout* layout,
                             const int32_t* block_table, int32_t max_pages,
                             int32_t n_pos, int32_t kv0, int32_t num_heads,
                             void* k_out, void* v_out, hipStream_t stream);
+
+/* ------------------------------------------------------- snapshots
+ * Prefix snapshots and their restoration (Sec. 3.4, "Keep Checkpointing
+ * from Undoing the Savings"; Appendix A, Fig. kv-detail (b); Table writer).
+ * A page of one layer's pool is packed as its four runs for all KV heads:
+ * K codes, K (scale, bias), V codes, V (scale, bias), exactly as the pool
+ * stores them (page_bytes = 2 * Hkv * page_size * (d/2 + 4 * d/G)). */
+
+/* page_bytes of this layout. */
+jf_status jf_kv_page_bytes(const jf_kv_layout* layout, size_t* bytes);
+
+/* Pack pages block_table[first .. first+count-1] of one layer's pool, in
+ * that order, into buf (count * page_bytes bytes of device memory, 16-byte
+ * aligned); or unpack buf into those pages.  block_table: int32 (device).
+ * A page ID outside [0, num_pages) packs as zeros and is skipped when
+ * unpacking.  One kernel on stream; the pages are read (or written) where
+ * they are.  A buf that is not device memory is rejected (JF_ERR_INVALID):
+ * kernels never dereference host memory.  Pool codes 16-byte and meta
+ * 4-byte aligned. */
+jf_status jf_kv_pack_pages(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                           const int32_t* block_table, int32_t first, int32_t count,
+                           void* buf, hipStream_t stream);
+jf_status jf_kv_unpack_pages(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                             const int32_t* block_table, int32_t first, int32_t count,
+                             const void* buf, hipStream_t stream);
+
+/* Save the first n_pos positions of one request, all n_layers layers
+ * (pools[l]: the layers' pools, one layout), to a file in one pass.  The
+ * pages are read in place through block_table (device; the same IDs in
+ * block_table_host, checked to lie in the pool) and streamed to the host
+ * through two caller buffers of staging_bytes each (at least two pages;
+ * 16-byte aligned): staging_dev (device memory) and staging (pinned host
+ * memory).  Each is used as two halves in turn: a kernel packs pages into a
+ * device half, a copy moves them to the host half, and the host writes the
+ * other half meanwhile, so the memory used is those buffers, whatever
+ * n_pos is (no copy of the cache is made).  The file is written as
+ * path + ".tmp" and renamed to path once complete and flushed (fsync), so
+ * path holds either a whole snapshot or what it held before; on failure the
+ * temporary file is removed.  Format: safetensors (8-byte little-endian
+ * header length, JSON header, data), one U8 tensor "layer<l>" of shape
+ * [ceil(n_pos / page_size)][page_bytes] per layer, the layout and n_pos in
+ * the header's metadata; whole pages are saved (slots past n_pos as they
+ * are).  Synchronous: returns once the file is published.  The request
+ * keeps its pages, which must not change or be released until the call
+ * returns.  JF_ERR_INVALID for staging buffers of the wrong kind; JF_ERR_IO
+ * on file errors, with errno's text in jf_last_error. */
+jf_status jf_snapshot_save(const char* path, const jf_kv_layout* layout,
+                           const jf_kv_pool_ptrs* pools, int32_t n_layers,
+                           const int32_t* block_table, const int32_t* block_table_host,
+                           int32_t max_pages, int32_t n_pos, void* staging_dev,
+                           void* staging, size_t staging_bytes, hipStream_t stream);
+
+/* Restore a snapshot written by jf_snapshot_save with the same layout and
+ * layer count into the pages of a request's table (block_table device,
+ * block_table_host the same IDs; its first ceil(n_pos / page_size) entries
+ * must be distinct pages of the pool, reserved by the caller), writing the
+ * packed runs straight into those pages: pieces of the file are read into
+ * the pinned staging halves in turn, copied to the device halves and
+ * unpacked by a kernel while the next piece is read.  *n_pos_out receives
+ * the snapshot's position count.  Synchronous.  JF_ERR_INVALID if the file
+ * is not such a snapshot (header, layout, layer count or size differ), the
+ * table is too short or lists a page twice, or a staging buffer is of the
+ * wrong kind; JF_ERR_IO on read errors. */
+jf_status jf_snapshot_restore(const char* path, const jf_kv_layout* layout,
+                              const jf_kv_pool_ptrs* pools, int32_t n_layers,
+                              const int32_t* block_table, const int32_t* block_table_host,
+                              int32_t max_pages, void* staging_dev, void* staging,
+                              size_t staging_bytes, int32_t* n_pos_out, hipStream_t stream);
 
 /* ---------------------------------------------------------------- TQ4
  * The paper's own 4-bit format (Sec. 3.1, eq. codec; Appendix A, Table

@@ -6,7 +6,12 @@
 // request, page IDs returned on completion); shared prefixes hold reference
 // counts and reservation is all-or-nothing (Sec. 3.3, eq. reservation);
 // releasing a request recycles its zero-reference pages (Algorithm 1).
+#include <fcntl.h>
+#include <sys/stat.h>
+#include <unistd.h>
+
 #include <algorithm>
+#include <cerrno>
 #include <climits>
 #include <cmath>
 #include <cstdarg>
@@ -702,6 +707,362 @@ jf_status jf_tq4_reconstruct(const jf_kv_layout* layout, const void* k_words,
                                                     k_signs, v_signs, centroids, block_table,
                                                     n_pos, kv0, num_heads, k_out, v_out, stream),
                        "tq4_reconstruct launch");
+}
+
+// ------------------------------------------------------------------ snapshots
+namespace {
+
+jf_status check_pool_aligned(const jf_kv_pool_ptrs* p) {
+  jf_status st = check_pool(p);
+  if (st) return st;
+  if ((((uintptr_t)p->k_codes | (uintptr_t)p->v_codes) & 15) ||
+      (((uintptr_t)p->k_meta | (uintptr_t)p->v_meta) & 3))
+    return fail(JF_ERR_INVALID, "pool codes must be 16-byte and meta 4-byte aligned");
+  return ok();
+}
+
+// Whether p is device memory (false also when the runtime cannot tell).
+// Kernels never dereference host memory: a host allocation is usable on the
+// device only through the device pointer of a mapped allocation.
+bool is_device_memory(const void* p) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeDevice;
+}
+
+bool is_pinned_host_memory(const void* p) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return a.type == hipMemoryTypeHost;
+}
+
+jf_status page_copy(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                    const int32_t* block_table, int32_t first, int32_t count, const void* buf,
+                    bool unpack, hipStream_t stream) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if ((st = check_pool_aligned(pool))) return st;
+  if (first < 0 || count < 0 || (int64_t)first + count > INT32_MAX)
+    return fail(JF_ERR_INVALID, "first and count must be >= 0");
+  if (count == 0) return ok();
+  if (!block_table || !buf) return fail(JF_ERR_INVALID, "NULL pointer");
+  if ((uintptr_t)buf & 15) return fail(JF_ERR_INVALID, "buf must be 16-byte aligned");
+  if (!is_device_memory(buf)) return fail(JF_ERR_INVALID, "buf must be device memory");
+  return device_status(jfkv::launch_page_runs(*layout, *pool, block_table, first, count,
+                                              const_cast<void*>(buf), unpack, stream),
+                       unpack ? "unpack_pages launch" : "pack_pages launch");
+}
+
+// The safetensors header of a snapshot: one U8 tensor per layer holding its
+// pages in logical order; the layout and length as metadata (strings, as
+// the format requires); padded with spaces to a multiple of 8 bytes.
+std::string snapshot_header(const jf_kv_layout& L, int32_t n_layers, int32_t n_pos, size_t pb) {
+  const int64_t n_pages = ((int64_t)n_pos + L.page_size - 1) / L.page_size;
+  char buf[512];
+  snprintf(buf, sizeof(buf),
+           "{\"__metadata__\":{\"format\":\"jfkv-pages-1\",\"page_size\":\"%d\","
+           "\"num_kv_heads\":\"%d\",\"head_dim\":\"%d\",\"group_size\":\"%d\","
+           "\"n_layers\":\"%d\",\"n_pos\":\"%d\",\"page_bytes\":\"%zu\"}",
+           L.page_size, L.num_kv_heads, L.head_dim, L.group_size, n_layers, n_pos, pb);
+  std::string h = buf;
+  const uint64_t layer_bytes = (uint64_t)n_pages * pb;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    snprintf(buf, sizeof(buf),
+             ",\"layer%d\":{\"dtype\":\"U8\",\"shape\":[%lld,%zu],\"data_offsets\":[%llu,%llu]}",
+             l, (long long)n_pages, pb, (unsigned long long)(l * layer_bytes),
+             (unsigned long long)((l + 1) * layer_bytes));
+    h += buf;
+  }
+  h += "}";
+  while (h.size() % 8) h += ' ';
+  return h;
+}
+
+bool write_all(int fd, const void* p, size_t n) {
+  const char* c = static_cast<const char*>(p);
+  while (n > 0) {
+    const ssize_t w = ::write(fd, c, n);
+    if (w < 0) {
+      if (errno == EINTR) continue;
+      return false;
+    }
+    c += w;
+    n -= (size_t)w;
+  }
+  return true;
+}
+
+bool pread_all(int fd, void* p, size_t n, off_t off) {
+  char* c = static_cast<char*>(p);
+  while (n > 0) {
+    const ssize_t r = ::pread(fd, c, n, off);
+    if (r < 0) {
+      if (errno == EINTR) continue;
+      return false;
+    }
+    if (r == 0) return false;  // end of file
+    c += r;
+    n -= (size_t)r;
+    off += r;
+  }
+  return true;
+}
+
+// Arguments shared by save and restore; pages_out = pages of n_pos.
+jf_status check_snapshot_args(const char* path, const jf_kv_layout* layout,
+                              const jf_kv_pool_ptrs* pools, int32_t n_layers,
+                              const int32_t* block_table, const int32_t* block_table_host,
+                              int32_t max_pages, void* staging_dev, void* staging,
+                              size_t staging_bytes) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if (!path || !pools || !staging || !staging_dev) return fail(JF_ERR_INVALID, "NULL pointer");
+  if (n_layers <= 0) return fail(JF_ERR_INVALID, "n_layers must be positive");
+  for (int32_t l = 0; l < n_layers; ++l)
+    if ((st = check_pool_aligned(&pools[l]))) return st;
+  if (max_pages < 0) return fail(JF_ERR_INVALID, "max_pages must be >= 0");
+  if (max_pages > 0 && (!block_table || !block_table_host))
+    return fail(JF_ERR_INVALID, "NULL block table");
+  if (((uintptr_t)staging | (uintptr_t)staging_dev) & 15)
+    return fail(JF_ERR_INVALID, "staging buffers must be 16-byte aligned");
+  const size_t pb = jfkv::page_bytes(*layout);
+  if (staging_bytes / 2 < pb)
+    return fail(JF_ERR_INVALID, "staging of %zu bytes holds less than two pages of %zu bytes",
+                staging_bytes, pb);
+  return ok();
+}
+
+// The staging buffers' kinds (asked of the runtime, after every other check).
+jf_status check_staging_kinds(const void* staging_dev, const void* staging) {
+  if (!is_device_memory(staging_dev))
+    return fail(JF_ERR_INVALID, "staging_dev must be device memory");
+  if (!is_pinned_host_memory(staging))
+    return fail(JF_ERR_INVALID, "staging must be pinned host memory");
+  return ok();
+}
+
+// Two events that alternate with the staging halves.
+struct EventPair {
+  hipEvent_t e[2] = {nullptr, nullptr};
+  hipError_t create() {
+    for (auto& x : e) {
+      hipError_t r = hipEventCreateWithFlags(&x, hipEventDisableTiming);
+      if (r != hipSuccess) return r;
+    }
+    return hipSuccess;
+  }
+  ~EventPair() {
+    for (auto& x : e)
+      if (x) (void)hipEventDestroy(x);
+  }
+};
+
+}  // namespace
+
+jf_status jf_kv_page_bytes(const jf_kv_layout* layout, size_t* bytes) {
+  jf_status st = check_layout(layout);
+  if (st) return st;
+  if (!bytes) return fail(JF_ERR_INVALID, "NULL output pointer");
+  *bytes = jfkv::page_bytes(*layout);
+  return ok();
+}
+
+jf_status jf_kv_pack_pages(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                           const int32_t* block_table, int32_t first, int32_t count, void* buf,
+                           hipStream_t stream) {
+  return page_copy(layout, pool, block_table, first, count, buf, false, stream);
+}
+
+jf_status jf_kv_unpack_pages(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
+                             const int32_t* block_table, int32_t first, int32_t count,
+                             const void* buf, hipStream_t stream) {
+  return page_copy(layout, pool, block_table, first, count, buf, true, stream);
+}
+
+jf_status jf_snapshot_save(const char* path, const jf_kv_layout* layout,
+                           const jf_kv_pool_ptrs* pools, int32_t n_layers,
+                           const int32_t* block_table, const int32_t* block_table_host,
+                           int32_t max_pages, int32_t n_pos, void* staging_dev, void* staging,
+                           size_t staging_bytes, hipStream_t stream) {
+  jf_status st = check_snapshot_args(path, layout, pools, n_layers, block_table,
+                                     block_table_host, max_pages, staging_dev, staging,
+                                     staging_bytes);
+  if (st) return st;
+  const int32_t P = layout->page_size;
+  if (n_pos < 0 || (int64_t)n_pos > (int64_t)max_pages * P)
+    return fail(JF_ERR_INVALID, "n_pos %d outside 0 .. max_pages * page_size", n_pos);
+  const int32_t n_pages = (int32_t)(((int64_t)n_pos + P - 1) / P);
+  for (int32_t i = 0; i < n_pages; ++i)
+    if (block_table_host[i] < 0 || block_table_host[i] >= layout->num_pages)
+      return fail(JF_ERR_INVALID, "page %d of the request (ID %d) is not in the pool", i,
+                  block_table_host[i]);
+  if ((st = check_staging_kinds(staging_dev, staging))) return st;
+  const size_t pb = jfkv::page_bytes(*layout);
+  const int32_t per = (int32_t)std::min<size_t>(staging_bytes / 2 / pb, (size_t)INT32_MAX);
+  const std::string header = snapshot_header(*layout, n_layers, n_pos, pb);
+  const std::string tmp = std::string(path) + ".tmp";
+  EventPair ev;
+  if (hipError_t e = ev.create(); e != hipSuccess) return device_status(e, "hipEventCreate");
+  const int fd = ::open(tmp.c_str(), O_WRONLY | O_CREAT | O_TRUNC | O_CLOEXEC, 0644);
+  if (fd < 0) return fail(JF_ERR_IO, "open %s: %s", tmp.c_str(), strerror(errno));
+  // on failure: let enqueued copies finish (the caller may free the staging
+  // buffers), drop the temporary file
+  auto abort_with = [&](jf_status s) {
+    (void)hipStreamSynchronize(stream);
+    ::close(fd);
+    ::unlink(tmp.c_str());
+    return s;
+  };
+  const uint64_t hl = header.size();
+  uint8_t len8[8];
+  for (int i = 0; i < 8; ++i) len8[i] = (uint8_t)(hl >> (8 * i));
+  if (!write_all(fd, len8, 8) || !write_all(fd, header.data(), header.size()))
+    return abort_with(fail(JF_ERR_IO, "write %s: %s", tmp.c_str(), strerror(errno)));
+  // chunk c: pages packed into device half c % 2 by a kernel, copied to host
+  // half c % 2 (stream order keeps a device half from being refilled before
+  // its copy), written to the file while chunk c + 1 packs and copies
+  uint8_t* dh[2] = {static_cast<uint8_t*>(staging_dev),
+                    static_cast<uint8_t*>(staging_dev) + per * pb};
+  uint8_t* hh[2] = {static_cast<uint8_t*>(staging), static_cast<uint8_t*>(staging) + per * pb};
+  size_t pending = 0;  // bytes of the chunk copied last, not yet written
+  int c = 0;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    for (int32_t p0 = 0; p0 < n_pages; p0 += per, ++c) {
+      const int32_t cnt = std::min(per, n_pages - p0);
+      const int h = c & 1;
+      const size_t nbytes = (size_t)cnt * pb;
+      hipError_t e = jfkv::launch_page_runs(*layout, pools[l], block_table, p0, cnt, dh[h],
+                                            false, stream);
+      if (e == hipSuccess) e = hipMemcpyAsync(hh[h], dh[h], nbytes, hipMemcpyDeviceToHost, stream);
+      if (e == hipSuccess) e = hipEventRecord(ev.e[h], stream);
+      if (e != hipSuccess) return abort_with(device_status(e, "snapshot pack"));
+      if (c > 0) {  // the previous chunk, in the other half
+        if ((e = hipEventSynchronize(ev.e[h ^ 1])) != hipSuccess)
+          return abort_with(device_status(e, "snapshot pack"));
+        if (!write_all(fd, hh[h ^ 1], pending))
+          return abort_with(fail(JF_ERR_IO, "write %s: %s", tmp.c_str(), strerror(errno)));
+      }
+      pending = nbytes;
+    }
+  }
+  if (c > 0) {
+    const int h = (c - 1) & 1;
+    if (hipError_t e = hipEventSynchronize(ev.e[h]); e != hipSuccess)
+      return abort_with(device_status(e, "snapshot pack"));
+    if (!write_all(fd, hh[h], pending))
+      return abort_with(fail(JF_ERR_IO, "write %s: %s", tmp.c_str(), strerror(errno)));
+  }
+  if (::fsync(fd) != 0)
+    return abort_with(fail(JF_ERR_IO, "fsync %s: %s", tmp.c_str(), strerror(errno)));
+  if (::close(fd) != 0) {
+    ::unlink(tmp.c_str());
+    return fail(JF_ERR_IO, "close %s: %s", tmp.c_str(), strerror(errno));
+  }
+  if (::rename(tmp.c_str(), path) != 0) {
+    const int err = errno;
+    ::unlink(tmp.c_str());
+    return fail(JF_ERR_IO, "rename %s -> %s: %s", tmp.c_str(), path, strerror(err));
+  }
+  return ok();
+}
+
+jf_status jf_snapshot_restore(const char* path, const jf_kv_layout* layout,
+                              const jf_kv_pool_ptrs* pools, int32_t n_layers,
+                              const int32_t* block_table, const int32_t* block_table_host,
+                              int32_t max_pages, void* staging_dev, void* staging,
+                              size_t staging_bytes, int32_t* n_pos_out, hipStream_t stream) {
+  jf_status st = check_snapshot_args(path, layout, pools, n_layers, block_table,
+                                     block_table_host, max_pages, staging_dev, staging,
+                                     staging_bytes);
+  if (st) return st;
+  if (!n_pos_out) return fail(JF_ERR_INVALID, "NULL output pointer");
+  const int fd = ::open(path, O_RDONLY | O_CLOEXEC);
+  if (fd < 0) return fail(JF_ERR_IO, "open %s: %s", path, strerror(errno));
+  bool enqueued = false;
+  auto done = [&](jf_status s) {
+    if (enqueued) (void)hipStreamSynchronize(stream);
+    ::close(fd);
+    return s;
+  };
+  uint8_t len8[8];
+  if (!pread_all(fd, len8, 8, 0)) return done(fail(JF_ERR_INVALID, "%s: no header", path));
+  uint64_t hl = 0;
+  for (int i = 0; i < 8; ++i) hl |= (uint64_t)len8[i] << (8 * i);
+  if (hl == 0 || hl > (1u << 24)) return done(fail(JF_ERR_INVALID, "%s: bad header size", path));
+  std::string header(hl, '\0');
+  if (!pread_all(fd, &header[0], hl, 8)) return done(fail(JF_ERR_INVALID, "%s: short header", path));
+  // the position count, then the whole header must be the one save writes
+  const char* key = "\"n_pos\":\"";
+  const size_t at = header.find(key);
+  if (at == std::string::npos) return done(fail(JF_ERR_INVALID, "%s: not a snapshot", path));
+  const long long np_ll = strtoll(header.c_str() + at + strlen(key), nullptr, 10);
+  if (np_ll < 0 || np_ll > INT32_MAX) return done(fail(JF_ERR_INVALID, "%s: bad n_pos", path));
+  const int32_t n_pos = (int32_t)np_ll;
+  const size_t pb = jfkv::page_bytes(*layout);
+  if (header != snapshot_header(*layout, n_layers, n_pos, pb))
+    return done(fail(JF_ERR_INVALID,
+                     "%s: not a snapshot of this layout and layer count (header differs)", path));
+  const int32_t P = layout->page_size;
+  const int32_t n_pages = (int32_t)(((int64_t)n_pos + P - 1) / P);
+  struct stat sb;
+  if (::fstat(fd, &sb) != 0) return done(fail(JF_ERR_IO, "stat %s: %s", path, strerror(errno)));
+  const uint64_t data0 = 8 + hl;
+  if ((uint64_t)sb.st_size != data0 + (uint64_t)n_layers * n_pages * pb)
+    return done(fail(JF_ERR_INVALID, "%s: size %lld, expected %llu", path, (long long)sb.st_size,
+                     (unsigned long long)(data0 + (uint64_t)n_layers * n_pages * pb)));
+  if (n_pages > max_pages)
+    return done(fail(JF_ERR_INVALID, "the snapshot has %d pages, the table %d", n_pages,
+                     max_pages));
+  {
+    std::vector<int32_t> ids(block_table_host, block_table_host + n_pages);
+    for (int32_t id : ids)
+      if (id < 0 || id >= layout->num_pages)
+        return done(fail(JF_ERR_INVALID, "page ID %d is not in the pool", id));
+    std::sort(ids.begin(), ids.end());
+    if (std::adjacent_find(ids.begin(), ids.end()) != ids.end())
+      return done(fail(JF_ERR_INVALID, "the table lists a page twice"));
+  }
+  if ((st = check_staging_kinds(staging_dev, staging))) return done(st);
+  EventPair ev;
+  if (hipError_t e = ev.create(); e != hipSuccess) return done(device_status(e, "hipEventCreate"));
+  const int32_t per = (int32_t)std::min<size_t>(staging_bytes / 2 / pb, (size_t)INT32_MAX);
+  uint8_t* dh[2] = {static_cast<uint8_t*>(staging_dev),
+                    static_cast<uint8_t*>(staging_dev) + per * pb};
+  uint8_t* hh[2] = {static_cast<uint8_t*>(staging), static_cast<uint8_t*>(staging) + per * pb};
+  // chunk c: read into host half c % 2 once its previous copy (chunk c - 2)
+  // has left it, copied to device half c % 2, unpacked into the pages
+  int c = 0;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    for (int32_t p0 = 0; p0 < n_pages; p0 += per, ++c) {
+      const int32_t cnt = std::min(per, n_pages - p0);
+      const int h = c & 1;
+      const size_t nbytes = (size_t)cnt * pb;
+      hipError_t e = hipSuccess;
+      if (c >= 2 && (e = hipEventSynchronize(ev.e[h])) != hipSuccess)
+        return done(device_status(e, "snapshot unpack"));
+      const off_t off = (off_t)(data0 + ((uint64_t)l * n_pages + p0) * pb);
+      errno = 0;
+      if (!pread_all(fd, hh[h], nbytes, off))
+        return done(fail(JF_ERR_IO, "read %s: %s", path, errno ? strerror(errno) : "short"));
+      enqueued = true;
+      e = hipMemcpyAsync(dh[h], hh[h], nbytes, hipMemcpyHostToDevice, stream);
+      if (e == hipSuccess) e = hipEventRecord(ev.e[h], stream);  // host half h free again
+      if (e == hipSuccess)
+        e = jfkv::launch_page_runs(*layout, pools[l], block_table, p0, cnt, dh[h], true, stream);
+      if (e != hipSuccess) return done(device_status(e, "snapshot unpack"));
+    }
+  }
+  if (hipError_t e = hipStreamSynchronize(stream); e != hipSuccess)
+    return done(device_status(e, "snapshot unpack"));
+  *n_pos_out = n_pos;
+  ::close(fd);
+  return ok();
 }
 
 }  // extern "C"

@@ -76,6 +76,13 @@ hipError_t launch_tq4_reconstruct(const jf_kv_layout& L, const void* k_words, co
                                   int32_t num_heads, void* k_out, void* v_out,
                                   hipStream_t stream);
 
+// Packed bytes of one page (all KV heads: K codes, K meta, V codes, V meta),
+// and the page-run copy kernel (unpack: buffer -> pool).
+size_t page_bytes(const jf_kv_layout& L);
+hipError_t launch_page_runs(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
+                            const int32_t* block_table, int32_t first, int32_t count, void* buf,
+                            bool unpack, hipStream_t stream);
+
 hipError_t launch_prefill(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool,
                           const void* q, const void* k_chunk, const void* v_chunk,
                           int32_t T, int32_t num_q_heads,

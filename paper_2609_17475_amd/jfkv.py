@@ -15,9 +15,10 @@ from typing import Optional, Sequence
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("JFKV_LIB") or os.path.join(HERE, "libjfkv.so")  # JFKV_LIB: another build
 
-JF_OK, JF_ERR_INVALID, JF_ERR_NO_PAGES, JF_ERR_DEVICE, JF_ERR_UNSUPPORTED, JF_ERR_STATE = range(6)
+JF_OK, JF_ERR_INVALID, JF_ERR_NO_PAGES, JF_ERR_DEVICE, JF_ERR_UNSUPPORTED, JF_ERR_STATE, JF_ERR_IO = \
+    range(7)
 STATUS_NAMES = {0: "JF_OK", 1: "JF_ERR_INVALID", 2: "JF_ERR_NO_PAGES", 3: "JF_ERR_DEVICE",
-                4: "JF_ERR_UNSUPPORTED", 5: "JF_ERR_STATE"}
+                4: "JF_ERR_UNSUPPORTED", 5: "JF_ERR_STATE", 6: "JF_ERR_IO"}
 
 # every symbol include/jfkv.h declares
 EXPORTS = [
@@ -29,7 +30,8 @@ EXPORTS = [
     "jf_kv_quantize_append", "jf_decode_workspace_bytes", "jf_decode_attn_q4",
     "jf_verify_attn_q4", "jf_decode_step_q4", "jf_decode_step_q4_static", "jf_prefill_attn_q4",
     "jf_reconstruct_q4", "jf_tq4_pool_bytes", "jf_tq4_encode_append", "jf_tq4_decode_attn",
-    "jf_tq4_reconstruct",
+    "jf_tq4_reconstruct", "jf_kv_page_bytes", "jf_kv_pack_pages", "jf_kv_unpack_pages",
+    "jf_snapshot_save", "jf_snapshot_restore",
 ]
 
 
@@ -90,6 +92,11 @@ def _load():
         "jf_prefill_attn_q4": (st, [P, P, P, P, P, i32, i32, P, i32, i32, ctypes.c_float, P, P]),
         "jf_reconstruct_q4": (st, [P, P, P, i32, i32, i32, i32, P, P, P]),
         "jf_tq4_reconstruct": (st, [P, P, P, P, P, P, P, P, P, i32, i32, i32, i32, P, P, P]),
+        "jf_kv_page_bytes": (st, [P, ctypes.POINTER(sz)]),
+        "jf_kv_pack_pages": (st, [P, P, P, i32, i32, P, P]),
+        "jf_kv_unpack_pages": (st, [P, P, P, i32, i32, P, P]),
+        "jf_snapshot_save": (st, [ctypes.c_char_p, P, P, i32, P, P, i32, i32, P, P, sz, P]),
+        "jf_snapshot_restore": (st, [ctypes.c_char_p, P, P, i32, P, P, i32, P, P, sz, pi32, P]),
         "jf_tq4_pool_bytes": (st, [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
         "jf_tq4_encode_append": (st, [P, P, P, P, P, P, P, P, P, i32, i32, i32, P]),
         "jf_tq4_decode_attn": (st, [P, P, P, P, P, P, P, P, P, i32, i32, P, i32, P,
@@ -633,3 +640,77 @@ def jf_tq4_reconstruct(k_pool: TQ4Pool, v_pool: TQ4Pool, k_signs, v_signs, centr
                                   _ptr(v_signs), _ptr(centroids), _ptr(block_table),
                                   block_table.shape[-1], int(n_pos), int(kv0), int(num_heads),
                                   _ptr(k_out), _ptr(v_out), _stream(stream)))
+
+
+# ---------------------------------------------------------------- snapshots
+def kv_page_bytes(lay: Layout) -> int:
+    n = ctypes.c_size_t()
+    _check(lib.jf_kv_page_bytes(ctypes.byref(lay), ctypes.byref(n)))
+    return n.value
+
+
+def jf_kv_pack_pages(pool: KVPool, block_table, first: int, count: int, buf, stream=None):
+    """Pages block_table[first .. first+count-1] -> buf (device uint8)."""
+    import torch
+    _dev_check(block_table, "block_table", torch.int32)
+    if buf.dtype != torch.uint8 or buf.numel() < count * kv_page_bytes(pool.layout):
+        raise ValueError("buf must be uint8 with count * page_bytes bytes")
+    lay, ptrs = pool.layout, pool.ptrs()
+    _check(lib.jf_kv_pack_pages(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(block_table),
+                                int(first), int(count), _ptr(buf), _stream(stream)))
+
+
+def jf_kv_unpack_pages(pool: KVPool, block_table, first: int, count: int, buf, stream=None):
+    """buf (device uint8) -> pages block_table[first .. first+count-1]."""
+    import torch
+    _dev_check(block_table, "block_table", torch.int32)
+    if buf.dtype != torch.uint8 or buf.numel() < count * kv_page_bytes(pool.layout):
+        raise ValueError("buf must be uint8 with count * page_bytes bytes")
+    lay, ptrs = pool.layout, pool.ptrs()
+    _check(lib.jf_kv_unpack_pages(ctypes.byref(lay), ctypes.byref(ptrs), _ptr(block_table),
+                                  int(first), int(count), _ptr(buf), _stream(stream)))
+
+
+def _snapshot_args(pools, block_table, block_table_host, staging_dev, staging):
+    import numpy as np
+    import torch
+    lay = pools[0].layout
+    for p in pools:
+        if tuple(getattr(p.layout, f) for f, _ in Layout._fields_) != \
+                tuple(getattr(lay, f) for f, _ in Layout._fields_):
+            raise ValueError("every layer's pool must have the same layout")
+    _dev_check(block_table, "block_table", torch.int32)
+    _dev_check(staging_dev, "staging_dev", torch.uint8)
+    if staging.dtype != torch.uint8 or staging.device.type != "cpu" or not staging.is_pinned():
+        raise ValueError("staging must be a pinned host uint8 tensor")
+    if staging.numel() != staging_dev.numel():
+        raise ValueError("staging and staging_dev must have the same size")
+    host = np.ascontiguousarray(np.asarray(block_table_host, np.int32).reshape(-1))
+    if host.shape[0] != block_table.reshape(-1).shape[0]:
+        raise ValueError("block_table and block_table_host must have the same length")
+    arr = (PoolPtrs * len(pools))(*[p.ptrs() for p in pools])
+    return lay, arr, host
+
+
+def snapshot_save(path: str, pools, block_table, block_table_host, n_pos: int, staging_dev,
+                  staging, stream=None):
+    """Save positions 0..n_pos-1 of one request, every layer in `pools`, to
+    `path` (safetensors; see include/jfkv.h), through staging_dev (device) and
+    staging (pinned host), uint8 buffers of equal size."""
+    lay, arr, host = _snapshot_args(pools, block_table, block_table_host, staging_dev, staging)
+    _check(lib.jf_snapshot_save(os.fsencode(path), ctypes.byref(lay), arr, len(pools),
+                                _ptr(block_table), host.ctypes.data, host.shape[0], int(n_pos),
+                                _ptr(staging_dev), _ptr(staging), staging.numel(),
+                                _stream(stream)))
+
+
+def snapshot_restore(path: str, pools, block_table, block_table_host, staging_dev, staging,
+                     stream=None) -> int:
+    """Restore a snapshot into the request pages listed in block_table; returns n_pos."""
+    lay, arr, host = _snapshot_args(pools, block_table, block_table_host, staging_dev, staging)
+    n = ctypes.c_int32()
+    _check(lib.jf_snapshot_restore(os.fsencode(path), ctypes.byref(lay), arr, len(pools),
+                                   _ptr(block_table), host.ctypes.data, host.shape[0],
+                                   _ptr(staging_dev), _ptr(staging), staging.numel(),
+                                   ctypes.byref(n), _stream(stream)))
+    return n.value

@@ -110,3 +110,97 @@ def test_tq4_pool_bytes_and_validation():
     # nothing to encode: success without a launch
     assert L.jf_tq4_encode_append(ctypes.byref(lay), 16, 16, None, None, None, None, None, None,
                                   1, 4, 0, None) == 0
+
+
+# ---------------------------------------------------------------- snapshots
+def _snap_args(lay, n_layers=2, max_pages=4):
+    pools = (jfkv.PoolPtrs * n_layers)(*[jfkv.PoolPtrs(4096, 4096, 4096, 4096)
+                                         for _ in range(n_layers)])
+    host = (ctypes.c_int32 * max_pages)(*range(max_pages))
+    return pools, host
+
+
+def snapshot_header(P, hkv, d, G, n_layers, n_pos):
+    """The on-disk header the library writes (safetensors: JSON, padded with
+    spaces to 8 bytes), written out here to pin the format."""
+    pb = 2 * hkv * P * (d // 2 + 4 * d // G)
+    n_pages = -(-n_pos // P)
+    h = ('{"__metadata__":{"format":"jfkv-pages-1","page_size":"%d","num_kv_heads":"%d",'
+         '"head_dim":"%d","group_size":"%d","n_layers":"%d","n_pos":"%d","page_bytes":"%d"}'
+         % (P, hkv, d, G, n_layers, n_pos, pb))
+    for l in range(n_layers):
+        h += ',"layer%d":{"dtype":"U8","shape":[%d,%d],"data_offsets":[%d,%d]}' % (
+            l, n_pages, pb, l * n_pages * pb, (l + 1) * n_pages * pb)
+    h += "}"
+    h += " " * (-len(h) % 8)
+    return h.encode(), pb * n_pages * n_layers
+
+
+def test_page_bytes_and_pack_validation():
+    lay = jfkv.layout(256, 8, 128, 64, 16)
+    assert jfkv.kv_page_bytes(lay) == 256 * 1152
+    assert jfkv.kv_page_bytes(jfkv.layout(64, 2, 256, 32, 4)) == 2 * 2 * 64 * (128 + 32)
+    L = jfkv.lib
+    ptrs = jfkv.PoolPtrs(4096, 4096, 4096, 4096)
+    assert L.jf_kv_pack_pages(ctypes.byref(lay), ctypes.byref(ptrs), 4096, -1, 2, 4096,
+                              None) == jfkv.JF_ERR_INVALID
+    assert L.jf_kv_pack_pages(ctypes.byref(lay), ctypes.byref(ptrs), 4096, 0, 2, 4100,
+                              None) == jfkv.JF_ERR_INVALID  # buffer alignment
+    assert L.jf_kv_unpack_pages(ctypes.byref(lay), ctypes.byref(jfkv.PoolPtrs(4104, 4096, 4096, 4096)),
+                                4096, 0, 2, 4096, None) == jfkv.JF_ERR_INVALID  # codes alignment
+    assert L.jf_kv_pack_pages(ctypes.byref(lay), ctypes.byref(ptrs), 4096, 0, 0, None,
+                              None) == jfkv.JF_OK  # nothing to copy
+
+
+def test_snapshot_save_validation(tmp_path):
+    lay = jfkv.layout(256, 8, 128, 64, 16)
+    pools, host = _snap_args(lay)
+    pb = 256 * 1152
+    L = jfkv.lib
+    path = str(tmp_path / "s.safetensors").encode()
+
+    def save(p=path, n_layers=2, n_pos=300, staging_bytes=2 * pb, table=host, max_pages=4):
+        return L.jf_snapshot_save(p, ctypes.byref(lay), pools, n_layers, 4096,
+                                  ctypes.cast(table, ctypes.c_void_p), max_pages, n_pos, 4096,
+                                  4096, staging_bytes, None)
+    assert save(p=None) == jfkv.JF_ERR_INVALID
+    assert save(n_layers=0) == jfkv.JF_ERR_INVALID
+    assert save(staging_bytes=2 * pb - 1) == jfkv.JF_ERR_INVALID
+    assert b"two pages" in L.jf_last_error()
+    assert save(n_pos=4 * 256 + 1) == jfkv.JF_ERR_INVALID
+    bad = (ctypes.c_int32 * 4)(0, 16, 2, 3)  # page ID one past the pool
+    assert save(table=bad) == jfkv.JF_ERR_INVALID
+    assert not os.path.exists(path) and not os.path.exists(path + b".tmp")
+
+
+def test_snapshot_restore_rejects_foreign_files(tmp_path):
+    P, hkv, d, G, n_layers = 256, 8, 128, 64, 2
+    lay = jfkv.layout(P, hkv, d, G, 16)
+    pools, host = _snap_args(lay, n_layers=3)  # room for the n_layers = 3 call
+    L = jfkv.lib
+    n = ctypes.c_int32()
+
+    def restore(p, n_layers=n_layers, table=host, max_pages=4, out=ctypes.byref(n)):
+        return L.jf_snapshot_restore(p, ctypes.byref(lay), pools, n_layers, 4096,
+                                     ctypes.cast(table, ctypes.c_void_p), max_pages, 4096, 4096,
+                                     2 * P * 1152, out, None)
+
+    def write(name, header, data_len):
+        f = tmp_path / name
+        f.write_bytes(len(header).to_bytes(8, "little") + header + bytes(data_len))
+        return str(f).encode()
+
+    assert restore(str(tmp_path / "missing").encode()) == jfkv.JF_ERR_IO
+    h, nbytes = snapshot_header(P, hkv, d, G, n_layers, 700)
+    good = write("good", h, nbytes)
+    assert restore(good, out=None) == jfkv.JF_ERR_INVALID
+    assert restore(good, n_layers=3) == jfkv.JF_ERR_INVALID        # header differs
+    assert b"header differs" in L.jf_last_error()
+    h64, n64 = snapshot_header(P, hkv, d, 32, n_layers, 700)        # another group size
+    assert restore(write("g32", h64, n64)) == jfkv.JF_ERR_INVALID
+    assert restore(write("short", h, nbytes - 1)) == jfkv.JF_ERR_INVALID  # truncated
+    assert restore(good, max_pages=2) == jfkv.JF_ERR_INVALID       # 3 pages, table of 2
+    dup = (ctypes.c_int32 * 4)(5, 6, 5, 7)
+    assert restore(good, table=dup) == jfkv.JF_ERR_INVALID
+    assert b"twice" in L.jf_last_error()
+    assert restore(write("junk", b'{"a":1} ', 0)) == jfkv.JF_ERR_INVALID
