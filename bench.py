@@ -35,6 +35,8 @@ Other workloads (--workload) print their own line:
                    over prefill_chunk's prefix (HBM roofline), the grouped
                    reconstruct + SDPA prefill against the fused prefill, and
                    TQ4 reconstruction at 196,608 positions
+  snapshot_224k    16 layers x 229,376 positions saved to a file and restored
+                   through 64 MiB staging buffers (pack kernel: HBM roofline)
 """
 from __future__ import annotations
 
@@ -1038,9 +1040,124 @@ def bench_reconstruct(args):
     print(json.dumps(result), flush=True)
 
 
+def bench_snapshot(args):
+    """snapshot_224k: a 229,376-position (224K) prefix of one request in 16
+    layers' pools (8 KV heads, d 128, group 64: 896 pages, 264 MB per layer,
+    4.2 GB in all; the paper's snapshot probe uses 16 packed cache layers at
+    224K), saved to a file and restored into another request's pages through
+    64 MiB of device and 64 MiB of pinned host staging.  The page bytes are
+    random (the copies do not look at them).  HBM roofline over the page-pack
+    kernel packing one layer into device memory (each byte read and written
+    once); save and restore are reported end to end (file on the host's
+    temporary directory, removed afterwards)."""
+    import shutil
+    import tempfile
+    import numpy as np
+    import torch
+    from paper_2609_17475_amd import jfkv
+    dev = torch.device("cuda:0")
+    P, hkv, d, G, n_layers, L = 256, 8, 128, 64, 16, 229376
+    n_pages = L // P
+    NP = n_pages + 8
+    lay = jfkv.layout(P, hkv, d, G, NP)
+    pb = jfkv.kv_page_bytes(lay)
+    g = torch.Generator(device=dev).manual_seed(11)
+    pools = []
+    for _ in range(n_layers):
+        pl = jfkv.KVPool(lay, device=dev)
+        for n in ("k_codes", "v_codes", "k_meta", "v_meta"):
+            t = getattr(pl, n).view(torch.uint8)
+            t.copy_(torch.randint(0, 256, t.shape, generator=g, device=dev, dtype=torch.uint8))
+        pools.append(pl)
+    rng = np.random.default_rng(11)
+    table = rng.permutation(NP)[:n_pages].astype(np.int32)
+    table2 = rng.permutation(NP)[:n_pages].astype(np.int32)
+    t_dev, t2_dev = torch.from_numpy(table).to(dev), torch.from_numpy(table2).to(dev)
+    stage = 64 << 20
+    sd = torch.empty(stage, dtype=torch.uint8, device=dev)
+    sh = torch.empty(stage, dtype=torch.uint8).pin_memory()
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    # the pack kernel, one layer into device memory
+    buf = torch.empty(n_pages * pb, dtype=torch.uint8, device=dev)
+    steps = max(4, args.steps // 16)
+    t_pack, _ = _back_to_back(lambda s: jfkv.jf_kv_pack_pages(pools[s % n_layers], t_dev, 0,
+                                                              n_pages, buf, stream),
+                              args.warmup, steps, stream)
+    nbytes = 2 * n_pages * pb
+    achieved = nbytes / (t_pack * 1e-6) / 1e9
+    del buf
+    tmp = tempfile.mkdtemp(prefix="jfkv_snap_")
+    try:
+        path = os.path.join(tmp, "prefix.safetensors")
+        torch.cuda.synchronize()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        t0 = time.perf_counter()
+        jfkv.snapshot_save(path, pools, t_dev, table, L, sd, sh, stream)
+        t_save = time.perf_counter() - t0
+        peak_save = (torch.cuda.max_memory_allocated() - base) / 2**20
+        size = os.path.getsize(path)
+        pools2 = [jfkv.KVPool(lay, device=dev) for _ in range(n_layers)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        n_pos = jfkv.snapshot_restore(path, pools2, t2_dev, table2, sd, sh, stream)
+        t_restore = time.perf_counter() - t0
+        assert n_pos == L
+        # spot check: a layer's pages, packed from both pools
+        a = torch.empty(8 * pb, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for layer in (0, n_layers - 1):
+            jfkv.jf_kv_pack_pages(pools[layer], t_dev, n_pages - 8, 8, a, stream)
+            jfkv.jf_kv_pack_pages(pools2[layer], t2_dev, n_pages - 8, 8, b, stream)
+            torch.cuda.synchronize()
+            assert torch.equal(a, b), "restored pages differ"
+        cpu = None
+        if args.cpu_seconds > 0:  # the definition: page bytes gathered in order, written
+            host = [getattr(pools[0], n).view(torch.uint8).cpu().numpy().reshape(NP, -1)
+                    for n in ("k_codes", "k_meta", "v_codes", "v_meta")]
+            n_s = min(128, n_pages)
+            cpath = os.path.join(tmp, "cpu.bin")
+
+            def gather_write():
+                with open(cpath, "wb") as f:
+                    for i in range(n_s):
+                        f.write(np.concatenate([h[table[i]] for h in host]).tobytes())
+            m, dt = _repeat(gather_write, args.cpu_seconds)
+            cpu = dict(value=n_s * pb * m / dt / 1e9, unit="GB/s", cores=1, kind="oracle",
+                       seconds=dt, steps=m,
+                       sample="numpy gather of %d pages of one layer (logical order) and "
+                              "their write to a file, %d time(s)" % (n_s, m), **_host())
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    result = {
+        "metric": "prefix snapshot save GB/s (16 layers x 229,376 positions, 4.2 GB, bounded "
+                  "staging)",
+        "value": size / t_save / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": 1,
+        "warmup": 0, "ms_per_step": t_save * 1e3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u8 (packed pages)", "data": "synthetic (random bytes)",
+        "config": {"workload": "snapshot_224k", "positions": L, "layers": n_layers,
+                   "num_kv_heads": hkv, "head_dim": d, "group_size": G, "page_size": P,
+                   "page_bytes": pb, "file_bytes": size, "staging_MiB_device": stage >> 20,
+                   "staging_MiB_host": stage >> 20},
+        "seconds": {"save": t_save, "restore": t_restore},
+        "restore_GBs": size / t_restore / 1e9,
+        "incremental_device_peak_MiB_during_save": peak_save,
+        "us_per_step": {"pack_one_layer": t_pack},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "page_runs_kernel (pack, one layer into device memory)",
+                     "algorithmic_bytes": nbytes}}
+    if cpu is not None:
+        result["cpu_baseline"] = cpu
+    log("snapshot: save %.3f s, restore %.3f s, pack %.1f us (%.0f GB/s)" % (
+        t_save, t_restore, t_pack, achieved))
+    print(json.dumps(result), flush=True)
+
+
 WORKLOADS = ("decode_256k", "decode_4k", "decode_32k_loop", "ragged_2req", "prefill_chunk",
              "quantize_bulk", "tq4_encode_bulk", "tq4_decode_256k", "verify_256k",
-             "reconstruct_grouped")
+             "reconstruct_grouped", "snapshot_224k")
 
 
 def main():
@@ -1092,6 +1209,8 @@ def main():
         bench_verify(args)
     elif args.workload == "reconstruct_grouped":
         bench_reconstruct(args)
+    elif args.workload == "snapshot_224k":
+        bench_snapshot(args)
     else:
         bench_tq4_decode(args)
 
