@@ -334,8 +334,10 @@ jf_status jf_decode_step_q4_static(const jf_kv_layout* layout,
  *                are read; prefix_len must be <= max_pages * page_size
  *   out      fp16 [T][num_q_heads][d] (device)
  * Products run on fp16 matrix cores with fp32 accumulation.  Key codes
- * enter exactly, with scales and biases applied to the fp32 scores; values
- * enter as scale * code + bias rounded once to fp16. */
+ * enter exactly, with scales and biases applied to the fp32 scores; prefix
+ * values enter as (scale * code + bias) / 2 split into an fp16 high and low
+ * part (exact to ~2^-21 relative, no fp16 overflow for any group), the
+ * chunk's own fp16 rows exactly. */
 jf_status jf_prefill_attn_q4(const jf_kv_layout* layout,
                              const jf_kv_pool_ptrs* pool, const void* q,
                              const void* k_chunk, const void* v_chunk,
