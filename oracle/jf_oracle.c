@@ -356,7 +356,7 @@ int jfo_decode(const jfo_layout* L, const uint8_t* k_codes,
                int32_t Hq, const int32_t* block_tables, int32_t max_pages,
                const int32_t* seq_lens, double alpha, double* out) {
   int32_t H = L->num_kv_heads, d = L->head_dim;
-  if (H <= 0 || Hq % H || d > 512) return -1;
+  if (H <= 0 || B < 0 || Hq % H || d > 512) return -1;
   int32_t gq = Hq / H; /* query heads per KV head; head h reads kv = h / gq */
   for (int32_t b = 0; b < B; ++b)
     if (seq_lens[b] <= 0) return -1;
