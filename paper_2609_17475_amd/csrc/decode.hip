@@ -27,19 +27,22 @@
 //           of lane quarter "slot" (zero elsewhere), so every column belongs
 //           to one scale group; logit = sum over slots of
 //           (scale_g * S^T + bias_g * sum(q over the slot's dims)) * 2^24;
-//   values  O^T[dim][col] += (V codes - 8) [dim][pos] x W [pos][col] with
+//   values  O^T[dim][col] += V codes [dim][pos] x W [pos][col] with
 //           W = p * scale_g (fp16) of the group that column's slot stands
-//           for; the rest of the value, sum(p * (bias_g + 8 scale_g)), is
-//           accumulated separately in fp32 from the exact products p * bias
-//           and p * scale.  The codes enter centred: where an outlier
-//           channel widens a group's range, the other channels' codes sit
-//           near the middle and scale * code and bias are large and of
-//           opposite sign while the value is small, so uncentred sums would
-//           cancel and the matrix cores' fp32 accumulation (and the fp16
-//           rounding of W) would be amplified by |scale * code| / |o|;
-//           centred, the summands are of the size of the values themselves.
-//           A centred code is formed exactly: the nibble ORed into the
-//           mantissa of 1024 (fp16) minus 1032.
+//           for, the codes again subnormal operands (16 code * 2^-24: a
+//           shift and an AND per pair).
+//           The value is assembled as sum W (code - 8) + sum p (bias_g +
+//           8 scale_g): the centred form, because where an outlier channel
+//           widens a group's range the other channels' codes sit near the
+//           middle, scale * code and bias are large and of opposite sign
+//           while the value is small, and the fp16 rounding of W would be
+//           amplified by |scale * code| / |o| in an uncentred sum.  The
+//           centring costs no operand arithmetic: sum W (code - 8) =
+//           sum W code - 8 sum W with sum W taken from the same rounded W,
+//           so it equals the centred sum exactly; only the fp32 accumulation
+//           sees the larger uncentred partial sums (~2^-24 * 15 sum W per
+//           step).  sum p * bias, and sum (p * scale - W), are accumulated
+//           separately in fp32 from exact products.
 // Online softmax keeps one running maximum per head; it is raised only when
 // a logit exceeds it by more than 2 (log2 units), so p <= 4 and p * scale
 // stays within fp16 for any scale the quantizer produces (at most 65504 * 2
@@ -111,6 +114,20 @@ __device__ __forceinline__ float row_ror_add(float v) {
                                                                    0x120 + N, 0xF, 0xF, true));
 }
 
+// Maximum of eight finite or -inf values in four v_max3/v_max instructions
+// (the compiler's IEEE maximum first quiets each operand that does not come
+// from arithmetic it can see, one more instruction per value).  The inputs
+// are results of ordinary vector instructions, which the hardware interlocks.
+__device__ __forceinline__ float max8(float a, float b, float c, float d, float e, float f,
+                                      float g, float h) {
+  float x, y, z, r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(x) : "v"(a), "v"(b), "v"(c));
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(y) : "v"(d), "v"(e), "v"(f));
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(z) : "v"(g), "v"(h), "v"(x));
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(y), "v"(z));
+  return r;
+}
+
 // Lane index from a volatile instruction: code that uses it cannot be hoisted
 // out of a loop, so rarely taken paths keep no lane-derived registers live.
 __device__ __forceinline__ int lane_id_volatile() {
@@ -173,31 +190,22 @@ __device__ __forceinline__ h8 k_operand(uint32_t w) {
   return __builtin_bit_cast(h8, r);
 }
 // Dim K of a 4-dim chunk at eight positions from four position-pair V words
-// (word r: positions 2r and 2r+1), centred: code - 8 (K even) or
-// 16 (code - 8) (K odd: the high nibble of its byte), exact in fp16 (the
-// nibble ORed into 1024.0 gives 1024 + code, or 1024 + 16 code; subtracting
-// 1032, or 1152, is exact); k-slots in position order.  vk holds the masks
-// and the magic number in registers (see opaque), so that mask-and-OR is one
-// v_and_or_b32.
-struct VConsts {
-  uint32_t m_lo, m_hi, magic;
-};
+// (word r: positions 2r and 2r+1) as 16 code * 2^-24, subnormal fp16
+// operands: every nibble is moved to bits 4..7 of its half (the matrix cores
+// sum products of the smallest subnormals, code * 2^-24, with a bias of a few
+// fp32 ulps, which the centring's cancellation would amplify); k-slots in
+// position order.  m holds the mask in a register (see opaque).
 template <int K>
 __device__ __forceinline__ h8 v_operand(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
-                                        const VConsts& vk) {
-  constexpr int SH = (K >= 2) ? 8 : 0;
-  const uint32_t M = (K & 1) ? vk.m_hi : vk.m_lo;
-  constexpr _Float16 kOff = (K & 1) ? (_Float16)1152.0f : (_Float16)1032.0f;
-  const h2 off = {kOff, kOff};
-  const uint32_t ws[4] = {w0, w1, w2, w3};
-  h8 r;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const h2 c = as_h2(((ws[j] >> SH) & M) | vk.magic) - off;
-    r[2 * j] = c.x;
-    r[2 * j + 1] = c.y;
-  }
-  return r;
+                                        uint32_t m) {
+  auto f = [m](uint32_t w) {
+    if constexpr (K == 0) return (w << 4) & m;
+    else if constexpr (K == 1) return w & m;
+    else if constexpr (K == 2) return (w >> 4) & m;
+    else return (w >> 8) & m;
+  };
+  const u32x4 r = {f(w0), f(w1), f(w2), f(w3)};
+  return __builtin_bit_cast(h8, r);
 }
 // A value the compiler cannot see through (no instruction is emitted): a
 // constant passed through it stays in a register instead of being folded
@@ -772,7 +780,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
 #pragma unroll
     for (int k = 0; k < 4; ++k) acc_o[c][k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   float m_run = kMinit, thr = kMinit, l_run = 0.0f;
-  float bacc[NHALF], sacc8[NHALF];  // sums of p * bias and of p * scale (value groups)
+  float bacc[NHALF], sacc8[NHALF];  // sums of p * bias and of p * scale - W (value groups)
 #pragma unroll
   for (int e = 0; e < NHALF; ++e) bacc[e] = sacc8[e] = 0.0f;
 
@@ -801,7 +809,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   int t_row = pb * P + wave * kRowPos;  // first logical position of the row
   int issued_rows = kStages;            // rows whose loads were issued (incl. past the end)
   const h2 ones = {(_Float16)1.0f, (_Float16)1.0f};
-  const VConsts vk = {opaque(0x000F000Fu), opaque(0x00F000F0u), opaque(0x64006400u)};
+  const uint32_t vmask = opaque(0x00F000F0u);
+  const h2 mones = {(_Float16)-1.0f, (_Float16)-1.0f};
   auto row = [&](auto st_c) {
     constexpr int ST = decltype(st_c)::value;
     constexpr int OFF = ST * kStageBytes;
@@ -927,8 +936,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
           for (int e = 0; e < NHALF; ++e) vmw[e][t][i] = ok ? vmw[e][t][i] : 0u;
         }
     }
-    const float mx = kfold * fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
-                                   fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
+    const float mx = kfold * max8(sc[0][0], sc[0][1], sc[0][2], sc[0][3], sc[1][0], sc[1][1],
+                                  sc[1][2], sc[1][3]);
     if (__builtin_amdgcn_ballot_w64(mx > thr) != 0) {
       // new running maximum of the head: lanes with equal lane % 4
       const float M = xor_max_from(mx, 4);
@@ -971,16 +980,17 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         W[e][2 * r + 1] = w.y;
         bacc[e] = __builtin_amdgcn_fdot2(pk[r], bv, bacc[e], false);
         sacc8[e] = __builtin_amdgcn_fdot2(pk[r], sv, sacc8[e], false);
+        sacc8[e] = __builtin_amdgcn_fdot2(w, mones, sacc8[e], false);
       }
     }
     // ---- values: O^T += V codes x W, dims 4 (16 c + m) + k
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const h8 w = W[c >> 1 < NHALF ? c >> 1 : 0];
-      acc_o[c][0] = mfma(v_operand<0>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vk), w, acc_o[c][0]);
-      acc_o[c][1] = mfma(v_operand<1>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vk), w, acc_o[c][1]);
-      acc_o[c][2] = mfma(v_operand<2>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vk), w, acc_o[c][2]);
-      acc_o[c][3] = mfma(v_operand<3>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vk), w, acc_o[c][3]);
+      acc_o[c][0] = mfma(v_operand<0>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask), w, acc_o[c][0]);
+      acc_o[c][1] = mfma(v_operand<1>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask), w, acc_o[c][1]);
+      acc_o[c][2] = mfma(v_operand<2>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask), w, acc_o[c][2]);
+      acc_o[c][3] = mfma(v_operand<3>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask), w, acc_o[c][3]);
     }
     t_row += kWaves * kRowPos;
   };
@@ -1008,8 +1018,9 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     float bsum[NHALF];
 #pragma unroll
     for (int e = 0; e < NHALF; ++e) {
-      // the value groups' sums of p * (bias + 8 scale): the centred codes'
-      // offset restored with the exact products p * scale
+      // the value groups' sums of p * (bias + 8 scale) - 8 W: the bias part
+      // of the value and the centring of the codes (sacc8 holds
+      // sum (p * scale - W))
       float bq = bacc[e] + __shfl_xor(bacc[e], 16);
       bq += __shfl_xor(bq, 32);
       float sq8 = sacc8[e] + __shfl_xor(sacc8[e], 16);
@@ -1026,8 +1037,11 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         const float bg = bsum[(c >> 1) < NHALF ? (c >> 1) : 0];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float4 o4 = make_float4(acc_o[c][0][i] + bg, fmaf(acc_o[c][1][i], 0.0625f, bg),
-                                        acc_o[c][2][i] + bg, fmaf(acc_o[c][3][i], 0.0625f, bg));
+          // (code sums times 2^20, the operands' code scale)
+          const float4 o4 = make_float4(fmaf(acc_o[c][0][i], 1048576.0f, bg),
+                                        fmaf(acc_o[c][1][i], 1048576.0f, bg),
+                                        fmaf(acc_o[c][2][i], 1048576.0f, bg),
+                                        fmaf(acc_o[c][3][i], 1048576.0f, bg));
           *reinterpret_cast<float4*>(part + hse * D + 4 * (16 * c + 4 * qe + i)) = o4;
         }
       }
