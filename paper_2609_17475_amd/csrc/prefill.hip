@@ -368,6 +368,10 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
 
   // ---- one tile from buffer b: scores, online softmax, value products
   auto compute = [&](int b, int key0, int key_lim, bool chunk_tile) {
+    // matrix-core sections at raised wave priority: of the two waves of a
+    // SIMD, the one issuing matrix products goes first and the other's
+    // vector work fills the cycles between them
+    __builtin_amdgcn_s_setprio(1);
     // bias part first: key 16 mt + l16, slots (2g, 2g+1) = (b_g, b_g) on
     // lanes q4 == g / 4; it seeds the folded scores
     f32x4 sacc[MT][NR];
@@ -415,6 +419,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     // interleave the matrix products with the folds and LDS reads around
     // them (the scheduler's single-wave MFMA interleaving)
     __builtin_amdgcn_iglp_opt(1);
+    __builtin_amdgcn_s_setprio(0);
     // keys past the limit, and (chunk tiles) keys after the row's position
     const bool need_mask = key0 + KT > key_lim || (chunk_tile && key0 + KT - 1 > i_min);
     if (need_mask) {
@@ -482,6 +487,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     for (int n = 0; n < NR; ++n)
 #pragma unroll
       for (int k = 0; k < KS; ++k) pb[n][k] = __builtin_bit_cast(h8, pw[n][k]);
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int t = 0; t < DT; ++t)
 #pragma unroll
@@ -503,6 +509,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     // the same interleaving for the value products, the exponentials and the
     // row sums
     __builtin_amdgcn_iglp_opt(1);
+    __builtin_amdgcn_s_setprio(0);
   };
 
   for (int i = tid; i < 2 * KT * NBQ * 4; i += kThreads) (&sKb[0][0][0][0])[i] = 0u;
@@ -510,7 +517,10 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
 
   // ---- tiles 0 .. n_pre - 1 (prefix), then the chunk's; double-buffered:
   // tile j + 1 is reconstructed and tile j + 2's codes are fetched while
-  // tile j is computed; one barrier per tile
+  // tile j is computed; one barrier per tile.  Waves w and w + 4 share a
+  // SIMD; the second half does its part of the reconstruction before the
+  // tile's products and the first half after them, so that on each SIMD one
+  // wave's vector work meets the other's matrix products.
   int page_pf = -1;     // page of the tile in the prefetch registers
   int page_buf[2] = {0, 0};
   if (n_pre > 0) {
@@ -526,26 +536,33 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     stage_chunk(0, 0);
   }
   __syncthreads();
+  const bool early = wave >= kWaves / 2;  // wave-uniform
   for (int j = 0; j < n_tiles; ++j) {
     const int b = j & 1;
-    if (j + 1 < n_tiles) {
-      if (j + 1 < n_pre) {
-        dequant(j + 1, page_pf, b ^ 1);
-        page_buf[b ^ 1] = page_pf;
-      } else {
-        stage_chunk(j + 1 - n_pre, b ^ 1);
-        page_buf[b ^ 1] = 0;
+    // this thread's part of tile j + 1 into buffer b ^ 1, and tile j + 2's codes
+    auto prep = [&]() {
+      if (j + 1 < n_tiles) {
+        if (j + 1 < n_pre) {
+          dequant(j + 1, page_pf, b ^ 1);
+          page_buf[b ^ 1] = page_pf;
+        } else {
+          stage_chunk(j + 1 - n_pre, b ^ 1);
+          page_buf[b ^ 1] = 0;
+        }
       }
-    }
-    if (j + 2 < n_pre) {
-      page_pf = tile_page(j + 2);
-      prefetch(j + 2, page_pf);
-    }
+      if (j + 2 < n_pre) {
+        page_pf = tile_page(j + 2);
+        prefetch(j + 2, page_pf);
+      }
+    };
+    const int page_cur = page_buf[b];
+    if (early) prep();
     const bool chunk_tile = j >= n_pre;
     if (chunk_tile)
       compute(b, (j - n_pre) * KT, T, true);
-    else if ((unsigned)page_buf[b] < (unsigned)NP)  // a tile on an invalid page is skipped
+    else if ((unsigned)page_cur < (unsigned)NP)  // a tile on an invalid page is skipped
       compute(b, j * KT, prefix_len, false);
+    if (!early) prep();
     __syncthreads();
   }
 
