@@ -79,7 +79,6 @@ constexpr float kTau = 2.0f;  // lazy-rescale margin, log2 units
 constexpr float kMinit = -1e30f;
 constexpr int kMaxThreads = 512;    // a block: one split, one block per CU
 constexpr int kRowPos = 32;         // positions per row: two 16-position MFMA tiles
-constexpr int kHeadSlots = 4;       // query heads per block
 constexpr int kXcds = 8;            // XCDs of the chip (block placement only)
 constexpr int kRingBudget = 162816; // LDS bytes of a block's rings (a CU's LDS less 1 KiB)
 // Waves per block: two per SIMD where the LDS rings fit (d <= 128), so one
@@ -94,6 +93,16 @@ constexpr int kRingBudget = 162816; // LDS bytes of a block's rings (a CU's LDS 
 #endif
 template <int D>
 constexpr int waves_for() { return D <= 128 ? JF_DECODE_WAVES : 4; }
+// Query heads per block (a head chunk): the 16 columns of the matrix-core
+// products are head slots times column slots, and each column slot stands for
+// one scale group of a 128-dim half, so a head needs as many columns as a
+// half has groups (at least one); at most one head per wave (the combine).
+template <int D, int G>
+constexpr int head_slots() {
+  constexpr int ngh = (D < 128 ? D : 128) / G;
+  constexpr int hs = 16 / (ngh > 0 ? ngh : 1);
+  return hs < waves_for<D>() ? hs : waves_for<D>();
+}
 constexpr int kMaxStages = JF_DECODE_STAGES;  // LDS ring depth per wave (at most)
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
@@ -485,6 +494,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   constexpr int kFit = (kRingBudget - 16) / (kWaves * kStageBytes);
   constexpr int kStages = kFit < kMaxStages ? kFit : kMaxStages;
   static_assert(kStages >= 2, "ring depth");
+  constexpr int kHeadSlots = head_slots<D, G>();
+  constexpr int NS = 16 / kHeadSlots;      // column slots per head
   static_assert(kWaves % kHeadSlots == 0, "whole waves per head in the combine");
   constexpr bool kSwz = (D == 128);
   static_assert(DMAS_PER_ROW * (kStages - 1) < 64, "vmcnt range");
@@ -522,7 +533,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
 
   const int l16 = lane & 15, q4 = lane >> 4;
-  const int hs = l16 & 3, gs = l16 >> 2;  // accumulator column: head slot, column slot
+  const int hs = l16 % kHeadSlots, gs = l16 / kHeadSlots;  // accumulator column: head, slot
   const bool head_on = hs < nh;
 
   // Loads issued together, before anything waits for the request's length:
@@ -729,13 +740,15 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     }
   }
 
-  // ---- Q' operands.  Score column hs + 4 gs holds head hs restricted to the
-  // dims of scale group gs % NGH of each half (columns with equal group are
-  // copies), so each column's sum has one scale; k-slots (n0, n4, n1, n5, n2,
-  // n6, n3, n7) of each code word, odd nibbles' dims divided by 16.  qs: the
-  // group's query sum (times 2^-24, the code scale), its bias factor.
+  // ---- Q' operands.  Score column hs + kHeadSlots gs holds head hs
+  // restricted to the dims of scale group gs % NGH of each half (columns with
+  // equal group are copies), so each column's sum has one scale; k-slots (n0,
+  // n4, n1, n5, n2, n6, n3, n7) of each code word, odd nibbles' dims divided
+  // by 16.  qs: the group's query sum (times 2^-24, the code scale), its bias
+  // factor.  The value column of the same slot carries the same group.
   constexpr int NGH = HD / G;            // scale groups per half
-  const int gcol = gs % NGH;             // group (within a half) of the score column
+  static_assert(NS % NGH == 0, "every group of a half has a column slot");
+  const int gcol = gs % NGH;             // group (within a half) of the column
   const bool q_on = head_on && (DQ * q4) / G == gcol;
   // a negative softmax scale negates the query (exact) and leaves |scale|
   const uint32_t qneg = scale_log2 < 0.0f ? 0x80008000u : 0u;
@@ -797,8 +810,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   }
   {
     kma = ring_lds + 2 * KB + (gcol * kRowPos + 8 * q4) * 4;  // score column's group
-    const int gv = min((32 * gs) / G, NG - 1);  // group of the value column (first half)
-    vma = ring_lds + 2 * KB + kMetaBytes + (gv * kRowPos + 8 * q4) * 4;
+    vma = ring_lds + 2 * KB + kMetaBytes + (gcol * kRowPos + 8 * q4) * 4;  // (first half)
   }
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
@@ -908,8 +920,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         for (int t = 0; t < 2; ++t) sacc[e][t] = mfma(k_operand(kw[e][t][kb]), qB[e][kb], sacc[e][t]);
 
     // ---- logits: fold each column's group scale and bias, sum the distinct
-    // groups of the head (lanes l16 + 4k of the 16-lane row: columns of equal
-    // group are copies, so NGH - 1 rotations suffice), scale
+    // groups of the head (lanes l16 + kHeadSlots k of the 16-lane row: slots
+    // gs and gs + NGH are copies, so log2(NGH) rotations suffice), scale
     float sc[2][4];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -918,8 +930,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         float a = 0.0f;
 #pragma unroll
         for (int e = 0; e < NHALF; ++e) a = fold_meta(kmw[e][t][i], sacc[e][t][i], qs[e], a);
-        if constexpr (NGH >= 2) a = row_ror_add<4>(a);
-        if constexpr (NGH >= 4) a = row_ror_add<8>(a);
+        if constexpr (NGH >= 2) a = row_ror_add<kHeadSlots>(a);
+        if constexpr (NGH >= 4) a = row_ror_add<2 * kHeadSlots>(a);
         sc[t][i] = a;  // (scaled by kfold in the exponent)
       }
     if (!full) {
@@ -939,8 +951,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     const float mx = kfold * max8(sc[0][0], sc[0][1], sc[0][2], sc[0][3], sc[1][0], sc[1][1],
                                   sc[1][2], sc[1][3]);
     if (__builtin_amdgcn_ballot_w64(mx > thr) != 0) {
-      // new running maximum of the head: lanes with equal lane % 4
-      const float M = xor_max_from(mx, 4);
+      // new running maximum of the head: lanes with equal lane % kHeadSlots
+      const float M = xor_max_from(mx, kHeadSlots);
       if (M > m_run) {
         const float alpha = __builtin_amdgcn_exp2f(m_run - M);
         m_run = M;
@@ -1014,7 +1026,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   {
     const int lane_e = lane_id_volatile();
     const int me = lane_e & 15, qe = lane_e >> 4;
-    const int hse = me & 3, gse = me >> 2;
+    const int hse = me % kHeadSlots, gse = me / kHeadSlots;
     float bsum[NHALF];
 #pragma unroll
     for (int e = 0; e < NHALF; ++e) {
@@ -1031,9 +1043,12 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     lsum += __shfl_xor(lsum, 32);
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      // lane (col, qe) holds dims 4 (16 c + 4 qe + i) + k; its column's slot
-      // stands for their group when gse == 2 (c % 2) + qe / 2
-      if (gse == 2 * (c & 1) + (qe >> 1)) {
+      // lane (col, qe) holds dims 4 (16 c + 4 qe + i) + k, of group
+      // (64 (c % 2) + 16 qe) / G of their half; its column's slot stands for
+      // that group when gse % NGH equals it, and of the NS / NGH copies of a
+      // group copy r writes rows qe with qe (NS / NGH) / 4 == r
+      constexpr int R = NS / NGH;
+      if (gse % NGH == (64 * (c & 1) + 16 * qe) / G && gse / NGH == (qe * R) / 4) {
         const float bg = bsum[(c >> 1) < NHALF ? (c >> 1) : 0];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -1113,6 +1128,7 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
                     const int32_t* lens, float scale, int32_t max_splits, uint32_t* tickets,
                     float* records, void* out, int32_t sq, hipStream_t stream) {
   const int gq = Hq / L.num_kv_heads;
+  constexpr int kHeadSlots = head_slots<D, G>();
   const int n_hchunks = (gq + kHeadSlots - 1) / kHeadSlots;
   // Splits per request: enough blocks for one per CU when one request runs
   // alone, at most max_splits.  The count does not depend on the batch (a

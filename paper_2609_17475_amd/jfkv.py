@@ -272,6 +272,13 @@ def jf_kv_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_t
                                      _stream(stream)))
 
 
+def decode_head_chunk(head_dim: int, group_size: int) -> int:
+    """Query heads one decode block serves (a head chunk; the split cap of
+    jf_decode_attn_q4 divides the compute units by num_kv_heads * ceil(Gq /
+    this)): 4 for 32-dim groups or head_dim 256, else 8."""
+    return 4 if group_size == 32 or head_dim == 256 else 8
+
+
 def jf_decode_workspace_bytes(B: int, num_q_heads: int, head_dim: int, max_splits: int) -> int:
     n = ctypes.c_size_t()
     _check(lib.jf_decode_workspace_bytes(B, num_q_heads, head_dim, max_splits, ctypes.byref(n)))

@@ -36,7 +36,10 @@ def _q(seed, B, hq, d, scale=None):
     (256, 4, 24, 256, 64, (600,)),   # the paper's 24 q / 4 KV heads, d = 256
     (128, 2, 2, 128, 64, (300,)),    # one query head per KV head
     (64, 2, 6, 128, 32, (500,)),     # three per KV head
-    (64, 1, 8, 128, 64, (333,)),     # eight per KV head (two head chunks)
+    (64, 1, 8, 128, 64, (333,)),     # eight per KV head (one head chunk of eight)
+    (64, 1, 16, 128, 64, (333,)),    # sixteen per KV head (two chunks of eight)
+    (64, 2, 20, 128, 128, (400,)),   # ten per KV head, one group per half (chunks 8 + 2)
+    (64, 1, 12, 64, 64, (500,)),     # d = 64, twelve per KV head (chunks 8 + 4)
 ])
 def test_decode_matches_oracle(P, hkv, hq, d, G, lens):
     log("decode P=%d hkv=%d hq=%d d=%d G=%d lens=%s" % (P, hkv, hq, d, G, lens))

@@ -186,3 +186,37 @@ def test_tq4_decode_full_window():
     ref = case.oracle(q)
     err, rel = check_tol(got, ref, what="tq4 full window", **TOL)
     log("  max err %.2e rel L2 %.2e" % (err, rel))
+
+
+def test_workspace_shared_with_affine_decode_and_verifier():
+    """One workspace serves, in turn, affine decode, the short verifier, TQ4
+    decode and affine decode again, with different head counts and split
+    caps: every call leaves the completion counters zero, and every output
+    equals the output of the same call on a fresh workspace bitwise."""
+    from gpu_cases import build, decode_gpu
+    log("workspace shared by decode, verifier and TQ4 decode")
+    tq = Case(256, 4, (1500,), seed=91)
+    aff = build(P=64, hkv=2, d=128, G=64, hq=8, lens=(64 * 20 + 3,), seed=92)
+    ws = torch.zeros(jfkv.jf_decode_workspace_bytes(1, 24, D, 64), dtype=torch.uint8,
+                     device=DEV)
+    qa = _q(93, 1, 8)[:, :, :128].copy()
+    qv = (np.random.default_rng(94).standard_normal((1, 3, 8, 128)) / 16).astype(np.float16)
+    qt = _q(95, 1, 24)
+
+    def verify(w):
+        out = torch.empty((1, 3, 8, 128), dtype=torch.float16, device=DEV)
+        jfkv.jf_verify_attn_q4(aff.gpu, torch.from_numpy(qv).to(DEV),
+                               torch.from_numpy(aff.tables).to(DEV),
+                               torch.tensor(aff.lens, dtype=torch.int32, device=DEV), 1.0, 16,
+                               w, out)
+        torch.cuda.synchronize()
+        return out.cpu().numpy()
+
+    calls = [lambda w: decode_gpu(aff, qa, max_splits=64, ws=w), verify,
+             lambda w: tq.gpu(qt, max_splits=64, ws=w),
+             lambda w: decode_gpu(aff, qa, max_splits=5, ws=w), lambda w: tq.gpu(qt, max_splits=3, ws=w)]
+    for i, call in enumerate(calls):
+        got = call(ws)
+        assert torch.count_nonzero(ws[:262144]).item() == 0, "call %d left a counter set" % i
+        fresh = call(torch.zeros_like(ws))
+        assert np.array_equal(got, fresh), "call %d differs from a fresh workspace" % i
