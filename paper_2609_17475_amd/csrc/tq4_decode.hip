@@ -12,14 +12,13 @@
 // So the scan reads the packed indices and the norms where they are stored
 // (page-native, Sec. 3.1) and never reconstructs a vector.
 //
-// Each 4-bit index becomes its centroid as an fp16 matrix-core operand by
-// byte-permute lookups: the 16 fp16 centroids are held as two byte planes of
-// four registers each; one v_perm_b32 per plane and table half fetches the
-// low or high bytes of four entries, a byte mask from the index's top bit
-// picks the table half, and two more permutes interleave the bytes into
-// fp16 pairs (about three instructions per index, shared by every query
-// head of the KV head).  The centroids are rounded to fp16 once (relative
-// error <= 2^-11); q' enters as an fp16 high part plus an fp16 low part.
+// Each byte of packed indices becomes the fp16 centroids of its two indices
+// by one LDS read from a 256-entry table of centroid pairs (entry e: c[e % 16]
+// in the low half, c[e / 16] in the high half), shared by every query head of
+// the KV head: for keys the pair is directly an operand word (dims 2j, 2j + 1
+// of one position); for values two reads and a permute give one dim at two
+// positions.  The centroids are rounded to fp16 once (relative error
+// <= 2^-11); q' enters as an fp16 high part plus an fp16 low part.
 //
 // Matrix-core layout (v_mfma_f32_16x16x32_f16; lane (m, q4) = (lane % 16,
 // lane / 16) feeds operand row m, k-slots 8 q4 .. 8 q4 + 7, and receives
@@ -27,8 +26,7 @@
 //   scores  S^T[pos][head] over 8 k-steps of 32 dims, two 16-position tiles
 //           per 32-position row; tile t row m is position 8 (m / 4) + 4 t +
 //           m % 4, and k-step kb of lane quarter q4 is index word 8 q4 + kb
-//           (dims in the order 0, 2, 4, 6, 1, 3, 5, 7 of the word, the order
-//           the nibble selectors produce), so each lane's K data is 32
+//           (dims 0..7 of the word in order), so each lane's K data is 32
 //           contiguous bytes of one position and its scores are positions
 //           8 q4 .. 8 q4 + 7;
 //   values  u^T[dim][head] += c[z][dim][pos] x W[pos][head], W = p rho^_V
@@ -36,8 +34,9 @@
 //           (m, q4) holds index words 2 m, 2 m + 1 of positions 8 q4 ..
 //           8 q4 + 7 (8 bytes each) and the k-slots are exactly the positions
 //           of its own scores; byte b of those words holds dims 16 m + 2 b
-//           and + 1 of one position, gathered over four positions by three
-//           permutes into one selector word.
+//           and + 1 of one position.
+// Two waves per SIMD (eight per block): the table reads' latency of one wave
+// is covered by the other's work.
 // Online softmax per head with a lazy running maximum (raised only when a
 // logit exceeds it by more than 2 in log2 units, so p <= 4).
 #include <hip/hip_fp16.h>
@@ -58,7 +57,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kD = 256;           // head dimension of the format
 constexpr int kWordsPerVec = kD / 8;
-constexpr int kWaves = 4;         // one wave per SIMD, one block per CU
+constexpr int kWaves = 8;         // two waves per SIMD, one block per CU
+constexpr int kParts = 4;         // per-wave partial buffers (waves w and w + 4 merge first)
 constexpr int kThreads = 64 * kWaves;
 constexpr int kRowPos = 32;       // positions per row (two 16-position tiles)
 constexpr int kMaxCols = 16;      // query heads per KV head: one column block
@@ -67,67 +67,8 @@ constexpr float kTau = 2.0f;      // lazy-rescale margin, log2 units
 constexpr float kMinit = -1e30f;  // finite initial maximum (masked rows give p = 0)
 constexpr int kMaxSplits = 256;   // split cap of the launch (the combine's LDS bound)
 
-// Byte planes of the 16 fp16 centroids: l[k] holds the low bytes of entries
-// 4k .. 4k + 3, h[k] their high bytes.
-struct Tab {
-  uint32_t l[4], h[4];
-};
-
 __device__ __forceinline__ f32x4 mfma(h8 a, h8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
-
-// m ? a : b, bitwise
-__device__ __forceinline__ uint32_t bsel(uint32_t m, uint32_t a, uint32_t b) {
-  return (a & m) | (b & ~m);
-}
-
-// 0xFF in each byte of the result whose byte of x has its top bit set (byte
-// permute selectors 8..11 replicate the top bit of bytes 1, 3, 5, 7 of the
-// pair {x, x << 8}, i.e. of bytes 0, 2, 1, 3 of x).
-__device__ __forceinline__ uint32_t top_bit_mask(uint32_t x) {
-  return __builtin_amdgcn_perm(x, x << 8, 0x0B090A08u);
-}
-
-// The fp16 centroids of four indices given as entry bytes i (0..7 within a
-// table half) and half masks m (0xFF where the index is 8..15):
-// e01 = entries of bytes 0 and 1, e23 = of bytes 2 and 3 (low half first).
-__device__ __forceinline__ void lookup4(uint32_t i, uint32_t m, const Tab& T, uint32_t& e01,
-                                        uint32_t& e23) {
-  const uint32_t lo = bsel(m, __builtin_amdgcn_perm(T.l[3], T.l[2], i),
-                           __builtin_amdgcn_perm(T.l[1], T.l[0], i));
-  const uint32_t hi = bsel(m, __builtin_amdgcn_perm(T.h[3], T.h[2], i),
-                           __builtin_amdgcn_perm(T.h[1], T.h[0], i));
-  e01 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
-  e23 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
-}
-
-// The centroids of the four low nibbles (n = 0) or high nibbles (n = 1) of
-// the bytes of w: bit 3 of a low nibble is bit 7 of w << 4.
-__device__ __forceinline__ void lookup_nibbles(uint32_t w, int n, const Tab& T, uint32_t& e01,
-                                               uint32_t& e23) {
-  if (n == 0)
-    lookup4(w & 0x07070707u, top_bit_mask(w << 4), T, e01, e23);
-  else
-    lookup4((w >> 4) & 0x07070707u, top_bit_mask(w), T, e01, e23);
-}
-
-// Score operand of one index word (eight consecutive dims of one position):
-// k-slots hold dims 0, 2, 4, 6, 1, 3, 5, 7 of the word.
-__device__ __forceinline__ h8 k_operand(uint32_t w, const Tab& T) {
-  uint32_t r0, r1, r2, r3;
-  lookup_nibbles(w, 0, T, r0, r1);
-  lookup_nibbles(w, 1, T, r2, r3);
-  const u32x4 r = {r0, r1, r2, r3};
-  return __builtin_bit_cast(h8, r);
-}
-
-// Byte b of the words a0 .. a3 (four positions) as one selector word.
-__device__ __forceinline__ uint32_t gather_byte(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3,
-                                                uint32_t sel_pair) {
-  const uint32_t x01 = __builtin_amdgcn_perm(a1, a0, sel_pair);
-  const uint32_t x23 = __builtin_amdgcn_perm(a3, a2, sel_pair);
-  return __builtin_amdgcn_perm(x23, x01, 0x05040100u);
 }
 
 // In-place Walsh-Hadamard transform (unnormalised, natural order) of n rows
@@ -170,9 +111,10 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     float* __restrict__ ws, uint32_t* __restrict__ tickets, __half* __restrict__ out, int Hq,
     int Hkv, int P, int NP, int max_pages, int max_splits, int split_cap, float scale_log2) {
   __shared__ float s_x[kMaxCols * kD];                   // q' rotation; final rotation
-  __shared__ float s_part[kWaves][kMaxCols * (kD + 2)];  // per-wave partials (u, m, l)
+  __shared__ float s_part[kParts][kMaxCols * (kD + 2)];  // per-wave partials (u, m, l)
   __shared__ h8 s_qop[8][2][64];                         // score B operands (q' high, low)
   __shared__ uint32_t s_ticket;
+  __shared__ uint32_t s_pair[256];  // index byte -> fp16 centroids of its low and high nibble
 
   const int split = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
   const int gq = Hq / Hkv;
@@ -195,19 +137,11 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   split_range(n_pages, S, split, pb, pe);
   const int t_end = min(pe * P, L);
 
-  // ---- centroid byte planes (fp16, round to nearest even)
-  Tab T;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    uint32_t lo = 0, hi = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t bits = __builtin_bit_cast(uint16_t, (_Float16)centroids[4 * k + e]);
-      lo |= (bits & 0xFFu) << (8 * e);
-      hi |= (bits >> 8) << (8 * e);
-    }
-    T.l[k] = lo;
-    T.h[k] = hi;
+  // pair table: entry e holds c[e & 15] (low half) and c[e >> 4] (high half)
+  for (int e = tid; e < 256; e += kThreads) {
+    const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)centroids[e & 15]);
+    const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)centroids[e >> 4]);
+    s_pair[e] = lo | (hi << 16);
   }
 
   // ---- q' = H S q / 16 per query head (a negative scale negates it)
@@ -219,8 +153,8 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   __syncthreads();
   fwht_rows(s_x, gq);
   // B operands in LDS (one 16-byte entry per lane, read back conflict-free):
-  // k-step kb, lane (col, q4): word 8 q4 + kb, dims 0,2,4,6,1,3,5,7, as an
-  // fp16 high part and an fp16 low part; waves fill two k-steps each
+  // k-step kb, lane (col, q4): word 8 q4 + kb, dims 0..7 of it, as an
+  // fp16 high part and an fp16 low part; each wave fills one k-step
 #pragma unroll
   for (int k2 = 0; k2 < 8 / kWaves; ++k2) {
     const int kb = (8 / kWaves) * wave + k2;
@@ -229,7 +163,7 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     h8 hi, lo;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int d = 8 * w + ((e < 4) ? 2 * e : 2 * (e - 4) + 1);
+      const int d = 8 * w + e;
       const float v = s_x[min(l16, gq - 1) * kD + d] * 0.0625f;
       const _Float16 vh = col_on ? (_Float16)v : (_Float16)0.0f;
       hi[e] = vh;
@@ -302,7 +236,10 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
       const h8 qh = s_qop[kb][0][lane], ql = s_qop[kb][1][lane];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const h8 a = k_operand(w[t][kb], T);
+        const uint32_t x = w[t][kb];
+        const u32x4 r = {s_pair[x & 0xFFu], s_pair[(x >> 8) & 0xFFu], s_pair[(x >> 16) & 0xFFu],
+                         s_pair[x >> 24]};
+        const h8 a = __builtin_bit_cast(h8, r);
         acc[t] = mfma(a, qh, acc[t]);
         acc[t] = mfma(a, ql, acc[t]);
       }
@@ -359,18 +296,18 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     // ---- values: product j has row m = dim 16 m + j
 #pragma unroll
     for (int bb = 0; bb < 8; ++bb) {
-      const uint32_t selp = (uint32_t)(bb & 3) | ((uint32_t)(4 + (bb & 3)) << 8) | 0x0C0C0000u;
-      uint32_t src[8];
+      // centroid pairs (low, high nibble of byte bb) of the eight positions
+      uint32_t t[8];
 #pragma unroll
-      for (int p = 0; p < 8; ++p) src[p] = (bb < 4) ? rb.v[p].x : rb.v[p].y;
-      const uint32_t s03 = gather_byte(src[0], src[1], src[2], src[3], selp);
-      const uint32_t s47 = gather_byte(src[4], src[5], src[6], src[7], selp);
+      for (int p = 0; p < 8; ++p) {
+        const uint32_t word = (bb < 4) ? rb.v[p].x : rb.v[p].y;
+        t[p] = s_pair[(word >> (8 * (bb & 3))) & 0xFFu];
+      }
 #pragma unroll
       for (int hn = 0; hn < 2; ++hn) {  // low nibble: dim 16 m + 2 bb; high: + 1
-        uint32_t a0, a1, a2, a3;
-        lookup_nibbles(s03, hn, T, a0, a1);
-        lookup_nibbles(s47, hn, T, a2, a3);
-        const u32x4 a = {a0, a1, a2, a3};
+        const uint32_t sel = hn ? 0x07060302u : 0x05040100u;
+        const u32x4 a = {__builtin_amdgcn_perm(t[1], t[0], sel), __builtin_amdgcn_perm(t[3], t[2], sel),
+                         __builtin_amdgcn_perm(t[5], t[4], sel), __builtin_amdgcn_perm(t[7], t[6], sel)};
         const int j = 2 * bb + hn;
         acc_v[j] = mfma(__builtin_bit_cast(h8, a), W, acc_v[j]);
       }
@@ -393,8 +330,9 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   {
     float lsum = l_run + __shfl_xor(l_run, 16);
     lsum += __shfl_xor(lsum, 32);
-    float* part = s_part[wave];
-    if (l16 < gq) {
+    // waves 4..7 write their partials; waves 0..3 fold their own into them
+    float* part = s_part[wave & (kParts - 1)];
+    if (wave >= kParts && l16 < gq) {
 #pragma unroll
       for (int j = 0; j < 16; ++j)
 #pragma unroll
@@ -404,19 +342,36 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
         part[l16 * (kD + 2) + kD + 1] = lsum;
       }
     }
+    __syncthreads();
+    if (wave < kParts && l16 < gq) {
+      const float mo = part[l16 * (kD + 2) + kD], lo = part[l16 * (kD + 2) + kD + 1];
+      const float M = fmaxf(m_run, mo);
+      const float f = __builtin_amdgcn_exp2f(m_run - M), fo = __builtin_amdgcn_exp2f(mo - M);
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float* u = &part[l16 * (kD + 2) + 64 * q4 + 16 * i + j];
+          *u = fmaf(f, acc_v[j][i], fo * *u);
+        }
+      if (q4 == 0) {
+        part[l16 * (kD + 2) + kD] = M;
+        part[l16 * (kD + 2) + kD + 1] = fmaf(f, lsum, fo * lo);
+      }
+    }
   }
   __syncthreads();
   for (int o = tid; o < gq * kD; o += kThreads) {
     const int h = o / kD, d = o % kD;
-    float mw[kWaves], M = kMinit;
+    float mw[kParts], M = kMinit;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < kParts; ++w) {
       mw[w] = s_part[w][h * (kD + 2) + kD];
       M = fmaxf(M, mw[w]);
     }
     float num = 0.0f, den = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < kParts; ++w) {
       const float f = __builtin_amdgcn_exp2f(mw[w] - M);
       num = fmaf(f, s_part[w][h * (kD + 2) + d], num);
       den = fmaf(f, s_part[w][h * (kD + 2) + kD + 1], den);
