@@ -17,7 +17,9 @@
 // in the low half, c[e / 16] in the high half), shared by every query head of
 // the KV head: for keys the pair is directly an operand word (dims 2j, 2j + 1
 // of one position); for values two reads and a permute give one dim at two
-// positions.  The centroids are rounded to fp16 once (relative error
+// positions.  The table is held 32 times, interleaved so that lane l reads
+// copy l % 32 from bank l % 32 (random entries would otherwise collide in
+// the LDS banks).  The centroids are rounded to fp16 once (relative error
 // <= 2^-11); q' enters as an fp16 high part plus an fp16 low part.
 //
 // Matrix-core layout (v_mfma_f32_16x16x32_f16; lane (m, q4) = (lane % 16,
@@ -114,7 +116,7 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   __shared__ float s_part[kParts][kMaxCols * (kD + 2)];  // per-wave partials (u, m, l)
   __shared__ h8 s_qop[8][2][64];                         // score B operands (q' high, low)
   __shared__ uint32_t s_ticket;
-  __shared__ uint32_t s_pair[256];  // index byte -> fp16 centroids of its low and high nibble
+  __shared__ uint32_t s_pair[256 * 32];  // index byte -> fp16 centroids of its nibbles, 32 copies
 
   const int split = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
   const int gq = Hq / Hkv;
@@ -137,11 +139,13 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   split_range(n_pages, S, split, pb, pe);
   const int t_end = min(pe * P, L);
 
-  // pair table: entry e holds c[e & 15] (low half) and c[e >> 4] (high half)
+  // pair table: entry e holds c[e & 15] (low half) and c[e >> 4] (high half),
+  // copy c at word 32 e + c
   for (int e = tid; e < 256; e += kThreads) {
     const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)centroids[e & 15]);
     const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)centroids[e >> 4]);
-    s_pair[e] = lo | (hi << 16);
+#pragma unroll
+    for (int c = 0; c < 32; ++c) s_pair[e * 32 + c] = lo | (hi << 16);
   }
 
   // ---- q' = H S q / 16 per query head (a negative scale negates it)
@@ -214,6 +218,7 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     rb.vn = *reinterpret_cast<const uint4*>(v_norms + vec0 + 8 * q4);
   };
 
+  const uint32_t* tab = s_pair + (lane & 31);  // this lane's copy: its own bank
   f32x4 acc_v[16];
 #pragma unroll
   for (int j = 0; j < 16; ++j) acc_v[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -237,8 +242,8 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const uint32_t x = w[t][kb];
-        const u32x4 r = {s_pair[x & 0xFFu], s_pair[(x >> 8) & 0xFFu], s_pair[(x >> 16) & 0xFFu],
-                         s_pair[x >> 24]};
+        const u32x4 r = {tab[(x & 0xFFu) * 32], tab[((x >> 8) & 0xFFu) * 32],
+                         tab[((x >> 16) & 0xFFu) * 32], tab[(x >> 24) * 32]};
         const h8 a = __builtin_bit_cast(h8, r);
         acc[t] = mfma(a, qh, acc[t]);
         acc[t] = mfma(a, ql, acc[t]);
@@ -301,7 +306,7 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
 #pragma unroll
       for (int p = 0; p < 8; ++p) {
         const uint32_t word = (bb < 4) ? rb.v[p].x : rb.v[p].y;
-        t[p] = s_pair[(word >> (8 * (bb & 3))) & 0xFFu];
+        t[p] = tab[((word >> (8 * (bb & 3))) & 0xFFu) * 32];
       }
 #pragma unroll
       for (int hn = 0; hn < 2; ++hn) {  // low nibble: dim 16 m + 2 bb; high: + 1
