@@ -16,9 +16,19 @@
 //
 // Index of a coordinate: the number of midpoint thresholds between adjacent
 // centroids that it strictly exceeds (a coordinate on a threshold keeps the
-// lower index), found by a 4-step binary search over the float32 midpoints
-// (c_j + c_{j+1}) / 2 held in LDS.  y is the transformed vector times one
-// correctly rounded reciprocal of 16 rho.
+// lower index), over the float32 midpoints (c_j + c_{j+1}) / 2.  It is read
+// from a table of 64 buckets of the coordinate range: the bucket map
+// floor(y / w + o), clamped, is monotone, so every threshold whose own
+// bucket is lower lies below y and every one in a higher bucket above it;
+// an entry holds the count of thresholds in lower buckets and the one
+// threshold of its bucket (+inf if none), and the index is that count plus
+// one comparison.  If a codebook puts two thresholds in one bucket, the block
+// uses a 4-step binary search over the midpoints instead.  Both give the
+// same index for every y.  y is the transformed vector times one correctly
+// rounded reciprocal of 16 rho.
+//
+// The destination of a row (request, logical position, page) is looked up
+// once per row: a wave's vectors are consecutive, Hkv of them per row.
 // A vector of norm 0 has every coordinate 0.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -33,6 +43,7 @@ constexpr int kD = 256;          // head dimension of the format
 constexpr int kWavesPerBlock = 4;
 constexpr int kVecPerWave = 8;   // vectors per wave, their loads issued together
 constexpr int kLevels = 16;
+constexpr int kBuckets = 64;     // index buckets (at most one threshold each)
 
 __device__ __forceinline__ float2 h2_to_f2(uint32_t u) {
   return __half22float2(__builtin_bit_cast(__half2, u));
@@ -75,11 +86,41 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
     int n_vec) {
   // thresholds for a 4-step binary search: entry 15 is +inf (never passed)
   __shared__ float thr[kLevels];
+  // bucket table: y falls in bucket b = clamp(floor(fma(y, bk_inv, bk_off)),
+  // 0, kBuckets - 1), a monotone map, so every threshold in a lower bucket is
+  // below y and every one in a higher bucket above it; entry b holds their
+  // count (below) and the bucket's own threshold (+inf if none)
+  __shared__ float2 bucket[kBuckets];
+  __shared__ int s_multi;  // a bucket holds two thresholds: binary search instead
   if (threadIdx.x < kLevels)
     thr[threadIdx.x] = threadIdx.x < kLevels - 1
                            ? (centroids[threadIdx.x] + centroids[threadIdx.x + 1]) * 0.5f
                            : INFINITY;
+  if (threadIdx.x == 0) s_multi = 0;
   __syncthreads();
+  // buckets of width (t_14 - t_0) / (kBuckets - 2) from one width below t_0
+  const float t_first = thr[0], t_last = thr[kLevels - 2];
+  const float bk_inv = (float)(kBuckets - 2) / (t_last - t_first);
+  const float bk_off = 1.0f - t_first * bk_inv;
+  auto bucket_of = [&](float y) {  // (clamped before the conversion: no overflow)
+    return (int)__builtin_amdgcn_fmed3f(fmaf(y, bk_inv, bk_off), 0.0f, (float)(kBuckets - 1));
+  };
+  if (threadIdx.x < kBuckets) {
+    int below = 0, inside = 0;
+    float t_in = INFINITY;
+    for (int k = 0; k < kLevels - 1; ++k) {
+      const int bt = bucket_of(thr[k]);
+      below += bt < (int)threadIdx.x;
+      if (bt == (int)threadIdx.x) {
+        ++inside;
+        t_in = thr[k];
+      }
+    }
+    bucket[threadIdx.x] = make_float2(__builtin_bit_cast(float, below), t_in);
+    if (inside > 1 || !(bk_inv > 0.0f) || !isfinite(bk_inv)) s_multi = 1;  // benign race: all write 1
+  }
+  __syncthreads();
+  const bool use_buckets = s_multi == 0;  // block-uniform
 
   const int lane = threadIdx.x & 63;
   // wave-uniform from here to the stores: the vector, its request, page and
@@ -95,11 +136,12 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
   for (int v = 0; v < kVecPerWave; ++v)
     if (v < nv) raw[v] = __builtin_nontemporal_load(&xw[(int64_t)(vec0 + v) * (kD / 4) + lane]);
   const float4 s = reinterpret_cast<const float4*>(signs)[lane];
+  int row_cur = vec0 / Hkv, kv_cur = vec0 - row_cur * Hkv;  // of the next vector
+  int row_done = -1, page_row = -1, slot_in_page = 0;       // the looked-up row
 
 #pragma unroll
   for (int v = 0; v < kVecPerWave; ++v) {
     if (v >= nv) break;
-    const int vec = vec0 + v;
     const float2 f01 = h2_to_f2((uint32_t)raw[v]), f23 = h2_to_f2((uint32_t)(raw[v] >> 32));
 
     // norm: squares of fp16 values are exact in float32
@@ -129,6 +171,14 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
     const float y[4] = {e0 * inv, e1 * inv, e2 * inv, e3 * inv};
 
     uint32_t q = 0;  // four 4-bit indices: element 4 lane + j at bits 4j
+    if (use_buckets) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float2 e = bucket[bucket_of(y[j])];
+        const int idx = __builtin_bit_cast(int, e.x) + (y[j] > e.y ? 1 : 0);
+        q |= (uint32_t)idx << (4 * j);
+      }
+    } else {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       // off = 4 x the number of thresholds strictly below y[j] found so far
@@ -143,24 +193,33 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void tq4_encode_kernel(
       }
       q |= (uint32_t)(off >> 2) << (4 * j);
     }
+    }
     // word w = elements 8w .. 8w + 7: lanes 2w (low half) and 2w + 1
     const uint32_t partner = __builtin_bit_cast(uint32_t, xor_lane<1>(__builtin_bit_cast(float, q)));
     const uint32_t word = q | (partner << 16);
 
-    // request of this row and its logical position
-    const int row = vec / Hkv;
-    const int kv = vec - row * Hkv;
-    int32_t lo = 0, hi = B;  // largest b with cu_tok[b] <= row
-    while (hi - lo > 1) {
-      const int32_t mid = (lo + hi) >> 1;
-      if (cu_tok[mid] <= row) lo = mid; else hi = mid;
+    // (row, kv) of this vector; the row's destination is looked up once per
+    // row (the vectors of a wave are consecutive: Hkv of them per row)
+    const int kv = kv_cur;
+    if (++kv_cur == Hkv) kv_cur = 0;
+    if (row_cur != row_done) {
+      row_done = row_cur;
+      int32_t lo = 0, hi = B;  // request: largest b with cu_tok[b] <= row
+      while (hi - lo > 1) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (cu_tok[mid] <= row_cur) lo = mid; else hi = mid;
+      }
+      const int64_t pos = (int64_t)start_pos[lo] + (row_cur - cu_tok[lo]);
+      page_row = -1;
+      if (pos >= 0 && pos < (int64_t)max_pages * P) {
+        const int lp = (int)pos / P;
+        page_row = block_tables[(int64_t)lo * max_pages + lp];
+        slot_in_page = (int)pos - lp * P;
+      }
     }
-    const int64_t pos = (int64_t)start_pos[lo] + (row - cu_tok[lo]);
-    if (pos < 0 || pos >= (int64_t)max_pages * P) continue;
-    const int lp = (int)pos / P;
-    const int32_t page = block_tables[(int64_t)lo * max_pages + lp];
-    if (page < 0 || page >= NP) continue;
-    const int64_t slot = ((int64_t)page * Hkv + kv) * P + ((int)pos - lp * P);
+    if (kv_cur == 0) ++row_cur;
+    if (page_row < 0 || page_row >= NP) continue;
+    const int64_t slot = ((int64_t)page_row * Hkv + kv) * P + slot_in_page;
     if ((lane & 1) == 0) words[slot * (kD / 8) + (lane >> 1)] = word;
     if (lane == 0) norms[slot] = __float2half_rn(rho);
   }
