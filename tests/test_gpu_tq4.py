@@ -49,14 +49,14 @@ def tables(rng, lens, starts, P, NP, holes=()):
     return t
 
 
-def encode_gpu(lay, x, signs, lens, starts, table):
+def encode_gpu(lay, x, signs, lens, starts, table, c=None):
     pool = jfkv.TQ4Pool(lay, fill=POISON)
     dev = torch.device("cuda:0")
     cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32, device=dev)
     st = torch.tensor(starts, dtype=torch.int32, device=dev)
     jfkv.jf_tq4_encode_append(pool, torch.from_numpy(x).to(dev),
                               torch.from_numpy(signs.astype(np.float32)).to(dev),
-                              torch.from_numpy(codebook()).to(dev), cu, st,
+                              torch.from_numpy(codebook() if c is None else c).to(dev), cu, st,
                               torch.from_numpy(table).to(dev))
     torch.cuda.synchronize()
     return (pool.words.cpu().numpy().view(np.uint32), pool.norms.cpu().numpy())
@@ -77,10 +77,11 @@ def slots_of(lens, starts, table, P, rows=None):
     return out
 
 
-def check_vectors(x_rows, w_gpu, n_gpu, signs):
+def check_vectors(x_rows, w_gpu, n_gpu, signs, c=None):
     """Compare the kernel's words and norms for vectors x_rows [m][D] with
-    the oracle; returns the number of band cases."""
-    c = codebook()
+    the oracle (codebook c, default the format's); returns the number of band
+    cases."""
+    c = codebook() if c is None else c
     idx, n16, y = tq4.encode(x_rows, signs, c)
     g_idx = tq4.unpack(w_gpu)
     diff = g_idx.astype(np.int32) - idx.astype(np.int32)
@@ -215,3 +216,34 @@ def test_full_bulk_sampled():
         band += check_vectors(xs[:, kv], w[used[rows // P], kv, rows % P],
                               nrm[used[rows // P], kv, rows % P], signs)
     log("  band cases %d" % band)
+
+
+@pytest.mark.parametrize("kind", ["clustered", "uniform"])
+def test_other_codebooks(kind):
+    """Codebooks other than the format's: one whose two middle thresholds lie
+    within one bucket of the kernel's index table (the kernel falls back to a
+    binary search), and uniform levels (the table path with other
+    thresholds).  Indices and norms match the oracle with the same
+    codebook."""
+    log("tq4 encode, %s codebook" % kind)
+    c = codebook().astype(np.float32).copy()
+    if kind == "clustered":
+        c[8] = np.float32(c[7] + 1e-4)
+        c[9] = np.float32(c[8] + 1e-4)
+    else:
+        c = np.linspace(-0.2, 0.2, 16).astype(np.float32)
+    rng = np.random.default_rng(11)
+    P, hkv, NP = 64, 3, 8
+    lens, starts = (200, 77), (0, 10)
+    t = tables(rng, lens, starts, P, NP)
+    x = rng.standard_normal((sum(lens), hkv, D)).astype(np.float16)
+    signs = tq4.signs(D, 0)
+    lay = jfkv.layout(P, hkv, D, 64, NP)
+    w, n = encode_gpu(lay, x, signs, lens, starts, t, c=c)
+    sl = slots_of(lens, starts, t, P)
+    rows = np.array([r for r, _, _ in sl])
+    pages = np.array([p for _, p, _ in sl])
+    slots = np.array([q for _, _, q in sl])
+    for kv in range(hkv):
+        check_vectors(x[rows, kv].astype(np.float64), w[pages, kv, slots], n[pages, kv, slots],
+                      signs, c=c)
