@@ -338,7 +338,7 @@ def bench_decode_steps(name, args):
     label = name if (name != "decode_256k" or window) else "decode_%d" % L0
     split_cap = min(args.max_splits,
                     max(1, torch.cuda.get_device_properties(0).multi_processor_count
-                        // (hkv * -(-(hq // hkv) // jfkv.decode_head_chunk(d, G)))))
+                        // (hkv * -(-(hq // hkv) // jfkv.decode_head_chunk(d, G, hq // hkv)))))
     result = {
         "metric": METRIC if window else "decode-attn KV positions/s/layer (%s)" % label,
         "value": logical / (wall_us * 1e-6), "unit": "KV positions/s/layer", "n_gpus": 1,
@@ -840,7 +840,7 @@ def bench_verify(args):
     nbytes = L * bpp + 2 * sq * hq * d * 2
     achieved = nbytes / (gpu_us * 1e-6) / 1e9
     gqv = hq // hkv * sq
-    n_hchunks = -(-gqv // jfkv.decode_head_chunk(d, G))
+    n_hchunks = -(-gqv // jfkv.decode_head_chunk(d, G, gqv))
     result = {
         "metric": "verify-attn KV positions/s/layer (3 causal query tokens, 32 q / 8 KV heads, "
                   "256K ctx)",

@@ -232,8 +232,9 @@ jf_status jf_decode_workspace_bytes(int32_t B, int32_t num_q_heads,
  *   max_splits   cap on partials per request and KV head (1..1024); a
  *                request with n pages uses S = min(max_splits, n,
  *                max(1, floor(compute units / (num_kv_heads *
- *                ceil(Gq / H))))), H the query heads one block serves: 4
- *                for 32-dim groups or head_dim 256, else 8
+ *                ceil(Gq / H))))), H the query heads one block serves:
+ *                h = 4 for 32-dim groups or head_dim 256, else 8, and
+ *                H = 2h when Gq > h and head_dim <= 128, else h
  *                page-aligned splits of equal page counts, the remainder on
  *                the first (S depends on neither the batch nor the other
  *                requests, so a request's output is the same in any batch)

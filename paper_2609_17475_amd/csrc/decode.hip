@@ -374,7 +374,7 @@ __device__ __forceinline__ size_t qrow(int b, int vh, int Hq, int sq) {
 // coherent loads and folded into a running maximum; the KP parts meet by
 // shuffles.  Records: [max_splits][D + 4] fp32 per head (o/l in 0..D-1, m at
 // D, l at D+1).
-template <int D, int WPH>
+template <int D, int WPH, int NW>
 __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int sq, int h0,
                                int nh, int max_splits, int S) {
   constexpr int DW = D / WPH;     // dims per wave
@@ -384,63 +384,65 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
   static_assert(KP >= 1 && 64 % CPL == 0, "");
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // scalar: the records' resource too
-  const int h = w / WPH, d0 = DW * (w % WPH);
-  if (h >= nh) return;
+  const int d0 = DW * (w % WPH);
   const int c = lane % CPL, k = lane / CPL;
-  const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (D + 4);
-  const __amdgpu_buffer_rsrc_t rs = records_rsrc(recs, (uint32_t)S * (D + 4) * 4);
-  float m_run = -INFINITY, den = 0.0f;
-  float num[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int s0 = k; s0 < S; s0 += KP * KCH) {
-    f32x4 o[KCH];
-    f32x2 ml[KCH];
+  // wave w combines heads w / WPH, w / WPH + NW / WPH, ...
+  for (int h = w / WPH; h < nh; h += NW / WPH) {
+    const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (D + 4);
+    const __amdgpu_buffer_rsrc_t rs = records_rsrc(recs, (uint32_t)S * (D + 4) * 4);
+    float m_run = -INFINITY, den = 0.0f;
+    float num[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int s0 = k; s0 < S; s0 += KP * KCH) {
+      f32x4 o[KCH];
+      f32x2 ml[KCH];
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int s = min(s0 + KP * i, S - 1);  // past the end: a valid record, weight 0
-      o[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (s * (D + 4) + d0 + 4 * c) * 4, 0, kCpolSc1);
-      ml[i] = __builtin_amdgcn_raw_buffer_load_b64(rs, (s * (D + 4) + D) * 4, 0, kCpolSc1);
+      for (int i = 0; i < KCH; ++i) {
+        const int s = min(s0 + KP * i, S - 1);  // past the end: a valid record, weight 0
+        o[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (s * (D + 4) + d0 + 4 * c) * 4, 0, kCpolSc1);
+        ml[i] = __builtin_amdgcn_raw_buffer_load_b64(rs, (s * (D + 4) + D) * 4, 0, kCpolSc1);
+      }
+      // (selects, not branches: the records' validity is per lane)
+      float mv[KCH];
+      float mx = m_run;
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) {
+        const bool on = (s0 + KP * i < S) & (ml[i].y > 0.0f);
+        mv[i] = on ? ml[i].x : -INFINITY;
+        mx = fmaxf(mx, mv[i]);
+      }
+      const float f = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - mx);
+      den *= f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) num[e] *= f;
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) {
+        const float wt = (mv[i] == -INFINITY) ? 0.0f : ml[i].y * __builtin_amdgcn_exp2f(mv[i] - mx);
+        den += wt;
+        num[0] = fmaf(wt, o[i].x, num[0]);
+        num[1] = fmaf(wt, o[i].y, num[1]);
+        num[2] = fmaf(wt, o[i].z, num[2]);
+        num[3] = fmaf(wt, o[i].w, num[3]);
+      }
+      m_run = mx;
     }
-    // (selects, not branches: the records' validity is per lane)
-    float mv[KCH];
-    float mx = m_run;
+    // merge the KP parts of each chunk (lanes c, c + CPL, ...)
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const bool on = (s0 + KP * i < S) & (ml[i].y > 0.0f);
-      mv[i] = on ? ml[i].x : -INFINITY;
-      mx = fmaxf(mx, mv[i]);
+    for (int off = CPL; off < 64; off <<= 1) {
+      const float mo = __shfl_xor(m_run, off);
+      const float M = fmaxf(m_run, mo);
+      const float fa = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - M);
+      const float fb = (mo == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mo - M);
+      den = den * fa + __shfl_xor(den, off) * fb;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) num[e] = num[e] * fa + __shfl_xor(num[e], off) * fb;
+      m_run = M;
     }
-    const float f = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - mx);
-    den *= f;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) num[e] *= f;
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const float wt = (mv[i] == -INFINITY) ? 0.0f : ml[i].y * __builtin_amdgcn_exp2f(mv[i] - mx);
-      den += wt;
-      num[0] = fmaf(wt, o[i].x, num[0]);
-      num[1] = fmaf(wt, o[i].y, num[1]);
-      num[2] = fmaf(wt, o[i].z, num[2]);
-      num[3] = fmaf(wt, o[i].w, num[3]);
+    if (k == 0) {
+      const float r = den > 0.0f ? 1.0f / den : 0.0f;
+      __half2* dst = reinterpret_cast<__half2*>(out + qrow(b, h0 + h, Hq, sq) * D + d0 + 4 * c);
+      dst[0] = __floats2half2_rn(num[0] * r, num[1] * r);
+      dst[1] = __floats2half2_rn(num[2] * r, num[3] * r);
     }
-    m_run = mx;
-  }
-  // merge the KP parts of each chunk (lanes c, c + CPL, ...)
-#pragma unroll
-  for (int off = CPL; off < 64; off <<= 1) {
-    const float mo = __shfl_xor(m_run, off);
-    const float M = fmaxf(m_run, mo);
-    const float fa = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m_run - M);
-    const float fb = (mo == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(mo - M);
-    den = den * fa + __shfl_xor(den, off) * fb;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) num[e] = num[e] * fa + __shfl_xor(num[e], off) * fb;
-    m_run = M;
-  }
-  if (k == 0) {
-    const float r = den > 0.0f ? 1.0f / den : 0.0f;
-    __half2* dst = reinterpret_cast<__half2*>(out + qrow(b, h0 + h, Hq, sq) * D + d0 + 4 * c);
-    dst[0] = __floats2half2_rn(num[0] * r, num[1] * r);
-    dst[1] = __floats2half2_rn(num[2] * r, num[3] * r);
   }
 }
 
@@ -467,7 +469,7 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
 // without waiting, and writes the same bytes into its LDS stage once that
 // row's loads have landed (they may still see the slot's previous bytes);
 // no other block reads that page.
-template <int D, int G, bool APPEND>
+template <int D, int G, bool APPEND, int CS>
 __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     uint8_t* __restrict__ k_codes, uint32_t* __restrict__ k_meta,
     uint8_t* __restrict__ v_codes, uint32_t* __restrict__ v_meta,
@@ -494,12 +496,14 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   constexpr int kFit = (kRingBudget - 16) / (kWaves * kStageBytes);
   constexpr int kStages = kFit < kMaxStages ? kFit : kMaxStages;
   static_assert(kStages >= 2, "ring depth");
-  constexpr int kHeadSlots = head_slots<D, G>();
+  constexpr int kHeadSlots = head_slots<D, G>();  // heads per column set
   constexpr int NS = 16 / kHeadSlots;      // column slots per head
-  static_assert(kWaves % kHeadSlots == 0, "whole waves per head in the combine");
+  constexpr int kChunk = kHeadSlots * CS;  // heads per block: CS column sets
+  static_assert(kChunk <= kWaves ? kWaves % kChunk == 0 : kChunk % kWaves == 0,
+                "whole waves per head, or whole heads per wave, in the combine");
   constexpr bool kSwz = (D == 128);
   static_assert(DMAS_PER_ROW * (kStages - 1) < 64, "vmcnt range");
-  static_assert(kHeadSlots * D + 2 * kHeadSlots <= kStages * kStageBytes / 4, "merge fits a ring");
+  static_assert(kChunk * D + 2 * kChunk <= kStages * kStageBytes / 4, "merge fits a ring");
 
   __shared__ __attribute__((aligned(16))) uint8_t smem[kWaves][kStages][kStageBytes];
   __shared__ uint32_t s_ticket;
@@ -526,15 +530,22 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   }
   const int b = blockIdx.z;
   const int gq = Hq / Hkv;
-  const int h0 = kv * gq + hc * kHeadSlots;
-  const int nh = min(kHeadSlots, gq - hc * kHeadSlots);
+  const int h0 = kv * gq + hc * kChunk;
+  const int nh = min(kChunk, gq - hc * kChunk);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
 
   const int l16 = lane & 15, q4 = lane >> 4;
   const int hs = l16 % kHeadSlots, gs = l16 / kHeadSlots;  // accumulator column: head, slot
-  const bool head_on = hs < nh;
+  // column set cs holds heads cs kHeadSlots + hs of the chunk
+  bool head_on[CS];
+  int hsel[CS];  // the head whose query this lane's column reads (a valid one)
+#pragma unroll
+  for (int cs = 0; cs < CS; ++cs) {
+    head_on[cs] = cs * kHeadSlots + hs < nh;
+    hsel[cs] = min(cs * kHeadSlots + hs, nh - 1);
+  }
 
   // Loads issued together, before anything waits for the request's length:
   // the query words of head hs over the dims of quarter q4 (the lane's
@@ -542,14 +553,15 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   // fills its table (the common case; read again below otherwise), and, in
   // the fused step, the new row's fp16 values (lanes 0 .. D/8 - 1: K dims
   // 8 lane ..; lanes D/8 .. D/4 - 1: V) in the block that would hold it.
-  uint4 qraw[NHALF][WQ];
-  {
+  uint4 qraw[CS][NHALF][WQ];
+#pragma unroll
+  for (int cs = 0; cs < CS; ++cs) {
     const uint4* src = reinterpret_cast<const uint4*>(
-        q + qrow(b, h0 + min(hs, nh - 1), Hq, sq) * D + DQ * q4);
+        q + qrow(b, h0 + hsel[cs], Hq, sq) * D + DQ * q4);
 #pragma unroll
     for (int e = 0; e < NHALF; ++e)
 #pragma unroll
-      for (int kb = 0; kb < WQ; ++kb) qraw[e][kb] = src[(HD / 8) * e + kb];
+      for (int kb = 0; kb < WQ; ++kb) qraw[cs][e][kb] = src[(HD / 8) * e + kb];
   }
   const int S_full = min(split_cap, max_pages);
   int pb_full, pe_full;
@@ -582,7 +594,9 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   // causal limits of the verifier: token k of sq sees positions < L - sq + 1
   // + k (its own and those before it); rows below t_full need no mask
   const int t_full = min(t_end, L - sq + 1);
-  const int t_lim = min(t_end, L - sq + 1 + (h0 + min(hs, nh - 1)) % sq);
+  int t_lim[CS];
+#pragma unroll
+  for (int cs = 0; cs < CS; ++cs) t_lim[cs] = min(t_end, L - sq + 1 + (h0 + hsel[cs]) % sq);
   const int rows_per_page = P / kRowPos;
 
   // this wave's rows: the split's rows in page order, wave, wave + kWaves, ...
@@ -749,17 +763,19 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   constexpr int NGH = HD / G;            // scale groups per half
   static_assert(NS % NGH == 0, "every group of a half has a column slot");
   const int gcol = gs % NGH;             // group (within a half) of the column
-  const bool q_on = head_on && (DQ * q4) / G == gcol;
   // a negative softmax scale negates the query (exact) and leaves |scale|
   const uint32_t qneg = scale_log2 < 0.0f ? 0x80008000u : 0u;
-  h8 qB[NHALF][WQ];
-  float qs[NHALF];
+  h8 qB[CS][NHALF][WQ];
+  float qs[CS][NHALF];
+#pragma unroll
+  for (int cs = 0; cs < CS; ++cs)
 #pragma unroll
   for (int e = 0; e < NHALF; ++e) {
+    const bool q_on = head_on[cs] && (DQ * q4) / G == gcol;
     float s = 0.0f;
 #pragma unroll
     for (int kb = 0; kb < WQ; ++kb) {
-      const uint4 u = qraw[e][kb];
+      const uint4 u = qraw[cs][e][kb];
       const uint32_t wq[4] = {u.x ^ qneg, u.y ^ qneg, u.z ^ qneg, u.w ^ qneg};
       _Float16 x[8];
 #pragma unroll
@@ -773,7 +789,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
       h8 o = {x[0], x[4], x[1] * sixteenth, x[5] * sixteenth,
               x[2], x[6], x[3] * sixteenth, x[7] * sixteenth};
       if (!q_on) o = h8{};
-      qB[e][kb] = o;
+      qB[cs][e][kb] = o;
     }
     // the group's query sum: quarter sums of the four lanes l16 + 16 k
     const float sq[4] = {s, __shfl_xor(s, 16), __shfl_xor(s, 32), __shfl_xor(s, 48)};
@@ -781,21 +797,26 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
 #pragma unroll
     for (int k = 0; k < 4; ++k)
       if ((DQ * (q4 ^ k)) / G == gcol) g += sq[k];
-    qs[e] = head_on ? g * (1.0f / 16777216.0f) : 0.0f;
+    qs[cs][e] = head_on[cs] ? g * (1.0f / 16777216.0f) : 0.0f;
   }
   // 2^24 (the code scale) times |scale| in log2 units; a positive floor keeps
   // masked (-inf) scores at -inf when the scale is 0
   const float kfold = 16777216.0f * fmaxf(fabsf(scale_log2), 1e-30f);
 
-  f32x4 acc_o[NC][4];
+  f32x4 acc_o[CS][NC][4];
+  float m_run[CS], thr[CS], l_run[CS];
+  float bacc[CS][NHALF], sacc8[CS][NHALF];  // sums of p * bias and of p * scale - W (value groups)
 #pragma unroll
-  for (int c = 0; c < NC; ++c)
+  for (int cs = 0; cs < CS; ++cs) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) acc_o[c][k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  float m_run = kMinit, thr = kMinit, l_run = 0.0f;
-  float bacc[NHALF], sacc8[NHALF];  // sums of p * bias and of p * scale - W (value groups)
+    for (int c = 0; c < NC; ++c)
 #pragma unroll
-  for (int e = 0; e < NHALF; ++e) bacc[e] = sacc8[e] = 0.0f;
+      for (int k = 0; k < 4; ++k) acc_o[cs][c][k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    m_run[cs] = thr[cs] = kMinit;
+    l_run[cs] = 0.0f;
+#pragma unroll
+    for (int e = 0; e < NHALF; ++e) bacc[cs][e] = sacc8[cs][e] = 0.0f;
+  }
 
   // LDS read bases (stage 0)
   const int p0 = 8 * (l16 >> 2) + (l16 & 3);  // tile-0 position of row m = l16
@@ -906,34 +927,43 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     // the stage is in registers: refill it with the row kStages ahead
     issue(std::integral_constant<int, ST>{}, issued_rows++ < my_rows);
 
-    // ---- scores: S^T tiles, one accumulator per half
-    f32x4 sacc[NHALF][2];
+    // ---- scores: S^T tiles, one accumulator per half and column set (the
+    // K operands are shared by the sets)
+    f32x4 sacc[CS][NHALF][2];
 #pragma unroll
-    for (int e = 0; e < NHALF; ++e)
+    for (int cs = 0; cs < CS; ++cs)
 #pragma unroll
-      for (int t = 0; t < 2; ++t) sacc[e][t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      for (int e = 0; e < NHALF; ++e)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) sacc[cs][e][t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kb = 0; kb < WQ; ++kb)
 #pragma unroll
       for (int e = 0; e < NHALF; ++e)
 #pragma unroll
-        for (int t = 0; t < 2; ++t) sacc[e][t] = mfma(k_operand(kw[e][t][kb]), qB[e][kb], sacc[e][t]);
+        for (int t = 0; t < 2; ++t) {
+          const h8 ko = k_operand(kw[e][t][kb]);
+#pragma unroll
+          for (int cs = 0; cs < CS; ++cs) sacc[cs][e][t] = mfma(ko, qB[cs][e][kb], sacc[cs][e][t]);
+        }
 
     // ---- logits: fold each column's group scale and bias, sum the distinct
     // groups of the head (lanes l16 + kHeadSlots k of the 16-lane row: slots
     // gs and gs + NGH are copies, so log2(NGH) rotations suffice), scale
-    float sc[2][4];
+    float sc[CS][2][4];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int cs = 0; cs < CS; ++cs)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float a = 0.0f;
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int e = 0; e < NHALF; ++e) a = fold_meta(kmw[e][t][i], sacc[e][t][i], qs[e], a);
-        if constexpr (NGH >= 2) a = row_ror_add<kHeadSlots>(a);
-        if constexpr (NGH >= 4) a = row_ror_add<2 * kHeadSlots>(a);
-        sc[t][i] = a;  // (scaled by kfold in the exponent)
-      }
+        for (int i = 0; i < 4; ++i) {
+          float a = 0.0f;
+#pragma unroll
+          for (int e = 0; e < NHALF; ++e) a = fold_meta(kmw[e][t][i], sacc[cs][e][t][i], qs[cs][e], a);
+          if constexpr (NGH >= 2) a = row_ror_add<kHeadSlots>(a);
+          if constexpr (NGH >= 4) a = row_ror_add<2 * kHeadSlots>(a);
+          sc[cs][t][i] = a;  // (scaled by kfold in the exponent)
+        }
     if (!full) {
       // (an empty volatile statement keeps this a branch: the compiler would
       // otherwise compute the masks as selects on every row)
@@ -942,67 +972,82 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const bool ok = pg_ok && t_row + 8 * q4 + 4 * t + i < t_lim;
-          sc[t][i] = ok ? sc[t][i] : -INFINITY;
+          const int tp = t_row + 8 * q4 + 4 * t + i;
+          // positions past the split's end or in no page: no score, and no
+          // (scale, bias) words (they may hold anything)
+          const bool ok = pg_ok && tp < t_end;
+#pragma unroll
+          for (int cs = 0; cs < CS; ++cs) sc[cs][t][i] = ok && tp < t_lim[cs] ? sc[cs][t][i] : -INFINITY;
 #pragma unroll
           for (int e = 0; e < NHALF; ++e) vmw[e][t][i] = ok ? vmw[e][t][i] : 0u;
         }
     }
-    const float mx = kfold * max8(sc[0][0], sc[0][1], sc[0][2], sc[0][3], sc[1][0], sc[1][1],
-                                  sc[1][2], sc[1][3]);
-    if (__builtin_amdgcn_ballot_w64(mx > thr) != 0) {
-      // new running maximum of the head: lanes with equal lane % kHeadSlots
-      const float M = xor_max_from(mx, kHeadSlots);
-      if (M > m_run) {
-        const float alpha = __builtin_amdgcn_exp2f(m_run - M);
-        m_run = M;
-        thr = M + kTau;
-        l_run *= alpha;
+    h8 W[CS][NHALF];
 #pragma unroll
-        for (int e = 0; e < NHALF; ++e) {
-          bacc[e] *= alpha;
-          sacc8[e] *= alpha;
+    for (int cs = 0; cs < CS; ++cs) {
+      const float mx = kfold * max8(sc[cs][0][0], sc[cs][0][1], sc[cs][0][2], sc[cs][0][3],
+                                    sc[cs][1][0], sc[cs][1][1], sc[cs][1][2], sc[cs][1][3]);
+      if (__builtin_amdgcn_ballot_w64(mx > thr[cs]) != 0) {
+        // new running maximum of the head: lanes with equal lane % kHeadSlots
+        const float M = xor_max_from(mx, kHeadSlots);
+        if (M > m_run[cs]) {
+          const float alpha = __builtin_amdgcn_exp2f(m_run[cs] - M);
+          m_run[cs] = M;
+          thr[cs] = M + kTau;
+          l_run[cs] *= alpha;
+#pragma unroll
+          for (int e = 0; e < NHALF; ++e) {
+            bacc[cs][e] *= alpha;
+            sacc8[cs][e] *= alpha;
+          }
+#pragma unroll
+          for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) acc_o[cs][c][k] *= alpha;
         }
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-          for (int k = 0; k < 4; ++k) acc_o[c][k] *= alpha;
       }
-    }
-    // ---- p (fp16 pairs of positions 8 q4 + 2r, + 1), row sum, W = p * scale
-    h2 pk[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = r >> 1, i = 2 * (r & 1);
-      pk[r] = h2{(_Float16)__builtin_amdgcn_exp2f(fmaf(sc[t][i], kfold, -m_run)),
-                 (_Float16)__builtin_amdgcn_exp2f(fmaf(sc[t][i + 1], kfold, -m_run))};
-      l_run = __builtin_amdgcn_fdot2(pk[r], ones, l_run, false);
-    }
-    h8 W[NHALF];
-#pragma unroll
-    for (int e = 0; e < NHALF; ++e) {
+      // ---- p (fp16 pairs of positions 8 q4 + 2r, + 1), row sum, W = p * scale
+      h2 pk[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = r >> 1, i = 2 * (r & 1);
-        const uint32_t a = vmw[e][t][i], c = vmw[e][t][i + 1];
-        const h2 sv = as_h2(__builtin_amdgcn_perm(c, a, 0x05040100u));
-        const h2 bv = as_h2(__builtin_amdgcn_perm(c, a, 0x07060302u));
-        const h2 w = pk[r] * sv;
-        W[e][2 * r] = w.x;
-        W[e][2 * r + 1] = w.y;
-        bacc[e] = __builtin_amdgcn_fdot2(pk[r], bv, bacc[e], false);
-        sacc8[e] = __builtin_amdgcn_fdot2(pk[r], sv, sacc8[e], false);
-        sacc8[e] = __builtin_amdgcn_fdot2(w, mones, sacc8[e], false);
+        pk[r] = h2{(_Float16)__builtin_amdgcn_exp2f(fmaf(sc[cs][t][i], kfold, -m_run[cs])),
+                   (_Float16)__builtin_amdgcn_exp2f(fmaf(sc[cs][t][i + 1], kfold, -m_run[cs]))};
+        l_run[cs] = __builtin_amdgcn_fdot2(pk[r], ones, l_run[cs], false);
+      }
+#pragma unroll
+      for (int e = 0; e < NHALF; ++e) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = r >> 1, i = 2 * (r & 1);
+          const uint32_t a = vmw[e][t][i], c = vmw[e][t][i + 1];
+          const h2 sv = as_h2(__builtin_amdgcn_perm(c, a, 0x05040100u));
+          const h2 bv = as_h2(__builtin_amdgcn_perm(c, a, 0x07060302u));
+          const h2 w = pk[r] * sv;
+          W[cs][e][2 * r] = w.x;
+          W[cs][e][2 * r + 1] = w.y;
+          bacc[cs][e] = __builtin_amdgcn_fdot2(pk[r], bv, bacc[cs][e], false);
+          sacc8[cs][e] = __builtin_amdgcn_fdot2(pk[r], sv, sacc8[cs][e], false);
+          sacc8[cs][e] = __builtin_amdgcn_fdot2(w, mones, sacc8[cs][e], false);
+        }
       }
     }
-    // ---- values: O^T += V codes x W, dims 4 (16 c + m) + k
+    // ---- values: O^T += V codes x W, dims 4 (16 c + m) + k (the V
+    // operands are shared by the sets)
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      const h8 w = W[c >> 1 < NHALF ? c >> 1 : 0];
-      acc_o[c][0] = mfma(v_operand<0>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask), w, acc_o[c][0]);
-      acc_o[c][1] = mfma(v_operand<1>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask), w, acc_o[c][1]);
-      acc_o[c][2] = mfma(v_operand<2>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask), w, acc_o[c][2]);
-      acc_o[c][3] = mfma(v_operand<3>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask), w, acc_o[c][3]);
+      const int e = c >> 1 < NHALF ? c >> 1 : 0;
+      const h8 v0 = v_operand<0>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask);
+      const h8 v1 = v_operand<1>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask);
+      const h8 v2 = v_operand<2>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask);
+      const h8 v3 = v_operand<3>(vw[c][0], vw[c][1], vw[c][2], vw[c][3], vmask);
+#pragma unroll
+      for (int cs = 0; cs < CS; ++cs) {
+        acc_o[cs][c][0] = mfma(v0, W[cs][e], acc_o[cs][c][0]);
+        acc_o[cs][c][1] = mfma(v1, W[cs][e], acc_o[cs][c][1]);
+        acc_o[cs][c][2] = mfma(v2, W[cs][e], acc_o[cs][c][2]);
+        acc_o[cs][c][3] = mfma(v3, W[cs][e], acc_o[cs][c][3]);
+      }
     }
     t_row += kWaves * kRowPos;
   };
@@ -1020,50 +1065,54 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   // the code factor plus the bias sums), its maximum and its row sum into its
   // own ring, which is idle now; after one barrier the split's threads add
   // the waves' parts, rescaled to the split's maximum.
-  float* part = reinterpret_cast<float*>(ring);  // [kHeadSlots][D]
-  float* part_m = part + kHeadSlots * D;          // [kHeadSlots]
-  float* part_l = part_m + kHeadSlots;            // [kHeadSlots]
+  float* part = reinterpret_cast<float*>(ring);  // [kChunk][D]
+  float* part_m = part + kChunk * D;              // [kChunk]
+  float* part_l = part_m + kChunk;                // [kChunk]
   {
     const int lane_e = lane_id_volatile();
     const int me = lane_e & 15, qe = lane_e >> 4;
     const int hse = me % kHeadSlots, gse = me / kHeadSlots;
-    float bsum[NHALF];
 #pragma unroll
-    for (int e = 0; e < NHALF; ++e) {
-      // the value groups' sums of p * (bias + 8 scale) - 8 W: the bias part
-      // of the value and the centring of the codes (sacc8 holds
-      // sum (p * scale - W))
-      float bq = bacc[e] + __shfl_xor(bacc[e], 16);
-      bq += __shfl_xor(bq, 32);
-      float sq8 = sacc8[e] + __shfl_xor(sacc8[e], 16);
-      sq8 += __shfl_xor(sq8, 32);
-      bsum[e] = fmaf(8.0f, sq8, bq);
-    }
-    float lsum = l_run + __shfl_xor(l_run, 16);
-    lsum += __shfl_xor(lsum, 32);
+    for (int cs = 0; cs < CS; ++cs) {
+      float bsum[NHALF];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      // lane (col, qe) holds dims 4 (16 c + 4 qe + i) + k, of group
-      // (64 (c % 2) + 16 qe) / G of their half; its column's slot stands for
-      // that group when gse % NGH equals it, and of the NS / NGH copies of a
-      // group copy r writes rows qe with qe (NS / NGH) / 4 == r
-      constexpr int R = NS / NGH;
-      if (gse % NGH == (64 * (c & 1) + 16 * qe) / G && gse / NGH == (qe * R) / 4) {
-        const float bg = bsum[(c >> 1) < NHALF ? (c >> 1) : 0];
+      for (int e = 0; e < NHALF; ++e) {
+        // the value groups' sums of p * (bias + 8 scale) - 8 W: the bias part
+        // of the value and the centring of the codes (sacc8 holds
+        // sum (p * scale - W))
+        float bq = bacc[cs][e] + __shfl_xor(bacc[cs][e], 16);
+        bq += __shfl_xor(bq, 32);
+        float sq8 = sacc8[cs][e] + __shfl_xor(sacc8[cs][e], 16);
+        sq8 += __shfl_xor(sq8, 32);
+        bsum[e] = fmaf(8.0f, sq8, bq);
+      }
+      float lsum = l_run[cs] + __shfl_xor(l_run[cs], 16);
+      lsum += __shfl_xor(lsum, 32);
+      const int hp = cs * kHeadSlots + hse;  // the column's head in the chunk
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          // (code sums times 2^20, the operands' code scale)
-          const float4 o4 = make_float4(fmaf(acc_o[c][0][i], 1048576.0f, bg),
-                                        fmaf(acc_o[c][1][i], 1048576.0f, bg),
-                                        fmaf(acc_o[c][2][i], 1048576.0f, bg),
-                                        fmaf(acc_o[c][3][i], 1048576.0f, bg));
-          *reinterpret_cast<float4*>(part + hse * D + 4 * (16 * c + 4 * qe + i)) = o4;
+      for (int c = 0; c < NC; ++c) {
+        // lane (col, qe) holds dims 4 (16 c + 4 qe + i) + k, of group
+        // (64 (c % 2) + 16 qe) / G of their half; its column's slot stands for
+        // that group when gse % NGH equals it, and of the NS / NGH copies of a
+        // group copy r writes rows qe with qe (NS / NGH) / 4 == r
+        constexpr int R = NS / NGH;
+        if (gse % NGH == (64 * (c & 1) + 16 * qe) / G && gse / NGH == (qe * R) / 4) {
+          const float bg = bsum[(c >> 1) < NHALF ? (c >> 1) : 0];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            // (code sums times 2^20, the operands' code scale)
+            const float4 o4 = make_float4(fmaf(acc_o[cs][c][0][i], 1048576.0f, bg),
+                                          fmaf(acc_o[cs][c][1][i], 1048576.0f, bg),
+                                          fmaf(acc_o[cs][c][2][i], 1048576.0f, bg),
+                                          fmaf(acc_o[cs][c][3][i], 1048576.0f, bg));
+            *reinterpret_cast<float4*>(part + hp * D + 4 * (16 * c + 4 * qe + i)) = o4;
+          }
         }
       }
-    }
-    if (lane_e < kHeadSlots) {
-      part_m[lane_e] = m_run;
-      part_l[lane_e] = lsum;
+      if (lane_e < kHeadSlots) {
+        part_m[cs * kHeadSlots + lane_e] = m_run[cs];
+        part_l[cs * kHeadSlots + lane_e] = lsum;
+      }
     }
   }
   __syncthreads();
@@ -1078,7 +1127,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
       float M = kMinit;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        mw[w] = base[w * kWaveFloats + kHeadSlots * D + h];
+        mw[w] = base[w * kWaveFloats + kChunk * D + h];
         M = fmaxf(M, mw[w]);
       }
       float num = 0.0f, den = 0.0f;
@@ -1087,7 +1136,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
         const float* pw = base + w * kWaveFloats;
         const float f = __builtin_amdgcn_exp2f(mw[w] - M);
         num = fmaf(f, pw[h * D + dd], num);
-        den = fmaf(f, pw[kHeadSlots * D + kHeadSlots + h], den);
+        den = fmaf(f, pw[kChunk * D + kChunk + h], den);
       }
       // agent-scope stores write through to the device-coherent level, so the
       // block that combines (on any XCD) reads them without a cache flush
@@ -1118,18 +1167,19 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
   if (s_ticket != (uint32_t)(S - 1)) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  combine_splits<D, kWaves / kHeadSlots>(ws, out, b, Hq, sq, h0, nh, max_splits, S);
+  combine_splits<D, (kChunk < kWaves ? kWaves / kChunk : 1), kWaves>(ws, out, b, Hq, sq, h0, nh,
+                                                                        max_splits, S);
 }
 
-template <int D, int G, bool APPEND>
-hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
-                    const void* v_new, const void* q,
-                    int32_t B, int32_t Hq, const int32_t* bt, int32_t max_pages,
-                    const int32_t* lens, float scale, int32_t max_splits, uint32_t* tickets,
-                    float* records, void* out, int32_t sq, hipStream_t stream) {
+template <int D, int G, bool APPEND, int CS>
+hipError_t launch_cs(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
+                     const void* v_new, const void* q,
+                     int32_t B, int32_t Hq, const int32_t* bt, int32_t max_pages,
+                     const int32_t* lens, float scale, int32_t max_splits, uint32_t* tickets,
+                     float* records, void* out, int32_t sq, hipStream_t stream) {
   const int gq = Hq / L.num_kv_heads;
-  constexpr int kHeadSlots = head_slots<D, G>();
-  const int n_hchunks = (gq + kHeadSlots - 1) / kHeadSlots;
+  constexpr int kChunk = head_slots<D, G>() * CS;
+  const int n_hchunks = (gq + kChunk - 1) / kChunk;
   // Splits per request: enough blocks for one per CU when one request runs
   // alone, at most max_splits.  The count does not depend on the batch (a
   // request's output is bitwise the same in any batch) nor on the lengths
@@ -1143,7 +1193,7 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
   dim3 grid = n_hchunks == 1
                   ? dim3(split_cap, L.num_kv_heads, B)
                   : dim3((uint32_t)(((slots + kXcds - 1) / kXcds) * kXcds * n_hchunks), 1, B);
-  hipLaunchKernelGGL((decode_kernel<D, G, APPEND>), grid, dim3(64 * waves_for<D>()), 0, stream,
+  hipLaunchKernelGGL((decode_kernel<D, G, APPEND, CS>), grid, dim3(64 * waves_for<D>()), 0, stream,
                      static_cast<uint8_t*>(pool.k_codes), static_cast<uint32_t*>(pool.k_meta),
                      static_cast<uint8_t*>(pool.v_codes), static_cast<uint32_t*>(pool.v_meta),
                      static_cast<const uint4*>(k_new), static_cast<const uint4*>(v_new),
@@ -1153,6 +1203,25 @@ hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const vo
                      n_hchunks,
                      scale * kLog2e);
   return hipGetLastError();
+}
+
+// Two column sets per block where one would leave query heads of the KV head
+// for a second chunk (more heads than head_slots, as in the short verifier,
+// whose heads are query heads times tokens); head_dim 256 keeps one set (its
+// accumulators fill the registers).
+template <int D, int G, bool APPEND>
+hipError_t launch_t(const jf_kv_layout& L, const jf_kv_pool_ptrs& pool, const void* k_new,
+                    const void* v_new, const void* q,
+                    int32_t B, int32_t Hq, const int32_t* bt, int32_t max_pages,
+                    const int32_t* lens, float scale, int32_t max_splits, uint32_t* tickets,
+                    float* records, void* out, int32_t sq, hipStream_t stream) {
+  if constexpr (D <= 128) {
+    if (Hq / L.num_kv_heads > head_slots<D, G>())
+      return launch_cs<D, G, APPEND, 2>(L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens,
+                                         scale, max_splits, tickets, records, out, sq, stream);
+  }
+  return launch_cs<D, G, APPEND, 1>(L, pool, k_new, v_new, q, B, Hq, bt, max_pages, lens, scale,
+                                    max_splits, tickets, records, out, sq, stream);
 }
 
 }  // namespace

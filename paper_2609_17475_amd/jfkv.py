@@ -272,11 +272,14 @@ def jf_kv_quantize_append(pool: KVPool, k_new, v_new, cu_tok, start_pos, block_t
                                      _stream(stream)))
 
 
-def decode_head_chunk(head_dim: int, group_size: int) -> int:
+def decode_head_chunk(head_dim: int, group_size: int, gq: int) -> int:
     """Query heads one decode block serves (a head chunk; the split cap of
     jf_decode_attn_q4 divides the compute units by num_kv_heads * ceil(Gq /
-    this)): 4 for 32-dim groups or head_dim 256, else 8."""
-    return 4 if group_size == 32 or head_dim == 256 else 8
+    this)).  A column set holds 4 heads for 32-dim groups or head_dim 256,
+    else 8; blocks take two sets when Gq (query heads per KV head, times
+    tokens for the verifier) exceeds one set and head_dim <= 128."""
+    hs = 4 if group_size == 32 or head_dim == 256 else 8
+    return 2 * hs if head_dim <= 128 and gq > hs else hs
 
 
 def jf_decode_workspace_bytes(B: int, num_q_heads: int, head_dim: int, max_splits: int) -> int:

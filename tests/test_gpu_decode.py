@@ -36,10 +36,13 @@ def _q(seed, B, hq, d, scale=None):
     (256, 4, 24, 256, 64, (600,)),   # the paper's 24 q / 4 KV heads, d = 256
     (128, 2, 2, 128, 64, (300,)),    # one query head per KV head
     (64, 2, 6, 128, 32, (500,)),     # three per KV head
-    (64, 1, 8, 128, 64, (333,)),     # eight per KV head (one head chunk of eight)
-    (64, 1, 16, 128, 64, (333,)),    # sixteen per KV head (two chunks of eight)
-    (64, 2, 20, 128, 128, (400,)),   # ten per KV head, one group per half (chunks 8 + 2)
-    (64, 1, 12, 64, 64, (500,)),     # d = 64, twelve per KV head (chunks 8 + 4)
+    (64, 1, 8, 128, 64, (333,)),     # eight per KV head (one column set of eight)
+    (64, 1, 16, 128, 64, (333,)),    # sixteen per KV head (one chunk of two sets of eight)
+    (64, 2, 20, 128, 128, (400,)),   # ten per KV head, one group per half (second set: 2)
+    (64, 1, 12, 64, 64, (500,)),     # d = 64, twelve per KV head (sets of 8 + 4)
+    (64, 1, 20, 128, 64, (450,)),    # twenty per KV head (chunks of 16 + 4)
+    (64, 1, 12, 128, 32, (350,)),    # 32-dim groups, twelve (chunks of 2 x 4 + 4)
+    (64, 1, 40, 256, 64, (300,)),    # d = 256: one set per chunk (chunks of 4)
 ])
 def test_decode_matches_oracle(P, hkv, hq, d, G, lens):
     log("decode P=%d hkv=%d hq=%d d=%d G=%d lens=%s" % (P, hkv, hq, d, G, lens))
