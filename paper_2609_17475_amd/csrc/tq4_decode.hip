@@ -392,9 +392,10 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
 
   // ---- the last split of (request, KV head) to finish combines them all
   // (log-sum-exp over the splits, in the rotated space), then rotates back.
-  // Ordering as in the affine decode: record stores, then the ticket
-  // increment (acq_rel, device scope); the last block takes a device-scope
-  // acquire fence before it reads the records.
+  // Ordering: record stores, then the ticket increment (acq_rel, device
+  // scope); the last block takes a device-scope acquire fence before it
+  // reads the records (with ordinary loads, so the release and acquire are
+  // needed here).
   __syncthreads();
   uint32_t* ticket = tickets + (size_t)b * Hkv + kv;
   if (tid == 0)
