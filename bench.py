@@ -113,6 +113,38 @@ def copy_calibration(n_bytes: int, reps: int):
           flush=True)
 
 
+def read_calibration(n_bytes: int, args):
+    """The practical read ceiling: jf_calib_read_stream (the kernels' 16-byte
+    non-temporal loads, nothing else) over n_bytes, 8 rotated buffers, timed
+    with HIP events over 20 and over 200 back-to-back calls per grid size."""
+    import torch
+    from paper_2609_17475_amd import jfkv
+    dev = torch.device("cuda:0")
+    n_bytes -= n_bytes % 16
+    bufs = [torch.ones(n_bytes, dtype=torch.uint8, device=dev) for _ in range(8)]
+    sink = torch.zeros(4, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    rows = []
+    for blocks in (256, 1024, 2048):
+        for i in range(8):
+            jfkv.jf_calib_read_stream(bufs[i], blocks, sink, stream)
+        torch.cuda.synchronize()
+        for reps in (20, 200):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for i in range(reps):
+                jfkv.jf_calib_read_stream(bufs[i % 8], blocks, sink, stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            rows.append({"blocks": blocks, "reps": reps, "us_per_call": round(us, 2),
+                         "GBs": round(n_bytes / (us * 1e-6) / 1e9, 1),
+                         "frac_of_8TBs": round(n_bytes / (us * 1e-6) / 8e12, 4)})
+    print(json.dumps({"read_calibration": {"bytes": n_bytes, "buffers": 8, "threads_per_block": 512,
+                                           "load": "16-byte non-temporal, 8 in flight per lane",
+                                           "results": rows}}), flush=True)
+
+
 def _timed(calls, warmup, steps, stream):
     """Mean HIP-event duration (us) of each step's calls, and wall us/step."""
     import numpy as np
@@ -1182,6 +1214,8 @@ def main():
                          "decode_<positions> line without the counter traffic")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes (counter calibration)")
+    ap.add_argument("--read-calibration", type=int, default=0, metavar="BYTES",
+                    help="only time one read pass over BYTES bytes (the practical read ceiling)")
     ap.add_argument("--workload", default="decode_256k", choices=WORKLOADS)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -1195,6 +1229,9 @@ def main():
         return
     import torch
     torch.cuda.set_device(torch.device("cuda:0"))
+    if args.read_calibration:
+        read_calibration(args.read_calibration, args)
+        return
     if args.workload in DECODE_STEP_WORKLOADS:
         bench_decode_steps(args.workload, args)
     elif args.workload == "decode_32k_loop":

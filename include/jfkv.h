@@ -395,6 +395,18 @@ jf_status jf_kv_unpack_pages(const jf_kv_layout* layout, const jf_kv_pool_ptrs* 
                              const int32_t* block_table, int32_t first, int32_t count,
                              const void* buf, hipStream_t stream);
 
+/* Read-rate calibration (not part of the method): reads bytes (a positive
+ * multiple of 16) of device memory at buf once, with the 16-byte
+ * non-temporal loads of the HBM-bound kernels, `blocks` blocks of 512
+ * threads each reading one contiguous share, and does nothing else.  The
+ * time it takes on a buffer of the decode's size is the practical read
+ * ceiling the kernels' fractions of peak are compared with.  sink: 4 bytes
+ * of device memory (written only for a buffer whose words xor to a fixed
+ * 96-bit pattern).  buf 16-byte aligned; blocks 1..65535.  One kernel on
+ * stream. */
+jf_status jf_calib_read_stream(const void* buf, size_t bytes, int32_t blocks, void* sink,
+                               hipStream_t stream);
+
 /* Save the first n_pos positions of one request, all n_layers layers
  * (pools[l]: the layers' pools, one layout), to a file in one pass.  The
  * pages are read in place through block_table (device; the same IDs in

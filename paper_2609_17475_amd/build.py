@@ -20,7 +20,7 @@ LIB = os.path.join(HERE, "libjfkv.so")
 ARCH = os.environ.get("JFKV_ARCH", "gfx950")
 
 SOURCES = ["jfkv_host.cpp", "quantize.hip", "decode.hip", "prefill.hip", "tq4.hip",
-           "tq4_decode.hip", "reconstruct.hip", "pages.hip"]
+           "tq4_decode.hip", "reconstruct.hip", "pages.hip", "calib.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]

@@ -873,6 +873,20 @@ jf_status jf_kv_page_bytes(const jf_kv_layout* layout, size_t* bytes) {
   return ok();
 }
 
+jf_status jf_calib_read_stream(const void* buf, size_t bytes, int32_t blocks, void* sink,
+                               hipStream_t stream) {
+  if (!buf || !sink) return fail(JF_ERR_INVALID, "NULL pointer");
+  if (bytes == 0 || bytes % 16) return fail(JF_ERR_INVALID, "bytes must be a positive multiple of 16");
+  if ((uintptr_t)buf & 15) return fail(JF_ERR_INVALID, "buf must be 16-byte aligned");
+  if ((uintptr_t)sink & 3) return fail(JF_ERR_INVALID, "sink must be 4-byte aligned");
+  if (blocks < 1 || blocks > 65535) return fail(JF_ERR_INVALID, "blocks must be 1 .. 65535");
+  if (!is_device_memory(buf) || !is_device_memory(sink))
+    return fail(JF_ERR_INVALID, "buf and sink must be device memory");
+  return device_status(jfkv::launch_read_stream(buf, bytes, blocks, static_cast<uint32_t*>(sink),
+                                                stream),
+                       "read_stream launch");
+}
+
 jf_status jf_kv_pack_pages(const jf_kv_layout* layout, const jf_kv_pool_ptrs* pool,
                            const int32_t* block_table, int32_t first, int32_t count, void* buf,
                            hipStream_t stream) {

@@ -102,4 +102,8 @@ hipError_t launch_tq4_decode(const jf_kv_layout& L, const void* k_words, const v
                              int32_t max_pages, const int32_t* seq_lens, float softmax_scale,
                              int32_t max_splits, void* ws, void* out, hipStream_t stream);
 
+// Read-rate calibration: one pass over bytes (a multiple of 16) of buf.
+hipError_t launch_read_stream(const void* buf, size_t bytes, int32_t blocks, uint32_t* sink,
+                              hipStream_t stream);
+
 }  // namespace jfkv

@@ -31,7 +31,7 @@ EXPORTS = [
     "jf_verify_attn_q4", "jf_decode_step_q4", "jf_decode_step_q4_static", "jf_prefill_attn_q4",
     "jf_reconstruct_q4", "jf_tq4_pool_bytes", "jf_tq4_encode_append", "jf_tq4_decode_attn",
     "jf_tq4_reconstruct", "jf_kv_page_bytes", "jf_kv_pack_pages", "jf_kv_unpack_pages",
-    "jf_snapshot_save", "jf_snapshot_restore",
+    "jf_snapshot_save", "jf_snapshot_restore", "jf_calib_read_stream",
 ]
 
 
@@ -95,6 +95,7 @@ def _load():
         "jf_kv_page_bytes": (st, [P, ctypes.POINTER(sz)]),
         "jf_kv_pack_pages": (st, [P, P, P, i32, i32, P, P]),
         "jf_kv_unpack_pages": (st, [P, P, P, i32, i32, P, P]),
+        "jf_calib_read_stream": (st, [P, sz, i32, P, P]),
         "jf_snapshot_save": (st, [ctypes.c_char_p, P, P, i32, P, P, i32, i32, P, P, sz, P]),
         "jf_snapshot_restore": (st, [ctypes.c_char_p, P, P, i32, P, P, i32, P, P, sz, pi32, P]),
         "jf_tq4_pool_bytes": (st, [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]),
@@ -657,6 +658,16 @@ def kv_page_bytes(lay: Layout) -> int:
     n = ctypes.c_size_t()
     _check(lib.jf_kv_page_bytes(ctypes.byref(lay), ctypes.byref(n)))
     return n.value
+
+
+def jf_calib_read_stream(buf, blocks: int, sink, stream=None):
+    """One read of buf (device, 16-byte multiple) with the kernels' load type
+    (read-rate calibration)."""
+    import torch
+    if not buf.is_cuda or not sink.is_cuda or buf.numel() * buf.element_size() % 16:
+        raise ValueError("buf and sink must be device tensors, buf a multiple of 16 bytes")
+    _check(lib.jf_calib_read_stream(_ptr(buf), buf.numel() * buf.element_size(), int(blocks),
+                                    _ptr(sink), _stream(stream)))
 
 
 def jf_kv_pack_pages(pool: KVPool, block_table, first: int, count: int, buf, stream=None):

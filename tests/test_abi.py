@@ -152,6 +152,17 @@ def test_page_bytes_and_pack_validation():
                               None) == jfkv.JF_OK  # nothing to copy
 
 
+def test_read_calibration_validation():
+    L = jfkv.lib
+    assert L.jf_calib_read_stream(None, 4096, 256, 4096, None) == jfkv.JF_ERR_INVALID
+    assert L.jf_calib_read_stream(4096, 0, 256, 4096, None) == jfkv.JF_ERR_INVALID
+    assert L.jf_calib_read_stream(4096, 4100, 256, 4096, None) == jfkv.JF_ERR_INVALID
+    assert L.jf_calib_read_stream(4104, 4096, 256, 4096, None) == jfkv.JF_ERR_INVALID
+    assert L.jf_calib_read_stream(4096, 4096, 256, 4098, None) == jfkv.JF_ERR_INVALID
+    assert L.jf_calib_read_stream(4096, 4096, 0, 4096, None) == jfkv.JF_ERR_INVALID
+    assert L.jf_calib_read_stream(4096, 4096, 65536, 4096, None) == jfkv.JF_ERR_INVALID
+
+
 def test_snapshot_save_validation(tmp_path):
     lay = jfkv.layout(256, 8, 128, 64, 16)
     pools, host = _snap_args(lay)
