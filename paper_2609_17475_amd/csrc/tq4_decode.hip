@@ -56,6 +56,17 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Streaming loads of page data (non-temporal: read once per call).
+__device__ __forceinline__ uint4 ld_nt(const uint32_t* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 ld_nt2(const uint32_t* p) {
+  const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+  return make_uint2(v.x, v.y);
+}
 
 constexpr int kD = 256;           // head dimension of the format
 constexpr int kWordsPerVec = kD / 8;
@@ -207,15 +218,14 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int pos = 8 * (l16 >> 2) + 4 * t + (l16 & 3);
-      const uint4* src = reinterpret_cast<const uint4*>(k_words + (vec0 + pos) * kWordsPerVec + 8 * q4);
-      rb.k[t][0] = src[0];
-      rb.k[t][1] = src[1];
+      const uint32_t* src = k_words + (vec0 + pos) * kWordsPerVec + 8 * q4;
+      rb.k[t][0] = ld_nt(src);
+      rb.k[t][1] = ld_nt(src + 4);
     }
 #pragma unroll
-    for (int p = 0; p < 8; ++p)
-      rb.v[p] = *reinterpret_cast<const uint2*>(v_words + (vec0 + 8 * q4 + p) * kWordsPerVec + 2 * l16);
-    rb.kn = *reinterpret_cast<const uint4*>(k_norms + vec0 + 8 * q4);
-    rb.vn = *reinterpret_cast<const uint4*>(v_norms + vec0 + 8 * q4);
+    for (int p = 0; p < 8; ++p) rb.v[p] = ld_nt2(v_words + (vec0 + 8 * q4 + p) * kWordsPerVec + 2 * l16);
+    rb.kn = ld_nt(reinterpret_cast<const uint32_t*>(k_norms + vec0 + 8 * q4));
+    rb.vn = ld_nt(reinterpret_cast<const uint32_t*>(v_norms + vec0 + 8 * q4));
   };
 
   const uint32_t* tab = s_pair + (lane & 31);  // this lane's copy: its own bank

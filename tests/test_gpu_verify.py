@@ -62,6 +62,8 @@ def verify_gpu(case, q, max_splits=64, scale=1.0, lens=None, ws=None):
     (64, 4, 24, 256, 64, (600,), 3),       # 24 q / 4 KV heads, d = 256
     (128, 2, 2, 128, 128, (300,), 4),      # one query head per KV head
     (64, 2, 6, 128, 32, (500, 2), 3),      # a request shorter than Sq
+    (64, 1, 8, 128, 64, (700,), 3),        # 24 (head, token) pairs: chunks of 16 + 8
+    (64, 2, 8, 64, 64, (650,), 3),         # d = 64, 12 pairs: one block, two column sets
 ])
 def test_verify_matches_oracle(P, hkv, hq, d, G, lens, sq):
     log("verify P=%d hkv=%d hq=%d d=%d G=%d lens=%s sq=%d" % (P, hkv, hq, d, G, lens, sq))
