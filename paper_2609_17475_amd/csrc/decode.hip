@@ -22,11 +22,14 @@
 // nibble at bits 4..7: 16 c * 2^-24), which the matrix cores take exactly,
 // so one AND per pair of codes makes an operand; the scale and bias of each
 // group are applied to the fp32 results:
-//   scores  S^T[pos][col] = K codes [pos][dim] x Q' [dim][col], where column
-//           col = head + 4 * slot holds head "head" restricted to the dims
-//           of lane quarter "slot" (zero elsewhere), so every column belongs
-//           to one scale group; logit = sum over slots of
-//           (scale_g * S^T + bias_g * sum(q over the slot's dims)) * 2^24;
+//   scores  S^T[pos][col] = K codes [pos][dim] x Q' [dim][col]: the 16
+//           columns are head slots x column slots (col = head + H * slot, H
+//           head slots), column slot "slot" stands for scale group slot mod
+//           (groups per 128-dim half) of its head's half, and Q' holds that
+//           head's query restricted to the group's dims (zero elsewhere), so
+//           every column belongs to one scale group; logit = sum over the
+//           head's distinct groups of
+//           (scale_g * S^T + bias_g * sum(q over g's dims)) * 2^24;
 //   values  O^T[dim][col] += V codes [dim][pos] x W [pos][col] with
 //           W = p * scale_g (fp16) of the group that column's slot stands
 //           for, the codes again subnormal operands (16 code * 2^-24: a
@@ -447,13 +450,17 @@ __device__ void combine_splits(const float* ws, __half* out, int b, int Hq, int 
 }
 
 // Decode kernel.  Block = 8 (d <= 128) or 4 waves = one split of one
-// (request, KV head, chunk of up to 4 query heads).  Lane (m, q) =
+// (request, KV head, head chunk).  A chunk is CS column sets of H head slots
+// (H = head_slots(): 8 for 64- and 128-dim groups at d <= 128, 4 for 32-dim
+// groups or d = 256); the sets share every row's K and V operands and keep
+// their own softmax state and accumulators.  Lane (m, q) =
 // (lane % 16, lane / 16) feeds row m
 // and k-quarter q of the MFMA operands and receives column m, rows 4q..4q+3
 // of the 16x16 results.
 //   scores: tile t (0, 1) row m = position 8 (m / 4) + 4 t + m % 4 of the row,
 //           A = the lane's K quarter (dims q D/4 .. of each 128-dim half),
-//           B = Q' (column h + 4 s: head h, dims of quarter s only);
+//           B = Q' of the set (column h + H s: head h, dims of the scale
+//           group slot s stands for only);
 //           result lane (col, q), element i = position 8 q + 4 t + i;
 //   values: tile (c, k) row m = dim 4 (16 c + m) + k, A = positions 8 q .. 8 q
 //           + 7 (the lane's four position pairs) of that dim, B = W of the
