@@ -971,7 +971,7 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
           if constexpr (NGH >= 4) a = row_ror_add<2 * kHeadSlots>(a);
           sc[cs][t][i] = a;  // (scaled by kfold in the exponent)
         }
-    if (!full) {
+    if (__builtin_expect(!full, 0)) {
       // (an empty volatile statement keeps this a branch: the compiler would
       // otherwise compute the masks as selects on every row)
       asm volatile("" ::: "memory");
