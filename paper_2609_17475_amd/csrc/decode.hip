@@ -957,6 +957,8 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     // ---- logits: fold each column's group scale and bias, sum the distinct
     // groups of the head (lanes l16 + kHeadSlots k of the 16-lane row: slots
     // gs and gs + NGH are copies, so log2(NGH) rotations suffice), scale
+    // (all folds first, then the rotations: a rotation reads a value two
+    // instructions after it was written at the earliest, so no wait states)
     float sc[CS][2][4];
 #pragma unroll
     for (int cs = 0; cs < CS; ++cs)
@@ -967,9 +969,16 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
           float a = 0.0f;
 #pragma unroll
           for (int e = 0; e < NHALF; ++e) a = fold_meta(kmw[e][t][i], sacc[cs][e][t][i], qs[cs][e], a);
-          if constexpr (NGH >= 2) a = row_ror_add<kHeadSlots>(a);
-          if constexpr (NGH >= 4) a = row_ror_add<2 * kHeadSlots>(a);
           sc[cs][t][i] = a;  // (scaled by kfold in the exponent)
+        }
+#pragma unroll
+    for (int cs = 0; cs < CS; ++cs)
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if constexpr (NGH >= 2) sc[cs][t][i] = row_ror_add<kHeadSlots>(sc[cs][t][i]);
+          if constexpr (NGH >= 4) sc[cs][t][i] = row_ror_add<2 * kHeadSlots>(sc[cs][t][i]);
         }
     if (__builtin_expect(!full, 0)) {
       // (an empty volatile statement keeps this a branch: the compiler would
