@@ -17,9 +17,12 @@
 // in the low half, c[e / 16] in the high half), shared by every query head of
 // the KV head: for keys the pair is directly an operand word (dims 2j, 2j + 1
 // of one position); for values two reads and a permute give one dim at two
-// positions.  The table is held 32 times, interleaved so that lane l reads
-// copy l % 32 from bank l % 32 (random entries would otherwise collide in
-// the LDS banks).  The centroids are rounded to fp16 once (relative error
+// positions.  The table is held 64 times, interleaved so that lane l reads
+// copy l from its own bank (random entries would otherwise collide in the LDS
+// banks), and 64 KiB-aligned, so that one byte permute of the index word
+// forms a lookup's address (the index byte is the address's second byte).
+// The table's 64 KiB hold q' before the page loop and the final rotation
+// after it.  The centroids are rounded to fp16 once (relative error
 // <= 2^-11); q' enters as an fp16 high part plus an fp16 low part.
 //
 // Matrix-core layout (v_mfma_f32_16x16x32_f16; lane (m, q4) = (lane % 16,
@@ -123,11 +126,14 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     const int32_t* __restrict__ block_tables, const int32_t* __restrict__ seq_lens,
     float* __restrict__ ws, uint32_t* __restrict__ tickets, __half* __restrict__ out, int Hq,
     int Hkv, int P, int NP, int max_pages, int max_splits, int split_cap, float scale_log2) {
-  __shared__ float s_x[kMaxCols * kD];                   // q' rotation; final rotation
+  // index byte -> fp16 centroids of its nibbles, 64 copies (the page loop);
+  // before and after the loop the same bytes hold q' and the final rotation
+  __shared__ __attribute__((aligned(65536))) uint32_t s_tab[256 * 64];
+  float* const s_x = reinterpret_cast<float*>(s_tab);     // [kMaxCols][kD]
+  static_assert(kMaxCols * kD <= 256 * 64, "q' fits the table's bytes");
   __shared__ float s_part[kParts][kMaxCols * (kD + 2)];  // per-wave partials (u, m, l)
   __shared__ h8 s_qop[8][2][64];                         // score B operands (q' high, low)
   __shared__ uint32_t s_ticket;
-  __shared__ uint32_t s_pair[256 * 32];  // index byte -> fp16 centroids of its nibbles, 32 copies
 
   const int split = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
   const int gq = Hq / Hkv;
@@ -149,15 +155,6 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   int pb, pe;
   split_range(n_pages, S, split, pb, pe);
   const int t_end = min(pe * P, L);
-
-  // pair table: entry e holds c[e & 15] (low half) and c[e >> 4] (high half),
-  // copy c at word 32 e + c
-  for (int e = tid; e < 256; e += kThreads) {
-    const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)centroids[e & 15]);
-    const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)centroids[e >> 4]);
-#pragma unroll
-    for (int c = 0; c < 32; ++c) s_pair[e * 32 + c] = lo | (hi << 16);
-  }
 
   // ---- q' = H S q / 16 per query head (a negative scale negates it)
   const float qsign = scale_log2 < 0.0f ? -1.0f : 1.0f;
@@ -187,7 +184,16 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     s_qop[kb][0][lane] = hi;
     s_qop[kb][1][lane] = lo;
   }
-  __syncthreads();  // s_x is reused by the final rotation
+  __syncthreads();  // q' is in the operands: its bytes become the table
+  // pair table: entry e holds c[e & 15] (low half) and c[e >> 4] (high half),
+  // copy c (0..63) at word 64 e + c
+  for (int i = tid; i < 256 * 64; i += kThreads) {
+    const int e = i >> 6;
+    const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)centroids[e & 15]);
+    const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)centroids[e >> 4]);
+    s_tab[i] = lo | (hi << 16);
+  }
+  __syncthreads();
   const float kfold = fmaxf(fabsf(scale_log2), 1e-30f);  // |scale| in log2 units
 
   // ---- this wave's rows: split rows wave, wave + kWaves, ...
@@ -228,7 +234,16 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
     rb.vn = ld_nt(reinterpret_cast<const uint32_t*>(v_norms + vec0 + 8 * q4));
   };
 
-  const uint32_t* tab = s_pair + (lane & 31);  // this lane's copy: its own bank
+  // Lane l reads copy l (its own bank): the LDS address of entry e is
+  // base + 256 e + 4 l with the table 64 KiB-aligned, i.e. the base's bytes
+  // 2..3, the index byte itself as byte 1 and 4 l as byte 0, which one byte
+  // permute assembles.
+  const uint32_t lane4 = (uint32_t)(uintptr_t)s_tab + 4u * (uint32_t)lane;
+  // (k, the byte of the word, is a constant once the loops are unrolled)
+  auto lookup = [&](uint32_t word, uint32_t k) {
+    const uint32_t a = __builtin_amdgcn_perm(word, lane4, 0x03020000u | ((4u + k) << 8));
+    return *reinterpret_cast<const __attribute__((address_space(3))) uint32_t*>(a);
+  };
   f32x4 acc_v[16];
 #pragma unroll
   for (int j = 0; j < 16; ++j) acc_v[j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -252,8 +267,7 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const uint32_t x = w[t][kb];
-        const u32x4 r = {tab[(x & 0xFFu) * 32], tab[((x >> 8) & 0xFFu) * 32],
-                         tab[((x >> 16) & 0xFFu) * 32], tab[(x >> 24) * 32]};
+        const u32x4 r = {lookup(x, 0), lookup(x, 1), lookup(x, 2), lookup(x, 3)};
         const h8 a = __builtin_bit_cast(h8, r);
         acc[t] = mfma(a, qh, acc[t]);
         acc[t] = mfma(a, ql, acc[t]);
@@ -316,7 +330,7 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
 #pragma unroll
       for (int p = 0; p < 8; ++p) {
         const uint32_t word = (bb < 4) ? rb.v[p].x : rb.v[p].y;
-        t[p] = tab[((word >> (8 * (bb & 3))) & 0xFFu) * 32];
+        t[p] = lookup(word, bb & 3);
       }
 #pragma unroll
       for (int hn = 0; hn < 2; ++hn) {  // low nibble: dim 16 m + 2 bb; high: + 1
