@@ -812,7 +812,15 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
 
   f32x4 acc_o[CS][NC][4];
   float m_run[CS], thr[CS], l_run[CS];
-  float bacc[CS][NHALF], sacc8[CS][NHALF];  // sums of p * bias and of p * scale - W (value groups)
+  // The value groups' sums of p * bias and of p * scale - W.  d <= 128: both
+  // from matrix-core products into acc_bs, whose A operand rows are group
+  // g's bias (row g H), its scale (row g H + 1, where a second product with
+  // A = -1 subtracts W in the same accumulator) and zeros elsewhere (H head
+  // slots: lanes g H .. hold group g's (scale, bias) words); d = 256: per-lane
+  // dot products.
+  constexpr bool kSumMfma = NHALF == 1;
+  f32x4 acc_bs[CS];
+  float bacc[CS][NHALF], sacc8[CS][NHALF];
 #pragma unroll
   for (int cs = 0; cs < CS; ++cs) {
 #pragma unroll
@@ -821,9 +829,15 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
       for (int k = 0; k < 4; ++k) acc_o[cs][c][k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     m_run[cs] = thr[cs] = kMinit;
     l_run[cs] = 0.0f;
+    acc_bs[cs] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int e = 0; e < NHALF; ++e) bacc[cs][e] = sacc8[cs][e] = 0.0f;
   }
+  const int s_grp = l16 / kHeadSlots, s_row = l16 % kHeadSlots;  // the lane's sum row role
+  const bool s_bias = s_grp < NGH && s_row == 0, s_scale = s_grp < NGH && s_row == 1;
+  const uint32_t s_sel = s_bias ? 0x07060302u : s_scale ? 0x05040100u : 0x0C0C0C0Cu;
+  const _Float16 s_neg = s_scale ? (_Float16)-1.0f : (_Float16)0.0f;
+  const h8 s_aw = {s_neg, s_neg, s_neg, s_neg, s_neg, s_neg, s_neg, s_neg};
 
   // LDS read bases (stage 0)
   const int p0 = 8 * (l16 >> 2) + (l16 & 3);  // tile-0 position of row m = l16
@@ -1011,10 +1025,14 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
           m_run[cs] = M;
           thr[cs] = M + kTau;
           l_run[cs] *= alpha;
+          if constexpr (kSumMfma) {
+            acc_bs[cs] *= alpha;
+          } else {
 #pragma unroll
-          for (int e = 0; e < NHALF; ++e) {
-            bacc[cs][e] *= alpha;
-            sacc8[cs][e] *= alpha;
+            for (int e = 0; e < NHALF; ++e) {
+              bacc[cs][e] *= alpha;
+              sacc8[cs][e] *= alpha;
+            }
           }
 #pragma unroll
           for (int c = 0; c < NC; ++c)
@@ -1038,14 +1056,32 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
           const int t = r >> 1, i = 2 * (r & 1);
           const uint32_t a = vmw[e][t][i], c = vmw[e][t][i + 1];
           const h2 sv = as_h2(__builtin_amdgcn_perm(c, a, 0x05040100u));
-          const h2 bv = as_h2(__builtin_amdgcn_perm(c, a, 0x07060302u));
           const h2 w = pk[r] * sv;
           W[cs][e][2 * r] = w.x;
           W[cs][e][2 * r + 1] = w.y;
-          bacc[cs][e] = __builtin_amdgcn_fdot2(pk[r], bv, bacc[cs][e], false);
-          sacc8[cs][e] = __builtin_amdgcn_fdot2(pk[r], sv, sacc8[cs][e], false);
-          sacc8[cs][e] = __builtin_amdgcn_fdot2(w, mones, sacc8[cs][e], false);
+          if constexpr (!kSumMfma) {
+            const h2 bv = as_h2(__builtin_amdgcn_perm(c, a, 0x07060302u));
+            bacc[cs][e] = __builtin_amdgcn_fdot2(pk[r], bv, bacc[cs][e], false);
+            sacc8[cs][e] = __builtin_amdgcn_fdot2(pk[r], sv, sacc8[cs][e], false);
+            sacc8[cs][e] = __builtin_amdgcn_fdot2(w, mones, sacc8[cs][e], false);
+          }
         }
+      }
+      if constexpr (kSumMfma) {
+        // rows of bias and scale (positions in the k-slot order of p), then
+        // -W into the scale rows
+        u32x4 am;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = r >> 1, i = 2 * (r & 1);
+          am[r] = __builtin_amdgcn_perm(vmw[0][t][i + 1], vmw[0][t][i], s_sel);
+        }
+        const h8 pb = __builtin_bit_cast(h8, u32x4{__builtin_bit_cast(uint32_t, pk[0]),
+                                                   __builtin_bit_cast(uint32_t, pk[1]),
+                                                   __builtin_bit_cast(uint32_t, pk[2]),
+                                                   __builtin_bit_cast(uint32_t, pk[3])});
+        acc_bs[cs] = mfma(__builtin_bit_cast(h8, am), pb, acc_bs[cs]);
+        acc_bs[cs] = mfma(s_aw, W[cs][0], acc_bs[cs]);
       }
     }
     // ---- values: O^T += V codes x W, dims 4 (16 c + m) + k (the V
@@ -1090,17 +1126,26 @@ __global__ __launch_bounds__(kMaxThreads) void decode_kernel(
     const int hse = me % kHeadSlots, gse = me / kHeadSlots;
 #pragma unroll
     for (int cs = 0; cs < CS; ++cs) {
+      // the value groups' sums of p * (bias + 8 scale) - 8 W: the bias part
+      // of the value and the centring of the codes
       float bsum[NHALF];
+      if constexpr (kSumMfma) {
+        // column me's group g: rows g H (element 0) and g H + 1 (element 1)
+        // of acc_bs, held by lane me + 16 (g H / 4)
+        const int src = me + 16 * ((((me / kHeadSlots) % NGH) * kHeadSlots) / 4);
+        const float bq = __shfl(acc_bs[cs][0], src);
+        const float sq8 = __shfl(acc_bs[cs][1], src);
+        bsum[0] = fmaf(8.0f, sq8, bq);
+      } else {
 #pragma unroll
-      for (int e = 0; e < NHALF; ++e) {
-        // the value groups' sums of p * (bias + 8 scale) - 8 W: the bias part
-        // of the value and the centring of the codes (sacc8 holds
-        // sum (p * scale - W))
-        float bq = bacc[cs][e] + __shfl_xor(bacc[cs][e], 16);
-        bq += __shfl_xor(bq, 32);
-        float sq8 = sacc8[cs][e] + __shfl_xor(sacc8[cs][e], 16);
-        sq8 += __shfl_xor(sq8, 32);
-        bsum[e] = fmaf(8.0f, sq8, bq);
+        for (int e = 0; e < NHALF; ++e) {
+          // (sacc8 holds sum (p * scale - W))
+          float bq = bacc[cs][e] + __shfl_xor(bacc[cs][e], 16);
+          bq += __shfl_xor(bq, 32);
+          float sq8 = sacc8[cs][e] + __shfl_xor(sacc8[cs][e], 16);
+          sq8 += __shfl_xor(sq8, 32);
+          bsum[e] = fmaf(8.0f, sq8, bq);
+        }
       }
       float lsum = l_run[cs] + __shfl_xor(l_run[cs], 16);
       lsum += __shfl_xor(lsum, 32);
