@@ -34,7 +34,7 @@
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kIters = 4;  // 16-byte code loads in flight per lane
+constexpr int kIters = 2;  // 16-byte code loads in flight per lane (4: 5 % slower, 8: 10 %)
 
 // fp16 of s * q + b rounded once, via fp32 rounded to odd (see above).
 __device__ __forceinline__ float to_odd(float s, float q, float b) {
