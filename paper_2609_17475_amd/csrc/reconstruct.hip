@@ -21,9 +21,13 @@
 //
 // Work: a lane reads 16 bytes of codes (32 elements) of one position (K) or
 // of a pair of positions (V, stored position-paired) and their groups'
-// (scale, bias) words, and writes the fp16 values as 16-byte stores, so a
-// wave reads consecutive positions' codes as one contiguous run and writes
-// their operands contiguously.  Each lane keeps kIters loads in flight.
+// (scale, bias) words, so a wave reads consecutive positions' codes as one
+// contiguous run; each lane keeps kIters loads in flight.  The fp16 values
+// of a wave's load pass (2,048 elements, 4 KiB) go through
+// the wave's rows in LDS and leave as 16-byte stores of whole positions, so
+// each store instruction writes 1 KiB contiguously (stored straight from the
+// lanes that made them, each instruction touched a quarter of every
+// position's row, and the kernel took 40 % longer).
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -102,7 +106,7 @@ template <int D, int G, bool V>
 __device__ __forceinline__ void reconstruct_body(
     const uint4* __restrict__ codes, const uint32_t* __restrict__ meta,
     const int32_t* __restrict__ table, int n, int kv0, int Hkv, int P, int NP,
-    uint4* __restrict__ out) {
+    uint4* __restrict__ out, uint4* __restrict__ xs) {
   constexpr int LPU = V ? D / 16 : D / 32;  // lanes per unit (a position, or a pair)
   constexpr int UPW = 64 / LPU;             // units per wave and load
   constexpr int PER = V ? 2 : 1;            // positions per unit
@@ -110,6 +114,9 @@ __device__ __forceinline__ void reconstruct_body(
   constexpr int NG = D / G;                 // groups per position
   constexpr int CPP = D / 8;                // 16-byte output chunks per position
   static_assert(G >= EPL, "a lane's elements lie in one group");
+  constexpr int NPOS = UPW * PER;  // positions per load pass
+  constexpr int PITCH = CPP + 1;   // 16-byte chunks per LDS row (one of padding)
+  static_assert(NPOS * CPP == 256 && NPOS * PITCH == 256 + 2048 / D, "four 16-byte chunks per lane and pass");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int j = blockIdx.y;  // head within the group
@@ -137,7 +144,6 @@ __device__ __forceinline__ void reconstruct_body(
   }
 #pragma unroll
   for (int i = 0; i < kIters; ++i) {
-    const int t = PER * (u0 + i * UPW);
     uint32_t w[PER][EPL / 8];  // K-order code words per position
     if constexpr (V) {
       const uint32_t a[4] = {cw[i].x, cw[i].y, cw[i].z, cw[i].w};
@@ -149,17 +155,26 @@ __device__ __forceinline__ void reconstruct_body(
     } else {
       w[0][0] = cw[i].x; w[0][1] = cw[i].y; w[0][2] = cw[i].z; w[0][3] = cw[i].w;
     }
+    // the pass's outputs (NPOS consecutive positions) through the wave's
+    // LDS rows, so that each store covers whole positions: 1 KiB contiguous
+    // per store instruction
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
-      uint4 o[EPL / 8];
 #pragma unroll
-      for (int h = 0; h < EPL / 8; ++h) o[h] = emit8(w[e][h], mw[i][e]);
-      if (t + e < n) {
-        uint4* dst = out + ((size_t)j * n + t + e) * CPP + (EPL / 8) * c;
-#pragma unroll
-        for (int h = 0; h < EPL / 8; ++h) dst[h] = o[h];
-      }
+      for (int h = 0; h < EPL / 8; ++h)
+        xs[(PER * (lane / LPU) + e) * PITCH + (EPL / 8) * c + h] = emit8(w[e][h], mw[i][e]);
     }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    const int tb = PER * ((blockIdx.x * kWaves + wave) * kIters * UPW + i * UPW);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int q = lane + 64 * s, pos = q / CPP, ch = q % CPP;
+      const uint4 val = xs[pos * PITCH + ch];
+      if (tb + pos < n) out[((size_t)j * n + tb + pos) * CPP + ch] = val;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -170,10 +185,12 @@ __global__ __launch_bounds__(64 * kWaves) void reconstruct_kernel(
     const uint4* __restrict__ v_codes, const uint32_t* __restrict__ v_meta,
     const int32_t* __restrict__ table, int n, int kv0, int Hkv, int P, int NP,
     uint4* __restrict__ k_out, uint4* __restrict__ v_out) {
+  __shared__ uint4 xs[kWaves][256 + 2048 / D];  // 2048 / D rows of D / 8 + 1 chunks per wave
+  uint4* const xw = xs[threadIdx.x >> 6];
   if (blockIdx.z == 0)
-    reconstruct_body<D, G, false>(k_codes, k_meta, table, n, kv0, Hkv, P, NP, k_out);
+    reconstruct_body<D, G, false>(k_codes, k_meta, table, n, kv0, Hkv, P, NP, k_out, xw);
   else
-    reconstruct_body<D, G, true>(v_codes, v_meta, table, n, kv0, Hkv, P, NP, v_out);
+    reconstruct_body<D, G, true>(v_codes, v_meta, table, n, kv0, Hkv, P, NP, v_out, xw);
 }
 
 template <int D, int G>
