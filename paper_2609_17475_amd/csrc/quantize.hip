@@ -222,7 +222,7 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
     for (int i = 0; i < 8; ++i)
       *reinterpret_cast<u32x4*>(&stage[wib][i][16 * lane]) = nx[i];
     const Dest cd = nd;
-    const uint32_t ckv = kv, crest = rest;
+    const uint32_t ckv = kv, crest = rest;  // this tile's (kv and rest move on to the next)
     const bool more = (uint64_t)t + Wn < (uint64_t)n_tiles;
     if (more) {
       t += Wn;
@@ -397,7 +397,7 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
     }
     if (valid) {
 
-    const int64_t ph = (int64_t)page * Hkv + kv;  // (page, KV head) block
+    const int64_t ph = (int64_t)page * Hkv + ckv;  // (page, KV head) block
     if (kind == 0) {
       uint4* dst = reinterpret_cast<uint4*>(k_codes + (ph * P + slot) * (D / 2) + 32 * part);
       dst[0] = make_uint4(cw[0], cw[1], cw[2], cw[3]);

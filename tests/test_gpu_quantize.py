@@ -19,6 +19,11 @@ from paper_2609_17475_amd import jfkv  # noqa: E402
     (128, 4, 256, 64, (390,), 0),
     (64, 3, 128, 128, (65, 64, 1), 0),
     (256, 2, 256, 32, (257, 300), 256),
+    # more row tiles (938 x 2 x 3 of 64 rows) than waves in the persistent
+    # grid (4 x 4 waves per CU), with a KV-head count that does not divide
+    # the grid: waves move to another KV head between tiles, and each tile
+    # must be stored under its own
+    (64, 3, 64, 32, (60000,), 0),
 ])
 def test_pool_bytes_bit_exact(P, hkv, d, G, lens, prefix):
     log("quantize P=%d hkv=%d d=%d G=%d lens=%s prefix=%d" % (P, hkv, d, G, lens, prefix))
