@@ -60,6 +60,16 @@ typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Device-coherent (sc1) buffer loads of one head's split records (256
+// values, then m and l); the resource covers that head's max_splits records,
+// so the hardware also bounds-checks every access.
+constexpr int kCpolSc1 = 16;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t head_records(const float* base, int max_splits) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0,
+                                           max_splits * (256 + 4) * 4, 0x00020000);
+}
 
 // Streaming loads of page data (non-temporal: read once per call).
 __device__ __forceinline__ uint4 ld_nt(const uint32_t* p) {
@@ -416,17 +426,23 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
 
   // ---- the last split of (request, KV head) to finish combines them all
   // (log-sum-exp over the splits, in the rotated space), then rotates back.
-  // Ordering: record stores, then the ticket increment (acq_rel, device
-  // scope); the last block takes a device-scope acquire fence before it
-  // reads the records (with ordinary loads, so the release and acquire are
-  // needed here).
+  // Ordering: every word the blocks exchange is accessed with device-scope
+  // atomic instructions on both sides: the records are written by
+  // agent-scope atomic stores (global_store sc1, written through to the
+  // device-coherent level) and read by device-coherent loads (buffer_load
+  // sc1).  Each thread waits until its record stores have completed before
+  // the barrier that precedes the ticket increment, a device-scope atomic;
+  // the combining block issues its record loads only after it has seen the
+  // last ticket.  A release/acquire pair would add an L2 write-back before
+  // the increment and an invalidation after it, which matter only for data
+  // exchanged without device-scope atomics (there is none).
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's records are stored
   __syncthreads();
   uint32_t* ticket = tickets + (size_t)b * Hkv + kv;
   if (tid == 0)
-    s_ticket = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    s_ticket = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (s_ticket != (uint32_t)(S - 1)) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   if (tid == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   // split weights w_s = l_s 2^(m_s - M) (M the largest m_s of a non-empty
   // split) and their sum, one wave per head, lanes over the splits; kept in
@@ -436,14 +452,14 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   float* s_den = s_part[0] + kMaxCols * kMaxSplits;  // [gq]
   static_assert(kMaxCols * kMaxSplits + kMaxCols <= kMaxCols * (kD + 2), "weights fit");
   for (int h = wave; h < gq; h += kWaves) {
-    const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (kD + 4);
+    const auto rs = head_records(ws + ((size_t)b * Hq + h0 + h) * max_splits * (kD + 4), max_splits);
     float mv[kMaxSplits / 64], lv[kMaxSplits / 64];
     float M = -INFINITY;
 #pragma unroll
     for (int j = 0; j < kMaxSplits / 64; ++j) {
       const int s = lane + 64 * j;
-      const float2 ml = s < S ? *reinterpret_cast<const float2*>(recs + (size_t)s * (kD + 4) + kD)
-                              : make_float2(0.0f, 0.0f);
+      const f32x2 ml = s < S ? __builtin_amdgcn_raw_buffer_load_b64(rs, (s * (kD + 4) + kD) * 4, 0, kCpolSc1)
+                             : f32x2{0.0f, 0.0f};
       mv[j] = ml.y > 0.0f ? ml.x : -INFINITY;
       lv[j] = ml.y;
       M = fmaxf(M, mv[j]);
@@ -470,14 +486,14 @@ __global__ __launch_bounds__(kThreads) void tq4_decode_kernel(
   for (int task = wave; task < 2 * gq; task += kWaves) {
     const int h = task >> 1, k = lane >> 5;
     const int d0 = (kD / 2) * (task & 1) + 4 * (lane & 31);
-    const float* recs = ws + ((size_t)b * Hq + h0 + h) * max_splits * (kD + 4) + d0;
+    const auto rs = head_records(ws + ((size_t)b * Hq + h0 + h) * max_splits * (kD + 4), max_splits);
     float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     for (int s0 = k; s0 < S; s0 += 2 * kCh) {
-      float4 o[kCh];
+      f32x4 o[kCh];
 #pragma unroll
       for (int i = 0; i < kCh; ++i) {  // past the end: a valid record, weight 0
         const int s = min(s0 + 2 * i, S - 1);
-        o[i] = *reinterpret_cast<const float4*>(recs + (size_t)s * (kD + 4));
+        o[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, (s * (kD + 4) + d0) * 4, 0, kCpolSc1);
       }
 #pragma unroll
       for (int i = 0; i < kCh; ++i) {
